@@ -1,0 +1,110 @@
+"""CPU oracle package (test infrastructure only).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package. The product library never imports it
+and shares no code with it.
+
+* ``semsched_oracle``: the pure-Python oracle (the plain definition).
+* ``c_oracle_*``: ctypes wrappers of ``oracle.c``, the same definition in
+  plain C for large queues and for the timed CPU baseline.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+from .semsched_oracle import (  # noqa: F401
+    MAX_CLASSES,
+    OracleRangeError,
+    schedule_batched,
+    schedule_queue,
+)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+ORACLE_OK = 0
+ORACLE_EINVAL = -1
+ORACLE_ERANGE = -2
+
+
+def build_c_oracle() -> str:
+    """Compile oracle.c into liboracle.so (plain gcc, single-threaded)."""
+    tmp = _LIB + ".tmp"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC",
+                           "-o", tmp, _SRC])
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        build_c_oracle()
+    lib = ctypes.CDLL(_LIB)
+    vp = ctypes.c_void_p
+    i64 = ctypes.c_int64
+    lib.oracle_schedule.argtypes = [vp, vp, i64, vp, vp, vp, vp]
+    lib.oracle_schedule.restype = ctypes.c_int
+    lib.oracle_schedule_batched.argtypes = [vp, vp, vp, i64, ctypes.c_int32,
+                                            vp, vp, vp, vp]
+    lib.oracle_schedule_batched.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _join128(lo: np.ndarray, hi: np.ndarray) -> list:
+    return [int(h) << 64 | int(l) for l, h in zip(lo.tolist(), hi.tolist())]
+
+
+def c_oracle_queue(p: np.ndarray, l: np.ndarray):
+    """Single queue through oracle.c: (order i32, wait i64, totals[257] ints)."""
+    p = np.ascontiguousarray(p, dtype=np.uint8)
+    l = np.ascontiguousarray(l, dtype=np.int32)
+    n = p.shape[0]
+    order = np.empty(n, np.int32)
+    wait = np.empty(n, np.int64)
+    lo = np.zeros(257, np.uint64)
+    hi = np.zeros(257, np.uint64)
+    rc = _load().oracle_schedule(_ptr(p), _ptr(l), n, _ptr(order), _ptr(wait),
+                                 _ptr(lo), _ptr(hi))
+    if rc == ORACLE_ERANGE:
+        raise OracleRangeError("length < 0 or priority out of range")
+    if rc != ORACLE_OK:
+        raise ValueError(f"oracle_schedule failed: {rc}")
+    return order, wait, _join128(lo, hi)
+
+
+def c_oracle_batched(p: np.ndarray, l: np.ndarray, offsets: np.ndarray,
+                     num_classes: int):
+    """Batched queues through oracle.c; totals are S*(1+C) Python ints."""
+    p = np.ascontiguousarray(p, dtype=np.uint8)
+    l = np.ascontiguousarray(l, dtype=np.int32)
+    offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+    n = p.shape[0]
+    s = offsets.shape[0] - 1
+    order = np.empty(n, np.int32)
+    wait = np.empty(n, np.int64)
+    lo = np.zeros(max(1, s * (1 + num_classes)), np.uint64)
+    hi = np.zeros_like(lo)
+    rc = _load().oracle_schedule_batched(_ptr(p), _ptr(l), _ptr(offsets), s,
+                                         num_classes, _ptr(order), _ptr(wait),
+                                         _ptr(lo), _ptr(hi))
+    if rc == ORACLE_ERANGE:
+        raise OracleRangeError("length < 0 or priority out of range")
+    if rc != ORACLE_OK:
+        raise ValueError(f"oracle_schedule_batched failed: {rc}")
+    return order, wait, _join128(lo[: s * (1 + num_classes)],
+                                 hi[: s * (1 + num_classes)])

@@ -1,0 +1,140 @@
+/*
+ * CPU oracle for the semantic-scheduling hot path (plain C).
+ *
+ * TEST INFRASTRUCTURE ONLY. Nothing in the product path may link or call
+ * this file: only the tests, the smoke check and the benchmark's CPU
+ * baseline load it. It shares no code, header or table with the HIP library.
+ *
+ * The computation is the plain definition, the same as the pure-Python
+ * oracle (semsched_oracle.py), written for speed on large queues:
+ *
+ *   1. order: ids ascending by (rank p, predicted length l, id), i.e. the
+ *      drained min-heap keyed by the priority tuple (f_e, f_t) of
+ *      Algorithm 1 (MinHeap Construction); the id breaks exact ties
+ *      (the paper gives no tie rule).
+ *   2. wait[0] = 0, wait[k] = wait[k-1] + l[order[k-1]]  (exclusive prefix of
+ *      service times ahead of each request; Eq. 1 with equal arrivals).
+ *   3. totals[0] = sum of waits; totals[1+c] = sum over requests of class c.
+ *      Exact 128-bit (unsigned __int128), split into lo/hi words.
+ *
+ * The sort is a top-down merge sort on (p, l, id) records. Because the
+ * comparison covers the id, the order is total and any correct sort gives
+ * the same permutation.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+#define ORACLE_ERANGE (-2)
+#define ORACLE_ENOMEM (-3)
+
+typedef struct {
+  int32_t len;
+  int32_t id;
+  uint8_t pri;
+} rec_t;
+
+static int rec_less(const rec_t *a, const rec_t *b) {
+  if (a->pri != b->pri) return a->pri < b->pri;
+  if (a->len != b->len) return a->len < b->len;
+  return a->id < b->id;
+}
+
+static void merge_sort(rec_t *a, rec_t *tmp, int64_t n) {
+  if (n < 2) return;
+  int64_t h = n / 2;
+  merge_sort(a, tmp, h);
+  merge_sort(a + h, tmp, n - h);
+  int64_t i = 0, j = h, k = 0;
+  while (i < h && j < n) {
+    if (rec_less(&a[j], &a[i]))
+      tmp[k++] = a[j++];
+    else
+      tmp[k++] = a[i++];
+  }
+  while (i < h) tmp[k++] = a[i++];
+  while (j < n) tmp[k++] = a[j++];
+  memcpy(a, tmp, (size_t)n * sizeof(rec_t));
+}
+
+/* One queue. totals_lo/hi have 1 + num_classes entries. */
+static int schedule_one(const uint8_t *pri, const int32_t *len, int64_t n,
+                        int32_t num_classes, int32_t *order, int64_t *wait,
+                        uint64_t *totals_lo, uint64_t *totals_hi,
+                        rec_t *recs, rec_t *tmp) {
+  for (int64_t i = 0; i < n; ++i) {
+    if (len[i] < 0 || (int32_t)pri[i] >= num_classes) return ORACLE_ERANGE;
+    recs[i].pri = pri[i];
+    recs[i].len = len[i];
+    recs[i].id = (int32_t)i;
+  }
+  merge_sort(recs, tmp, n);
+
+  unsigned __int128 tot[257];
+  for (int c = 0; c <= num_classes; ++c) tot[c] = 0;
+  int64_t running = 0;
+  for (int64_t k = 0; k < n; ++k) {
+    order[k] = recs[k].id;
+    wait[k] = running;
+    tot[0] += (unsigned __int128)(uint64_t)running;
+    tot[1 + recs[k].pri] += (unsigned __int128)(uint64_t)running;
+    running += recs[k].len;
+  }
+  for (int c = 0; c <= num_classes; ++c) {
+    totals_lo[c] = (uint64_t)tot[c];
+    totals_hi[c] = (uint64_t)(tot[c] >> 64);
+  }
+  return ORACLE_OK;
+}
+
+int oracle_schedule(const uint8_t *pri, const int32_t *len, int64_t n,
+                    int32_t *order, int64_t *wait, uint64_t *totals_lo,
+                    uint64_t *totals_hi) {
+  if (n < 0 || n > INT32_MAX) return ORACLE_EINVAL;
+  rec_t *recs = (rec_t *)malloc((size_t)(n ? n : 1) * sizeof(rec_t));
+  rec_t *tmp = (rec_t *)malloc((size_t)(n ? n : 1) * sizeof(rec_t));
+  if (!recs || !tmp) {
+    free(recs);
+    free(tmp);
+    return ORACLE_ENOMEM;
+  }
+  int rc = schedule_one(pri, len, n, 256, order, wait, totals_lo, totals_hi,
+                        recs, tmp);
+  free(recs);
+  free(tmp);
+  return rc;
+}
+
+int oracle_schedule_batched(const uint8_t *pri, const int32_t *len,
+                            const int64_t *offsets, int64_t num_segments,
+                            int32_t num_classes, int32_t *order, int64_t *wait,
+                            uint64_t *totals_lo, uint64_t *totals_hi) {
+  if (num_segments < 0 || num_classes < 1 || num_classes > 256)
+    return ORACLE_EINVAL;
+  if (offsets[0] != 0) return ORACLE_EINVAL;
+  int64_t biggest = 0;
+  for (int64_t s = 0; s < num_segments; ++s) {
+    int64_t m = offsets[s + 1] - offsets[s];
+    if (m < 0 || m > INT32_MAX) return ORACLE_EINVAL;
+    if (m > biggest) biggest = m;
+  }
+  rec_t *recs = (rec_t *)malloc((size_t)(biggest ? biggest : 1) * sizeof(rec_t));
+  rec_t *tmp = (rec_t *)malloc((size_t)(biggest ? biggest : 1) * sizeof(rec_t));
+  if (!recs || !tmp) {
+    free(recs);
+    free(tmp);
+    return ORACLE_ENOMEM;
+  }
+  int rc = ORACLE_OK;
+  const int64_t stride = 1 + num_classes;
+  for (int64_t s = 0; s < num_segments && rc == ORACLE_OK; ++s) {
+    int64_t a = offsets[s], m = offsets[s + 1] - offsets[s];
+    rc = schedule_one(pri + a, len + a, m, num_classes, order + a, wait + a,
+                      totals_lo + s * stride, totals_hi + s * stride, recs, tmp);
+  }
+  free(recs);
+  free(tmp);
+  return rc;
+}
