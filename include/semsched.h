@@ -1,0 +1,172 @@
+/*
+ * semsched.h — C ABI of the MI355X (gfx950) semantic-scheduling hot path.
+ *
+ * What the library computes (the paper's Section 3.2 problem statement with
+ * all arrivals at time 0 and one server, and Section 3.3's priority tuple):
+ *
+ *   Each request i has an urgency rank priority[i] (Definition 1: the graded
+ *   poset's rank, 0 = most urgent ESI level) and a predicted service time
+ *   length[i] (the estimated remaining computation time f_t, here the
+ *   predicted generation length in tokens).
+ *
+ *   order  : request ids ascending by (priority, length, id). This is the
+ *            sequence obtained by draining the min-heap keyed by (f_e, f_t)
+ *            of Algorithm 1 (MinHeap Construction); under Eq. 2 (relative
+ *            constraint) it minimises the total waiting time of Eq. 1. Exact
+ *            (priority, length) ties go to the lower id (the paper gives no
+ *            tie rule; this one makes the schedule unique).
+ *   wait   : wait[k] = sum of length[order[j]] for j < k, int64, in schedule
+ *            order (wait[k] belongs to request order[k]). It is the time
+ *            before service starts; Eq. 1's finish-minus-arrival is
+ *            wait[k] + length[order[k]].
+ *   totals : totals[0] = sum of all waits; totals[1 + c] = sum of the waits
+ *            of class c (zero for an empty class). Exact signed 128-bit.
+ *
+ * Memory: every array argument is a DEVICE pointer (e.g. a torch ROCm
+ * tensor's data_ptr()) on the current HIP device, except where noted. Inputs
+ * are read only. Outputs are caller-owned and fully overwritten; after a
+ * failed call their contents are unspecified.
+ *
+ * Streams: `stream` arguments are a hipStream_t passed as void * (NULL = the
+ * null stream). The blocking calls run on the stream set by sem_set_stream
+ * and synchronise it before returning.
+ *
+ * Errors (return values):
+ *   SEM_OK       success.
+ *   SEM_EINVAL   null pointer with n > 0, n < 0 or n > INT32_MAX,
+ *                num_classes outside [1, 256], offsets not starting at 0,
+ *                decreasing, or not ending at the total, workspace too small.
+ *   SEM_ERANGE   some length < 0, or some priority >= num_classes (256 for
+ *                the single-queue calls). Detected on the device.
+ *   SEM_ENOMEM   the library could not allocate its internal workspace.
+ *   SEM_EDEVICE  a HIP runtime call failed.
+ *   SEM_ENOTIMPL the asynchronous batched call was given a queue longer than
+ *                SEM_SEGMENT_CAP (the blocking call handles any length).
+ */
+#ifndef SEMSCHED_H
+#define SEMSCHED_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Exact signed 128-bit integer, two's complement, little-endian words:
+ * value = hi * 2^64 + lo. Same layout as __int128 on x86-64 and gfx950. */
+typedef struct {
+  uint64_t lo;
+  int64_t hi;
+} sem_i128;
+
+#define SEM_MAX_CLASSES 256 /* priority is uint8 */
+#define SEM_SEGMENT_CAP 16384 /* longest queue scheduled inside one workgroup's LDS */
+
+enum {
+  SEM_OK = 0,
+  SEM_EINVAL = -1,
+  SEM_ERANGE = -2,
+  SEM_ENOMEM = -3,
+  SEM_EDEVICE = -4,
+  SEM_ENOTIMPL = -5
+};
+
+/*
+ * Schedule one queue of n requests (blocking).
+ *   priority  [n] uint8, rank of each request (0 = most urgent).
+ *   length    [n] int32, predicted service time, must be >= 0.
+ *   order_out [n] int32, ids in schedule order.
+ *   wait_out  [n] int64, wait of the request at each schedule position.
+ *   totals_out[1 + 256] sem_i128, total then per-class waits.
+ * Uses a workspace cached by the library (allocated on first need, grown as
+ * needed, freed at process exit). n = 0 is valid and zeroes totals_out.
+ */
+int sem_schedule(const uint8_t *priority, const int32_t *length, int64_t n,
+                 int32_t *order_out, int64_t *wait_out, sem_i128 *totals_out);
+
+/*
+ * Schedule num_segments independent queues laid out back to back (blocking).
+ *   offsets   [num_segments + 1] int64, DEVICE pointer; queue s holds
+ *             requests offsets[s] .. offsets[s+1]-1. Empty queues are valid.
+ *   order_out [N] int32, ids LOCAL to each queue (0-based arrival index),
+ *             queue s's schedule written at offsets[s] + k.
+ *   wait_out  [N] int64, same layout; waits restart at 0 in every queue.
+ *   totals_out[num_segments * (1 + num_classes)] sem_i128, queue-major:
+ *             queue s's total at s*(1+num_classes), class c at +1+c.
+ * Queues up to SEM_SEGMENT_CAP requests are scheduled one per workgroup in
+ * LDS; longer queues go through the multi-pass global path one at a time.
+ * The call copies offsets to the host once to plan the launches.
+ */
+int sem_schedule_batched(const uint8_t *priority, const int32_t *length,
+                         const int64_t *offsets, int64_t num_segments,
+                         int32_t num_classes, int32_t *order_out,
+                         int64_t *wait_out, sem_i128 *totals_out);
+
+/*
+ * Workspace size in bytes needed by the asynchronous calls for n requests
+ * in num_segments queues (num_segments = 1 for sem_schedule_async).
+ */
+size_t sem_workspace_bytes(int64_t n, int64_t num_segments);
+
+/*
+ * Asynchronous single-queue schedule: same arguments as sem_schedule plus a
+ * caller-owned DEVICE workspace of at least sem_workspace_bytes(n, 1) bytes
+ * (256-byte aligned) and the stream to enqueue on. Allocates nothing and
+ * does not synchronise. Host-detectable argument errors are returned at
+ * once; device-detected range errors are left in the workspace and returned
+ * by sem_check. A workspace must not be shared by calls in flight at the
+ * same time.
+ */
+int sem_schedule_async(const uint8_t *priority, const int32_t *length,
+                       int64_t n, int32_t *order_out, int64_t *wait_out,
+                       sem_i128 *totals_out, void *workspace, size_t ws_bytes,
+                       void *stream);
+
+/*
+ * Asynchronous batched schedule. `max_segment` is a host-side upper bound on
+ * the longest queue; it must be <= SEM_SEGMENT_CAP (else SEM_ENOTIMPL).
+ * Offsets are validated on the device (SEM_EINVAL via sem_check), as is a
+ * queue longer than max_segment.
+ */
+int sem_schedule_batched_async(const uint8_t *priority, const int32_t *length,
+                               const int64_t *offsets, int64_t num_segments,
+                               int32_t num_classes, int64_t n_total,
+                               int64_t max_segment, int32_t *order_out,
+                               int64_t *wait_out, sem_i128 *totals_out,
+                               void *workspace, size_t ws_bytes, void *stream);
+
+/* Stream used by the blocking calls (NULL = null stream). */
+int sem_set_stream(void *stream);
+
+/*
+ * Synchronise `stream` and return the status recorded in `workspace` by the
+ * last asynchronous call that used it (SEM_OK, SEM_ERANGE or SEM_EINVAL).
+ */
+int sem_check(const void *workspace, void *stream);
+
+/* Static description of an error code. */
+const char *sem_strerror(int code);
+
+/*
+ * Measurement hook. Arms a one-shot pair of events for one stage of the
+ * multi-pass single-queue path (n > SEM_SEGMENT_CAP): the next asynchronous
+ * or blocking single-queue call on that path records `before` and `after`
+ * (hipEvent_t passed as void *, created by the caller) on its stream right
+ * before and right after that stage's kernel, then disarms the stage.
+ *   stage: SEM_STAGE_HIST  (range check + first-digit histogram),
+ *          SEM_STAGE_FIRST (first scatter pass),
+ *          SEM_STAGE_FINAL (final scatter pass: order, waits, totals).
+ * Passing NULL events disarms the stage. Returns SEM_EINVAL for an unknown
+ * stage. The events are owned by the caller and must outlive the call.
+ */
+#define SEM_STAGE_HIST 0
+#define SEM_STAGE_FIRST 1
+#define SEM_STAGE_FINAL 2
+int sem_trace_stage(int stage, void *before, void *after);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEMSCHED_H */

@@ -1,0 +1,214 @@
+"""MI355X (gfx950) semantic-scheduling hot path: Python binding.
+
+This module only marshals arguments: it allocates outputs and workspaces as
+torch ROCm tensors and calls the C ABI of ``libsemsched.so`` (declared in
+``include/semsched.h``) on torch's current stream. Every step of the schedule
+runs in the library's HIP kernels; there is no CPU fallback. Importing the
+package fails loudly if the library has not been built
+(``python paper_2506_12204_amd/build.py``).
+
+What is computed (Section 3.2, Eq. 1 and Eq. 2 with all arrivals at time 0;
+Algorithm 1's (f_e, f_t) min-heap order): requests sorted by (priority,
+length, id), each request's wait as the exclusive prefix sum of the lengths
+ahead of it, and the exact total and per-class waits.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsemsched.so")
+
+SEM_OK = 0
+SEM_EINVAL = -1
+SEM_ERANGE = -2
+SEM_ENOMEM = -3
+SEM_EDEVICE = -4
+SEM_ENOTIMPL = -5
+MAX_CLASSES = 256
+SEGMENT_CAP = 16384
+
+SYMBOLS = (
+    "sem_schedule",
+    "sem_schedule_batched",
+    "sem_workspace_bytes",
+    "sem_schedule_async",
+    "sem_schedule_batched_async",
+    "sem_set_stream",
+    "sem_check",
+    "sem_strerror",
+    "sem_trace_stage",
+)
+STAGE_HIST, STAGE_FIRST, STAGE_FINAL = 0, 1, 2
+
+
+class SemschedError(RuntimeError):
+    """A library call returned a non-zero status."""
+
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(f"{what}: {strerror(code)} ({code})")
+
+
+class SemschedRangeError(SemschedError, ValueError):
+    """Some length < 0 or some priority >= num_classes."""
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python paper_2506_12204_amd/build.py`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    lib.sem_schedule.argtypes = [vp, vp, i64, vp, vp, vp]
+    lib.sem_schedule_batched.argtypes = [vp, vp, vp, i64, i32, vp, vp, vp]
+    lib.sem_workspace_bytes.argtypes = [i64, i64]
+    lib.sem_workspace_bytes.restype = sz
+    lib.sem_schedule_async.argtypes = [vp, vp, i64, vp, vp, vp, vp, sz, vp]
+    lib.sem_schedule_batched_async.argtypes = [vp, vp, vp, i64, i32, i64, i64, vp, vp, vp,
+                                               vp, sz, vp]
+    lib.sem_set_stream.argtypes = [vp]
+    lib.sem_check.argtypes = [vp, vp]
+    lib.sem_trace_stage.argtypes = [ctypes.c_int, vp, vp]
+    lib.sem_trace_stage.restype = ctypes.c_int
+    lib.sem_strerror.argtypes = [ctypes.c_int]
+    lib.sem_strerror.restype = ctypes.c_char_p
+    for name in ("sem_schedule", "sem_schedule_batched", "sem_schedule_async",
+                 "sem_schedule_batched_async", "sem_set_stream", "sem_check"):
+        getattr(lib, name).restype = ctypes.c_int
+    return lib
+
+
+lib = _load()
+
+
+def strerror(code: int) -> str:
+    return lib.sem_strerror(code).decode()
+
+
+def _raise(code: int, what: str) -> None:
+    if code == SEM_OK:
+        return
+    if code == SEM_ERANGE:
+        raise SemschedRangeError(code, what)
+    raise SemschedError(code, what)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return ctypes.c_void_p(t.data_ptr() if t is not None and t.numel() else 0)
+
+
+def _stream_handle(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check_inputs(priority: torch.Tensor, length: torch.Tensor) -> None:
+    if priority.dtype != torch.uint8 or length.dtype != torch.int32:
+        raise TypeError("priority must be uint8 and length int32")
+    if priority.device.type != "cuda" or length.device != priority.device:
+        raise TypeError("priority and length must live on the same GPU")
+    if priority.dim() != 1 or priority.shape != length.shape:
+        raise ValueError("priority and length must be 1-D and the same size")
+    if not (priority.is_contiguous() and length.is_contiguous()):
+        raise ValueError("inputs must be contiguous")
+
+
+def totals_to_ints(t: torch.Tensor) -> List[int]:
+    """Decode an int64 [..., 2] (lo, hi) tensor of sem_i128 values."""
+    flat = t.reshape(-1, 2).cpu().tolist()
+    return [(hi << 64) | (lo & 0xFFFFFFFFFFFFFFFF) for lo, hi in flat]
+
+
+def trace_stage(stage: int, before: int, after: int) -> None:
+    """Arm one-shot hipEvent_t handles around one stage of the next long-queue call."""
+    _raise(lib.sem_trace_stage(stage, ctypes.c_void_p(before), ctypes.c_void_p(after)),
+           "sem_trace_stage")
+
+
+def workspace_bytes(n: int, num_segments: int = 1) -> int:
+    return int(lib.sem_workspace_bytes(n, num_segments))
+
+
+class Scheduler:
+    """Reusable single-queue schedule of a fixed size n on one device.
+
+    Outputs and the workspace are allocated once; ``run`` enqueues the whole
+    schedule on the current stream without synchronising, ``check`` waits
+    and raises on a device-detected error.
+    """
+
+    def __init__(self, n: int, device="cuda"):
+        self.n = int(n)
+        self.device = torch.device(device)
+        self.order = torch.empty(self.n, dtype=torch.int32, device=self.device)
+        self.wait = torch.empty(self.n, dtype=torch.int64, device=self.device)
+        self.totals = torch.empty((1 + MAX_CLASSES, 2), dtype=torch.int64, device=self.device)
+        self.ws_bytes = workspace_bytes(self.n, 1)
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+
+    def run(self, priority: torch.Tensor, length: torch.Tensor) -> None:
+        _check_inputs(priority, length)
+        if priority.numel() != self.n:
+            raise ValueError("size differs from the Scheduler's n")
+        rc = lib.sem_schedule_async(_ptr(priority), _ptr(length), self.n, _ptr(self.order),
+                                    _ptr(self.wait), _ptr(self.totals), _ptr(self.workspace),
+                                    self.ws_bytes, _stream_handle(self.device))
+        _raise(rc, "sem_schedule_async")
+
+    def check(self) -> None:
+        _raise(lib.sem_check(_ptr(self.workspace), _stream_handle(self.device)), "sem_check")
+
+
+def schedule(priority: torch.Tensor, length: torch.Tensor
+             ) -> Tuple[torch.Tensor, torch.Tensor, List[int]]:
+    """Schedule one queue. Returns (order int32, wait int64, totals[257] ints)."""
+    _check_inputs(priority, length)
+    s = Scheduler(priority.numel(), priority.device)
+    s.run(priority, length)
+    s.check()
+    return s.order, s.wait, totals_to_ints(s.totals)
+
+
+def schedule_batched(priority: torch.Tensor, length: torch.Tensor, offsets: torch.Tensor,
+                     num_classes: int, max_segment: Optional[int] = None
+                     ) -> Tuple[torch.Tensor, torch.Tensor, List[int]]:
+    """Schedule independent queues laid out back to back.
+
+    Returns (order int32 with queue-local ids, wait int64, totals as
+    num_segments*(1+num_classes) ints, queue-major). With ``max_segment``
+    (<= SEGMENT_CAP) the call stays asynchronous up to the final check;
+    without it the library reads the offsets once on the host, which also
+    allows queues longer than SEGMENT_CAP.
+    """
+    _check_inputs(priority, length)
+    if offsets.dtype != torch.int64 or offsets.device != priority.device or offsets.dim() != 1:
+        raise TypeError("offsets must be a 1-D int64 tensor on the inputs' GPU")
+    offsets = offsets.contiguous()
+    s = offsets.numel() - 1
+    if s < 0:
+        raise ValueError("offsets needs at least one entry")
+    n = priority.numel()
+    dev = priority.device
+    order = torch.empty(n, dtype=torch.int32, device=dev)
+    wait = torch.empty(n, dtype=torch.int64, device=dev)
+    totals = torch.empty((max(s, 1), 1 + num_classes, 2), dtype=torch.int64, device=dev)
+    stream = _stream_handle(dev)
+    if max_segment is not None:
+        ws_bytes = workspace_bytes(n, max(s, 2))
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+        rc = lib.sem_schedule_batched_async(_ptr(priority), _ptr(length), _ptr(offsets), s,
+                                            num_classes, n, int(max_segment), _ptr(order),
+                                            _ptr(wait), _ptr(totals), _ptr(ws), ws_bytes, stream)
+        _raise(rc, "sem_schedule_batched_async")
+        _raise(lib.sem_check(_ptr(ws), stream), "sem_check")
+    else:
+        lib.sem_set_stream(stream)
+        rc = lib.sem_schedule_batched(_ptr(priority), _ptr(length), _ptr(offsets), s,
+                                      num_classes, _ptr(order), _ptr(wait), _ptr(totals))
+        _raise(rc, "sem_schedule_batched")
+    return order, wait, totals_to_ints(totals[:s]) if s else []

@@ -1,0 +1,418 @@
+// C ABI of the scheduling library: argument checks, workspace layout, launch
+// planning and error mapping. The operations themselves are defined in
+// semsched.h; every step of them runs in the HIP kernels of this directory.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <vector>
+
+#include "kernels.h"
+#include "semsched.h"
+
+using namespace semsched;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr size_t kHeaderBytes = 256;  // flags, counters, ranges, plan
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+  size_t flags = 0, done = 4, minmax = 16, tile_ctr = 32, plan = 64;
+  size_t hist_cnt = 0, hist_w = 0, cstat0 = 0, cstat1 = 0, wstat = 0;
+  size_t keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0;
+  size_t total = kHeaderBytes;
+  int64_t tiles = 0;
+  bool wide_status = false;
+};
+
+static_assert(sizeof(Plan) <= kHeaderBytes - 64, "plan must fit in the header");
+
+bool needs_global(int64_t n) { return n > kSegLargeCap; }
+
+Layout layout_for(int64_t n) {
+  Layout L;
+  if (!needs_global(n)) return L;
+  L.tiles = (n + kGlobalTile - 1) / kGlobalTile;
+  L.wide_status = n >= (int64_t(1) << 30);
+  const size_t st = L.wide_status ? 8 : 4;
+  size_t off = kHeaderBytes;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  L.hist_cnt = take(sizeof(uint32_t) * kMaxScatter * kMaxBins);
+  L.hist_w = take(sizeof(uint64_t) * kMaxScatter * kMaxBins);
+  L.cstat0 = take(st * L.tiles * kMaxBins);
+  L.cstat1 = take(st * L.tiles * kMaxBins);
+  L.wstat = take(8 * L.tiles * kMaxBins);
+  L.keys0 = take(8 * (size_t)n);
+  L.keys1 = take(8 * (size_t)n);
+  L.ids0 = take(4 * (size_t)n);
+  L.ids1 = take(4 * (size_t)n);
+  L.total = off;
+  return L;
+}
+
+// Width of the first (low-length) digit of the global path, 8..10 bits.
+// SEMSCHED_D0 overrides the default; it is read on every call.
+int d0_bits() {
+  const char* e = std::getenv("SEMSCHED_D0");
+  const int d = e ? std::atoi(e) : 8;
+  return std::min(10, std::max(8, d));
+}
+
+// SEMSCHED_FORCE_WIDE=1 makes the global path keep ids in their own array
+// even when key and id would share one u64 (the layout very wide key ranges
+// need); it lets that layout be exercised on small queues.
+int force_wide() {
+  const char* e = std::getenv("SEMSCHED_FORCE_WIDE");
+  return (e && e[0] == '1') ? 1 : 0;
+}
+
+int num_cus() {
+  static int v = [] {
+    int dev = 0;
+    hipDeviceProp_t prop;
+    if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess)
+      return prop.multiProcessorCount;
+    return 256;
+  }();
+  return v;
+}
+
+int map_flags(uint32_t f) {
+  if (f & kFlagInval) return SEM_EINVAL;
+  if (f & kFlagRange) return SEM_ERANGE;
+  return SEM_OK;
+}
+
+#define HIP_TRY(expr)                           \
+  do {                                          \
+    if ((expr) != hipSuccess) return SEM_EDEVICE; \
+  } while (0)
+
+// Library state for the blocking calls: one cached workspace per device.
+struct State {
+  std::mutex mu;
+  hipStream_t stream = nullptr;
+  std::map<int, std::pair<void*, size_t>> ws;
+};
+State& state() {
+  static State* s = new State();  // never destroyed: the HIP runtime may be gone at exit
+  return *s;
+}
+
+int cached_workspace(size_t bytes, void** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  auto& slot = state().ws[dev];
+  if (slot.second < bytes) {
+    if (slot.first) {
+      HIP_TRY(hipDeviceSynchronize());
+      HIP_TRY(hipFree(slot.first));
+      slot.first = nullptr;
+      slot.second = 0;
+    }
+    void* p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) return SEM_ENOMEM;
+    slot.first = p;
+    slot.second = bytes;
+  }
+  *out = slot.first;
+  return SEM_OK;
+}
+
+// One-shot measurement events, armed by sem_trace_stage.
+std::mutex& trace_mu() {
+  static std::mutex* m = new std::mutex();
+  return *m;
+}
+StageEvents& trace_slots() {
+  static StageEvents* e = new StageEvents();
+  return *e;
+}
+
+int finish(void* ws, hipStream_t st) {
+  HIP_TRY(hipStreamSynchronize(st));
+  uint32_t f = 0;
+  HIP_TRY(hipMemcpy(&f, ws, sizeof(f), hipMemcpyDeviceToHost));
+  return map_flags(f);
+}
+
+// Enqueue one queue (any n >= 0). Arguments already checked.
+int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_classes,
+                  int32_t* order, int64_t* wait, sem_i128* totals, void* ws, hipStream_t st) {
+  char* base = static_cast<char*>(ws);
+  uint32_t* flags = reinterpret_cast<uint32_t*>(base);
+  uint64_t* tot = reinterpret_cast<uint64_t*>(totals);
+  if (n == 0) {
+    if (launch_fill_zero(flags, 1, st) != hipSuccess) return SEM_EDEVICE;
+    if (launch_fill_zero(reinterpret_cast<uint32_t*>(tot), 4 * (size_t)(1 + num_classes), st) !=
+        hipSuccess)
+      return SEM_EDEVICE;
+    return SEM_OK;
+  }
+  if (!needs_global(n)) {
+    if (launch_fill_zero(flags, 1, st) != hipSuccess) return SEM_EDEVICE;
+    SegArgs a = {};
+    a.priority = p;
+    a.length = l;
+    a.offsets = nullptr;
+    a.num_segments = 1;
+    a.n_total = n;
+    a.max_segment = n;
+    a.num_classes = num_classes;
+    a.order = order;
+    a.wait = wait;
+    a.totals = tot;
+    a.flags = flags;
+    const SegSize sz = n <= kSegTinyCap     ? SegSize::kTiny
+                       : n <= kSegSmallCap  ? SegSize::kSmall
+                       : n <= kSegMediumCap ? SegSize::kMedium
+                                            : SegSize::kLarge;
+    return launch_segment_schedule(a, sz, 1, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
+  }
+  const Layout L = layout_for(n);
+  GArgs g = {};
+  g.priority = p;
+  g.length = l;
+  g.n = n;
+  g.order = order;
+  g.wait = wait;
+  g.totals = tot;
+  g.num_classes = num_classes;
+  g.d0 = d0_bits();
+  g.tiles = (int32_t)L.tiles;
+  g.wide_status = L.wide_status ? 1 : 0;
+  g.force_wide = force_wide();
+  g.flags = reinterpret_cast<uint32_t*>(base + L.flags);
+  g.done = reinterpret_cast<uint32_t*>(base + L.done);
+  g.minmax = reinterpret_cast<uint32_t*>(base + L.minmax);
+  g.tile_ctr = reinterpret_cast<uint32_t*>(base + L.tile_ctr);
+  g.plan = reinterpret_cast<Plan*>(base + L.plan);
+  g.hist_cnt = reinterpret_cast<uint32_t*>(base + L.hist_cnt);
+  g.hist_w = reinterpret_cast<uint64_t*>(base + L.hist_w);
+  g.cstat[0] = base + L.cstat0;
+  g.cstat[1] = base + L.cstat1;
+  g.wstat = reinterpret_cast<uint64_t*>(base + L.wstat);
+  g.keys[0] = reinterpret_cast<uint64_t*>(base + L.keys0);
+  g.keys[1] = reinterpret_cast<uint64_t*>(base + L.keys1);
+  g.ids[0] = reinterpret_cast<uint32_t*>(base + L.ids0);
+  g.ids[1] = reinterpret_cast<uint32_t*>(base + L.ids1);
+  StageEvents ev = {};
+  bool armed = false;
+  {
+    std::lock_guard<std::mutex> guard(trace_mu());
+    for (int k = 0; k < 3; ++k) {
+      ev.before[k] = trace_slots().before[k];
+      ev.after[k] = trace_slots().after[k];
+      armed = armed || ev.before[k] || ev.after[k];
+      trace_slots().before[k] = trace_slots().after[k] = nullptr;
+    }
+  }
+  return launch_global_schedule(g, st, armed ? &ev : nullptr) == hipSuccess ? SEM_OK
+                                                                           : SEM_EDEVICE;
+}
+
+int check_queue_args(const uint8_t* p, const int32_t* l, int64_t n, int32_t* order,
+                     int64_t* wait, sem_i128* totals) {
+  if (n < 0 || n > INT32_MAX) return SEM_EINVAL;
+  if (!totals) return SEM_EINVAL;
+  if (n > 0 && (!p || !l || !order || !wait)) return SEM_EINVAL;
+  return SEM_OK;
+}
+
+int check_batched_args(const uint8_t* p, const int32_t* l, const int64_t* offsets,
+                       int64_t num_segments, int32_t num_classes, int32_t* order,
+                       int64_t* wait, sem_i128* totals) {
+  if (num_segments < 0 || num_classes < 1 || num_classes > SEM_MAX_CLASSES) return SEM_EINVAL;
+  if (!offsets) return SEM_EINVAL;
+  if (num_segments > 0 && (!p || !l || !order || !wait || !totals)) return SEM_EINVAL;
+  return SEM_OK;
+}
+
+// Launch the LDS kernels for every size class that can occur in (lo, hi].
+int enqueue_segments(SegArgs a, int64_t seg_max, const int64_t* counts, hipStream_t st) {
+  const SegSize sizes[4] = {SegSize::kTiny, SegSize::kSmall, SegSize::kMedium, SegSize::kLarge};
+  const int64_t lo[4] = {-1, kSegTinyCap, kSegSmallCap, kSegMediumCap};
+  const int per_cu[4] = {16, 4, 4, 1};
+  for (int k = 0; k < 4; ++k) {
+    if (seg_max <= lo[k] && k > 0) continue;
+    if (counts && counts[k] == 0) continue;
+    const int64_t want = counts ? counts[k] : a.num_segments;
+    const int64_t cap = (int64_t)num_cus() * per_cu[k];
+    const int grid = (int)std::max<int64_t>(1, std::min(want, cap));
+    if (launch_segment_schedule(a, sizes[k], grid, st) != hipSuccess) return SEM_EDEVICE;
+  }
+  return SEM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sem_strerror(int code) {
+  switch (code) {
+    case SEM_OK: return "success";
+    case SEM_EINVAL: return "invalid argument";
+    case SEM_ERANGE: return "length < 0 or priority >= num_classes";
+    case SEM_ENOMEM: return "out of device memory";
+    case SEM_EDEVICE: return "HIP runtime error";
+    case SEM_ENOTIMPL: return "queue longer than SEM_SEGMENT_CAP in the asynchronous batched call";
+    default: return "unknown error";
+  }
+}
+
+int sem_trace_stage(int stage, void* before, void* after) {
+  if (stage < SEM_STAGE_HIST || stage > SEM_STAGE_FINAL) return SEM_EINVAL;
+  std::lock_guard<std::mutex> guard(trace_mu());
+  trace_slots().before[stage] = static_cast<hipEvent_t>(before);
+  trace_slots().after[stage] = static_cast<hipEvent_t>(after);
+  return SEM_OK;
+}
+
+int sem_set_stream(void* stream) {
+  std::lock_guard<std::mutex> g(state().mu);
+  state().stream = static_cast<hipStream_t>(stream);
+  return SEM_OK;
+}
+
+size_t sem_workspace_bytes(int64_t n, int64_t num_segments) {
+  if (n < 0) return 0;
+  if (num_segments == 1) return layout_for(n).total;
+  return kHeaderBytes;
+}
+
+int sem_check(const void* workspace, void* stream) {
+  if (!workspace) return SEM_EINVAL;
+  return finish(const_cast<void*>(workspace), static_cast<hipStream_t>(stream));
+}
+
+int sem_schedule_async(const uint8_t* priority, const int32_t* length, int64_t n,
+                       int32_t* order_out, int64_t* wait_out, sem_i128* totals_out,
+                       void* workspace, size_t ws_bytes, void* stream) {
+  const int rc = check_queue_args(priority, length, n, order_out, wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  if (!workspace || ws_bytes < sem_workspace_bytes(n, 1) ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return SEM_EINVAL;
+  return enqueue_queue(priority, length, n, SEM_MAX_CLASSES, order_out, wait_out, totals_out,
+                       workspace, static_cast<hipStream_t>(stream));
+}
+
+int sem_schedule(const uint8_t* priority, const int32_t* length, int64_t n, int32_t* order_out,
+                 int64_t* wait_out, sem_i128* totals_out) {
+  int rc = check_queue_args(priority, length, n, order_out, wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  std::lock_guard<std::mutex> g(state().mu);
+  void* ws = nullptr;
+  rc = cached_workspace(sem_workspace_bytes(n, 1), &ws);
+  if (rc != SEM_OK) return rc;
+  const hipStream_t st = state().stream;
+  rc = enqueue_queue(priority, length, n, SEM_MAX_CLASSES, order_out, wait_out, totals_out, ws,
+                     st);
+  if (rc != SEM_OK) return rc;
+  return finish(ws, st);
+}
+
+int sem_schedule_batched_async(const uint8_t* priority, const int32_t* length,
+                               const int64_t* offsets, int64_t num_segments,
+                               int32_t num_classes, int64_t n_total, int64_t max_segment,
+                               int32_t* order_out, int64_t* wait_out, sem_i128* totals_out,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  const int rc = check_batched_args(priority, length, offsets, num_segments, num_classes,
+                                    order_out, wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  if (n_total < 0 || max_segment < 0) return SEM_EINVAL;
+  if (max_segment > SEM_SEGMENT_CAP) return SEM_ENOTIMPL;
+  if (!workspace || ws_bytes < kHeaderBytes ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return SEM_EINVAL;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  uint32_t* flags = static_cast<uint32_t*>(workspace);
+  if (launch_fill_zero(flags, 1, st) != hipSuccess) return SEM_EDEVICE;
+  if (num_segments == 0) return SEM_OK;
+  SegArgs a = {};
+  a.priority = priority;
+  a.length = length;
+  a.offsets = offsets;
+  a.num_segments = num_segments;
+  a.n_total = n_total;
+  a.max_segment = max_segment;
+  a.num_classes = num_classes;
+  a.order = order_out;
+  a.wait = wait_out;
+  a.totals = reinterpret_cast<uint64_t*>(totals_out);
+  a.flags = flags;
+  return enqueue_segments(a, max_segment, nullptr, st);
+}
+
+int sem_schedule_batched(const uint8_t* priority, const int32_t* length,
+                         const int64_t* offsets, int64_t num_segments, int32_t num_classes,
+                         int32_t* order_out, int64_t* wait_out, sem_i128* totals_out) {
+  int rc = check_batched_args(priority, length, offsets, num_segments, num_classes, order_out,
+                              wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  if (num_segments == 0) return SEM_OK;
+  std::lock_guard<std::mutex> g(state().mu);
+  const hipStream_t st = state().stream;
+  std::vector<int64_t> off((size_t)num_segments + 1);
+  HIP_TRY(hipMemcpyAsync(off.data(), offsets, off.size() * sizeof(int64_t),
+                         hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  if (off[0] != 0) return SEM_EINVAL;
+  int64_t counts[4] = {0, 0, 0, 0};
+  int64_t seg_max = 0;
+  std::vector<int64_t> big;
+  for (int64_t s = 0; s < num_segments; ++s) {
+    const int64_t m = off[s + 1] - off[s];
+    if (m < 0 || m > INT32_MAX) return SEM_EINVAL;
+    seg_max = std::max(seg_max, m);
+    if (m <= kSegTinyCap) ++counts[0];
+    else if (m <= kSegSmallCap) ++counts[1];
+    else if (m <= kSegMediumCap) ++counts[2];
+    else if (m <= kSegLargeCap) ++counts[3];
+    else big.push_back(s);
+  }
+  size_t need = kHeaderBytes;
+  for (int64_t s : big) need = std::max(need, layout_for(off[s + 1] - off[s]).total);
+  void* ws = nullptr;
+  rc = cached_workspace(need, &ws);
+  if (rc != SEM_OK) return rc;
+  uint32_t* flags = static_cast<uint32_t*>(ws);
+  if (launch_fill_zero(flags, 1, st) != hipSuccess) return SEM_EDEVICE;
+  SegArgs a = {};
+  a.priority = priority;
+  a.length = length;
+  a.offsets = offsets;
+  a.num_segments = num_segments;
+  a.n_total = off[num_segments];
+  a.max_segment = INT64_MAX;  // long queues are simply not routed to the LDS kernels
+  a.num_classes = num_classes;
+  a.order = order_out;
+  a.wait = wait_out;
+  a.totals = reinterpret_cast<uint64_t*>(totals_out);
+  a.flags = flags;
+  rc = enqueue_segments(a, std::min<int64_t>(seg_max, kSegLargeCap), counts, st);
+  if (rc != SEM_OK) return rc;
+  rc = finish(ws, st);
+  if (rc != SEM_OK) return rc;
+  for (int64_t s : big) {
+    const int64_t b = off[s];
+    rc = enqueue_queue(priority + b, length + b, off[s + 1] - b, num_classes, order_out + b,
+                       wait_out + b, totals_out + s * (1 + (int64_t)num_classes), ws, st);
+    if (rc != SEM_OK) return rc;
+    rc = finish(ws, st);
+    if (rc != SEM_OK) return rc;
+  }
+  return SEM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,138 @@
+// Device helpers shared by the gfx950 scheduling kernels: wave64 digit
+// matching and ranking, wave-level scans and reductions, exact 128-bit
+// accumulation. Nothing here is specific to one kernel.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace semsched {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint32_t bit_width32(uint32_t x) {
+  return x ? 32u - __clz(x) : 0u;
+}
+
+__device__ __forceinline__ uint64_t lanes_below() { return __lanemask_lt(); }
+
+// Mask of the lanes of the wave whose `d` agrees with this lane's on the low
+// `nbits` bits. Every lane of the wave must execute it (all 64 are active in
+// every caller: invalid items carry a sentinel digit instead of idling).
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, int nbits) {
+  uint64_t peers = ~0ull;
+  for (int b = 0; b < nbits; ++b) {
+    const bool set = (d >> b) & 1u;
+    const uint64_t m = __ballot(set);
+    peers &= set ? m : ~m;
+  }
+  return peers;
+}
+
+// Stable per-wave ranking of one round of 64 digits against this wave's
+// running counters `cnt` (LDS, one u16 per digit, private to the wave).
+// Returns the number of earlier items of the wave (earlier rounds, then lower
+// lanes of this round) that carry the same digit, and advances the counter.
+__device__ __forceinline__ uint32_t rank_round(uint32_t d, int nbits,
+                                               uint16_t* cnt) {
+  const uint64_t peers = match_digit(d, nbits);
+  const uint32_t below = __popcll(peers & lanes_below());
+  const uint32_t base = cnt[d];
+  // All peers have read the old count before the lowest peer writes the new
+  // one: a wave's LDS operations complete in program order.
+  if (below == 0) cnt[d] = (uint16_t)(base + __popcll(peers));
+  return base + below;
+}
+
+// Inclusive wave scan of a 64-bit value.
+__device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint64_t o = __shfl_up(v, off, kWave);
+    if (lane_id() >= off) v += o;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t o = __shfl_up(v, off, kWave);
+    if (lane_id() >= off) v += o;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v = min(v, (uint32_t)__shfl_xor(v, off, kWave));
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v = max(v, (uint32_t)__shfl_xor(v, off, kWave));
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_or_u32(uint32_t v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v |= (uint32_t)__shfl_xor(v, off, kWave);
+  return v;
+}
+
+// Unsigned 128-bit accumulator (waits are non-negative).
+struct U128 {
+  uint64_t lo, hi;
+};
+
+__device__ __forceinline__ void add128(U128& a, uint64_t v) {
+  a.lo += v;
+  a.hi += (a.lo < v) ? 1u : 0u;
+}
+
+__device__ __forceinline__ void add128(U128& a, const U128& b) {
+  a.lo += b.lo;
+  a.hi += b.hi + ((a.lo < b.lo) ? 1u : 0u);
+}
+
+// Wave-wide sum of 128-bit values (result valid in every lane).
+__device__ __forceinline__ U128 wave_sum128(U128 v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) {
+    U128 o;
+    o.lo = __shfl_xor(v.lo, off, kWave);
+    o.hi = __shfl_xor(v.hi, off, kWave);
+    add128(v, o);
+  }
+  return v;
+}
+
+// Atomically add a 128-bit value into (lo, hi) words. The carry out of the
+// low word is derived from the value it held just before this addition, so
+// the pair stays exact under any interleaving of such calls.
+__device__ __forceinline__ void atomic_add128(uint64_t* lo, uint64_t* hi,
+                                              const U128& v) {
+  const uint64_t old =
+      atomicAdd(reinterpret_cast<unsigned long long*>(lo), (unsigned long long)v.lo);
+  const uint64_t carry = (old + v.lo < old) ? 1u : 0u;
+  atomicAdd(reinterpret_cast<unsigned long long*>(hi),
+            (unsigned long long)(v.hi + carry));
+}
+
+// Relaxed agent-scope loads and stores for the look-back status words. Each
+// word carries its own flag and value, so no ordering with other memory is
+// needed, only coherence across the XCDs' L2 caches.
+template <typename T>
+__device__ __forceinline__ T load_agent(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <typename T>
+__device__ __forceinline__ void store_agent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+}  // namespace semsched

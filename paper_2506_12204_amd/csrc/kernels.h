@@ -1,0 +1,98 @@
+// Host/device interface of the scheduling kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace semsched {
+
+// Device-detected error bits, OR-ed into the workspace's first word.
+constexpr uint32_t kFlagInval = 1u;  // bad offsets / queue longer than promised
+constexpr uint32_t kFlagRange = 2u;  // length < 0 or priority >= num_classes
+
+// Queue-size classes of the LDS path (one workgroup per queue).
+constexpr int kSegTinyCap = 256;      // 64 threads x 4 rounds
+constexpr int kSegSmallCap = 1024;    // 256 threads x 4 rounds
+constexpr int kSegMediumCap = 4096;   // 256 threads x 16 rounds
+constexpr int kSegLargeCap = 16384;   // 512 threads x 32 rounds
+enum class SegSize { kTiny, kSmall, kMedium, kLarge };
+
+struct SegArgs {
+  const uint8_t* priority;
+  const int32_t* length;
+  const int64_t* offsets;  // null: one queue of n_total requests
+  int64_t num_segments;
+  int64_t n_total;
+  int64_t max_segment;     // longer queues are reported as kFlagInval
+  int32_t num_classes;     // validation bound and totals stride - 1
+  int32_t* order;
+  int64_t* wait;
+  uint64_t* totals;        // (lo, hi) pairs, num_segments * (1 + num_classes)
+  uint32_t* flags;
+  int64_t route_lo, route_hi;  // this launch handles route_lo < m <= route_hi
+};
+
+hipError_t launch_segment_schedule(SegArgs a, SegSize size, int grid, hipStream_t st);
+
+// ---------------------------------------------------------------------------
+// Global multi-pass path (one queue longer than kSegLargeCap).
+
+constexpr int kMaxBins = 1024;   // digit bins of every scatter pass
+constexpr int kMaxScatter = 5;   // scatter passes: first, up to 3 middle, final
+constexpr int kGlobalThreads = 512;
+constexpr int kGlobalRounds = 16;
+constexpr int kGlobalTile = kGlobalThreads * kGlobalRounds;
+
+// Decided on the device by the histogram pass once the ranges are known.
+struct Plan {
+  uint32_t ok;        // 0 if a range error was found
+  uint32_t pmin;      // smallest priority
+  uint32_t hmin;      // smallest length >> d0
+  uint32_t H;         // (largest length >> d0) - hmin + 1
+  uint32_t P;         // largest priority - pmin + 1
+  uint32_t wh, wp;    // bit widths of the h and p fields of a key
+  uint32_t W;         // bit width of a request id
+  uint32_t packed;    // 1: element = key << W | id in one u64
+  uint32_t nscatter;  // number of scatter passes (>= 2)
+  uint32_t shift[kMaxScatter];  // digit = (u2 >> shift) & (bins - 1), passes >= 1
+  uint32_t nbits[kMaxScatter];
+  uint32_t nbins[kMaxScatter];
+};
+
+struct GArgs {
+  const uint8_t* priority;
+  const int32_t* length;
+  int64_t n;
+  int32_t* order;
+  int64_t* wait;
+  uint64_t* totals;     // (lo, hi) pairs, 1 + num_classes
+  int32_t num_classes;
+  int32_t d0;           // width of the first (low-length) digit
+  int32_t tiles;
+  int32_t wide_status;  // 1: count status words are u64
+  int32_t force_wide;   // 1: never pack the id into the key word
+  uint32_t* flags;
+  uint32_t* done;
+  uint32_t* minmax;     // pmin, pmax, lmin, lmax
+  uint32_t* tile_ctr;   // one per scatter pass
+  Plan* plan;
+  uint32_t* hist_cnt;   // [kMaxScatter][kMaxBins]
+  uint64_t* hist_w;     // [kMaxScatter][kMaxBins]
+  void* cstat[2];       // count look-back status, tiles * kMaxBins words each
+  uint64_t* wstat;      // weight look-back status, tiles * kMaxBins
+  uint64_t* keys[2];
+  uint32_t* ids[2];
+};
+
+// Optional events recorded around one stage's kernel (null: not armed).
+struct StageEvents {
+  hipEvent_t before[3];
+  hipEvent_t after[3];
+};
+
+hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEvents* ev);
+
+// Zeroes `count` 32-bit words (graph-safe replacement for a memset).
+hipError_t launch_fill_zero(uint32_t* p, size_t count, hipStream_t st);
+
+}  // namespace semsched

@@ -1,0 +1,93 @@
+"""The C ABI library loads, exports every declared entry point, and rejects
+bad arguments on the host (no GPU is touched by any call here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from tests._lib import LIB, ROOT, ensure_built
+
+HEADER = os.path.join(ROOT, "include", "semsched.h")
+
+
+@pytest.fixture(scope="module")
+def ss():
+    ensure_built()
+    import paper_2506_12204_amd as mod
+    return mod
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sem_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(ss):
+    names = declared_functions()
+    assert "sem_schedule" in names and "sem_schedule_batched" in names
+    lib = ctypes.CDLL(LIB)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(ss.SYMBOLS)
+
+
+def test_strerror(ss):
+    for code in (0, -1, -2, -3, -4, -5):
+        assert ss.strerror(code)
+    assert ss.strerror(-99) == "unknown error"
+
+
+def test_workspace_sizes(ss):
+    small = ss.workspace_bytes(16384, 1)
+    big = ss.workspace_bytes(1 << 20, 1)
+    assert small == 256
+    assert big > 24 * (1 << 20)  # two u64 key buffers + two u32 id buffers
+    assert ss.workspace_bytes(1 << 20, 1000) == 256
+    assert ss.workspace_bytes(-1, 1) == 0
+
+
+def test_queue_argument_errors(ss):
+    L = ss.lib
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 40)  # never dereferenced: the call fails first
+    assert L.sem_schedule(fake, fake, -1, fake, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_schedule(fake, fake, 1 << 31, fake, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_schedule(nul, fake, 5, fake, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_schedule(fake, fake, 5, fake, nul, fake) == ss.SEM_EINVAL
+    assert L.sem_schedule(fake, fake, 5, fake, fake, nul) == ss.SEM_EINVAL
+    # async: workspace missing, too small or misaligned
+    assert L.sem_schedule_async(fake, fake, 5, fake, fake, fake, nul, 4096, nul) == ss.SEM_EINVAL
+    assert L.sem_schedule_async(fake, fake, 1 << 20, fake, fake, fake, fake, 256,
+                                nul) == ss.SEM_EINVAL
+    assert L.sem_schedule_async(fake, fake, 5, fake, fake, fake, ctypes.c_void_p((1 << 40) + 8),
+                                4096, nul) == ss.SEM_EINVAL
+
+
+def test_batched_argument_errors(ss):
+    L = ss.lib
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 40)
+    assert L.sem_schedule_batched(fake, fake, fake, -1, 4, fake, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_schedule_batched(fake, fake, fake, 3, 0, fake, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_schedule_batched(fake, fake, fake, 3, 257, fake, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_schedule_batched(fake, fake, nul, 3, 4, fake, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_schedule_batched(fake, fake, fake, 3, 4, fake, fake, nul) == ss.SEM_EINVAL
+    A = L.sem_schedule_batched_async
+    assert A(fake, fake, fake, 3, 4, 10, ss.SEGMENT_CAP + 1, fake, fake, fake, fake, 256,
+             nul) == ss.SEM_ENOTIMPL
+    assert A(fake, fake, fake, 3, 4, -1, 5, fake, fake, fake, fake, 256, nul) == ss.SEM_EINVAL
+    assert A(fake, fake, fake, 3, 4, 10, 5, fake, fake, fake, fake, 128, nul) == ss.SEM_EINVAL
+    assert L.sem_check(nul, nul) == ss.SEM_EINVAL
+
+
+def test_binding_type_checks(ss):
+    import torch
+    p = torch.zeros(4, dtype=torch.uint8)
+    l = torch.zeros(4, dtype=torch.int32)
+    with pytest.raises(TypeError):
+        ss.schedule(p, l)  # CPU tensors are refused: there is no CPU path
+    with pytest.raises(TypeError):
+        ss.schedule(p.to(torch.int32), l)

@@ -1,0 +1,197 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Everything here is integer, so every comparison is bit-exact: order, every
+wait and every 128-bit total. The oracle is the plain C oracle (oracle.c),
+itself pinned to the pure-Python oracle and to the paper's optimisation
+problem by the CPU tests.
+"""
+
+import os
+
+import numpy as np
+import pytest
+
+from oracle import c_oracle_batched, c_oracle_queue
+from tests._lib import assert_same, ensure_built, gpu_available, gpu_batched, gpu_queue
+from workloads import fuzz_queue, fuzz_segments, generate
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    ensure_built()
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def check_queue(p, l, label):
+    say(f"[gpu] queue {label}: n={len(p)}")
+    assert_same(gpu_queue(p, l), c_oracle_queue(p, l), label)
+
+
+def check_batched(p, l, off, classes, label, max_segment=None):
+    say(f"[gpu] batched {label}: n={len(p)} segments={len(off) - 1}")
+    assert_same(gpu_batched(p, l, off, classes, max_segment),
+                c_oracle_batched(p, l, off, classes), label)
+
+
+# ---- the five workloads at full size -----------------------------------------
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3"])
+def test_workload_queue(name):
+    w = generate(name)
+    check_queue(w.priority, w.length, name)
+
+
+@pytest.mark.parametrize("name", ["c4", "c5"])
+def test_workload_batched(name):
+    w = generate(name)
+    check_batched(w.priority, w.length, w.offsets, w.num_classes, name)
+    maxseg = int(np.diff(w.offsets).max())
+    check_batched(w.priority, w.length, w.offsets, w.num_classes, name + "-async", maxseg)
+
+
+# ---- sizes around every tile and LDS-class boundary -----------------------------
+
+SIZES = [0, 1, 2, 63, 64, 65, 255, 256, 257, 1023, 1024, 1025, 4095, 4096, 4097,
+         16383, 16384, 16385, 24576, 24577, 65537, 100003]
+
+
+@pytest.mark.parametrize("n", SIZES)
+def test_fuzz_sizes(n):
+    p, l = fuzz_queue(n, seed=n, classes=7, max_len=5000, tie_frac=0.3)
+    check_queue(p, l, f"fuzz{n}")
+
+
+@pytest.mark.parametrize("d0", ["8", "9", "10"])
+def test_first_digit_widths(d0, monkeypatch):
+    monkeypatch.setenv("SEMSCHED_D0", d0)
+    p, l = fuzz_queue(200_000, seed=7, classes=5, max_len=32768, tie_frac=0.2)
+    check_queue(p, l, f"d0={d0}")
+
+
+# ---- degenerate and adversarial queues ----------------------------------------
+
+@pytest.mark.parametrize("n", [300, 5000, 40000])
+def test_all_keys_equal(n):
+    check_queue(np.full(n, 3, np.uint8), np.full(n, 7, np.int32), "all-equal")
+
+
+@pytest.mark.parametrize("n", [3000, 50000])
+def test_reverse_sorted(n):
+    p = np.repeat(np.arange(4, dtype=np.uint8)[::-1], n // 4 + 1)[:n]
+    l = np.arange(n, 0, -1).astype(np.int32)
+    check_queue(p, l, "reverse")
+
+
+@pytest.mark.parametrize("n", [1000, 70000])
+def test_one_class_and_zero_lengths(n):
+    rng = np.random.default_rng(n)
+    l = rng.integers(0, 3, n).astype(np.int32)
+    check_queue(np.zeros(n, np.uint8), l, "one-class-zeros")
+
+
+@pytest.mark.parametrize("n", [2000, 50000])
+def test_all_256_classes_full_length_range(n):
+    # 256 classes x lengths up to 2^31-1: the widest keys; on the global path
+    # this needs three middle passes.
+    rng = np.random.default_rng(99)
+    p = rng.integers(0, 256, n).astype(np.uint8)
+    l = rng.integers(0, 2**31 - 1, n, dtype=np.int64).astype(np.int32)
+    l[:5] = 2**31 - 1
+    l[5:10] = 0
+    check_queue(p, l, "256-classes")
+
+
+def test_max_length_totals_beyond_2_64():
+    n = 1 << 18
+    p = np.zeros(n, np.uint8)
+    l = np.full(n, 2**31 - 1, np.int32)
+    got = gpu_queue(p, l)
+    want = c_oracle_queue(p, l)
+    assert_same(got, want, "int32-max")
+    assert want[2][0] > 2**64
+
+
+@pytest.mark.parametrize("n", [20000, 100003])
+def test_forced_wide_layout(n, monkeypatch):
+    monkeypatch.setenv("SEMSCHED_FORCE_WIDE", "1")
+    p, l = fuzz_queue(n, seed=3, classes=9, max_len=100000, tie_frac=0.2)
+    check_queue(p, l, "wide")
+    rng = np.random.default_rng(5)
+    p = rng.integers(0, 256, n).astype(np.uint8)
+    l = rng.integers(0, 2**31 - 1, n, dtype=np.int64).astype(np.int32)
+    check_queue(p, l, "wide-mid-passes")
+
+
+def test_repeatable_bit_for_bit():
+    p, l = fuzz_queue(300_000, seed=11, classes=5, max_len=2000, tie_frac=0.5)
+    first = gpu_queue(p, l)
+    for _ in range(10):
+        assert_same(gpu_queue(p, l), first, "repeat")
+
+
+# ---- batched inputs ------------------------------------------------------------
+
+def test_batched_mixed_sizes_and_empty_queues():
+    sizes = [0, 1, 0, 255, 256, 257, 1024, 1025, 4096, 4097, 0, 16384, 16385, 70000, 3]
+    p, l, off = fuzz_segments(sizes, seed=21, classes=6, max_len=3000)
+    check_batched(p, l, off, 6, "mixed")
+
+
+def test_batched_async_small():
+    sizes = np.random.default_rng(1).integers(0, 700, 3000)
+    p, l, off = fuzz_segments(sizes, seed=22, classes=4, max_len=400)
+    check_batched(p, l, off, 4, "async", max_segment=int(sizes.max()))
+
+
+def test_batched_single_class_count():
+    p, l, off = fuzz_segments([5, 9, 2000], seed=23, classes=1, max_len=50)
+    check_batched(p, l, off, 1, "one-class")
+
+
+# ---- errors detected on the device ------------------------------------------------
+
+@pytest.mark.parametrize("n", [100, 3000, 50000])
+def test_negative_length_is_range_error(n):
+    import paper_2506_12204_amd as ss
+    p, l = fuzz_queue(n, seed=1)
+    l[n // 2] = -5
+    with pytest.raises(ss.SemschedRangeError):
+        gpu_queue(p, l)
+
+
+def test_priority_out_of_range_in_batched():
+    import paper_2506_12204_amd as ss
+    p, l, off = fuzz_segments([10, 20, 30], seed=2, classes=4)
+    p[15] = 4
+    with pytest.raises(ss.SemschedRangeError):
+        gpu_batched(p, l, off, 4)
+    with pytest.raises(ss.SemschedRangeError):
+        gpu_batched(p, l, off, 4, max_segment=30)
+
+
+def test_bad_offsets():
+    import paper_2506_12204_amd as ss
+    p, l, off = fuzz_segments([10, 20, 30], seed=3, classes=4)
+    bad = off.copy()
+    bad[2] = 5  # decreasing
+    with pytest.raises(ss.SemschedError):
+        gpu_batched(p, l, bad, 4)
+    with pytest.raises(ss.SemschedError):
+        gpu_batched(p, l, bad, 4, max_segment=30)
+    with pytest.raises(ss.SemschedError):  # a queue longer than promised
+        gpu_batched(p, l, off, 4, max_segment=20)
+
+
+def test_after_error_next_call_is_clean():
+    p, l = fuzz_queue(30000, seed=4)
+    good = (p.copy(), l.copy())
+    l[7] = -1
+    with pytest.raises(Exception):
+        gpu_queue(p, l)
+    check_queue(*good, "after-error")
