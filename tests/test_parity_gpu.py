@@ -55,6 +55,18 @@ def test_workload_batched(name):
     check_batched(w.priority, w.length, w.offsets, w.num_classes, name + "-async", maxseg)
 
 
+def test_batched_repeat_many_workgroups_per_cu():
+    # Regression: a barrier that let waves pass with LDS loads in flight let
+    # another wave's counter reset overwrite staged elements, intermittently,
+    # only when many workgroups shared a CU. Repeat the crowded launch.
+    w = generate("c5")
+    want = c_oracle_batched(w.priority, w.length, w.offsets, w.num_classes)
+    for k in range(4):
+        say(f"[gpu] c5 repeat {k}")
+        assert_same(gpu_batched(w.priority, w.length, w.offsets, w.num_classes,
+                                4096 if k % 2 else None), want, f"c5-repeat{k}")
+
+
 # ---- sizes around every tile and LDS-class boundary -----------------------------
 
 SIZES = [0, 1, 2, 63, 64, 65, 255, 256, 257, 1023, 1024, 1025, 4095, 4096, 4097,
