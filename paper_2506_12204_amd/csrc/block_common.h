@@ -18,7 +18,7 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t v, uint32_t* sc
   const int w = threadIdx.x / kWave;
   const uint32_t incl = wave_incl_scan_u32(v);
   if (lane_id() == kWave - 1) scratch[w] = incl;
-  __syncthreads();
+  block_sync();
   uint32_t off = 0, tot = 0;
 #pragma unroll
   for (int i = 0; i < NW; ++i) {
@@ -26,7 +26,7 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t v, uint32_t* sc
     off += (i < w) ? s : 0u;
     tot += s;
   }
-  __syncthreads();
+  block_sync();
   total = tot;
   return off + incl - v;
 }
@@ -38,7 +38,7 @@ __device__ __forceinline__ uint64_t block_excl_scan_u64(uint64_t v, uint64_t* sc
   const int w = threadIdx.x / kWave;
   const uint64_t incl = wave_incl_scan_u64(v);
   if (lane_id() == kWave - 1) scratch[w] = incl;
-  __syncthreads();
+  block_sync();
   uint64_t off = 0, tot = 0;
 #pragma unroll
   for (int i = 0; i < NW; ++i) {
@@ -46,7 +46,7 @@ __device__ __forceinline__ uint64_t block_excl_scan_u64(uint64_t v, uint64_t* sc
     off += (i < w) ? s : 0u;
     tot += s;
   }
-  __syncthreads();
+  block_sync();
   total = tot;
   return off + incl - v;
 }
@@ -90,7 +90,7 @@ __device__ void block_digit_offsets(uint16_t* cnt, int stride, int nbins,
     }
   }
   if (threadIdx.x == 0) excl[nbins] = total;
-  __syncthreads();
+  block_sync();
 }
 
 }  // namespace semsched

@@ -12,6 +12,17 @@ constexpr int kWave = 64;
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
+// Workgroup barrier that first drains this wave's outstanding LDS operations.
+// __syncthreads() alone may let a wave reach s_barrier with LDS loads still in
+// flight; another wave can then overwrite the location after the barrier
+// before that load has read it (observed as corrupted elements when the wave
+// counters reuse the stage buffer). Every barrier in these kernels guards a
+// write-after-read or read-after-write hand-over of LDS, so all of them wait.
+__device__ __forceinline__ void block_sync() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __syncthreads();
+}
+
 __device__ __forceinline__ uint32_t bit_width32(uint32_t x) {
   return x ? 32u - __clz(x) : 0u;
 }

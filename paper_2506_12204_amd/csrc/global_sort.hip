@@ -96,7 +96,7 @@ __global__ __launch_bounds__(kHistThreads) void g_hist(GArgs a, int vec_ok) {
   const int nb = 1 << a.d0;
   const uint32_t mask = (uint32_t)nb - 1;
   for (int b = t; b < nb; b += kHistThreads) s_hist[b] = 0;
-  __syncthreads();
+  block_sync();
 
   uint32_t lmin = 0xffffffffu, lmax = 0, pmin = 0xffu, pmax = 0, bad = 0;
   const int64_t stride = (int64_t)gridDim.x * kHistThreads;
@@ -131,7 +131,7 @@ __global__ __launch_bounds__(kHistThreads) void g_hist(GArgs a, int vec_ok) {
     s_red[2][w] = pmin;
     s_red[3][w] = pmax | (bad << 31);
   }
-  __syncthreads();
+  block_sync();
   if (t == 0) {
     for (int i = 1; i < HW; ++i) {
       lmin = min(lmin, s_red[0][i]);
@@ -165,9 +165,9 @@ __global__ __launch_bounds__(kHistThreads) void g_hist(GArgs a, int vec_ok) {
 
   // The last workgroup to finish turns the ranges into the Plan.
   __threadfence();
-  __syncthreads();
+  block_sync();
   if (t == 0) s_last = (atomicAdd(a.done, 1u) == gridDim.x - 1) ? 1u : 0u;
-  __syncthreads();
+  block_sync();
   if (!s_last || t != 0) return;
   __threadfence();
   const uint32_t fl = load_agent(a.flags);
@@ -372,9 +372,9 @@ __global__ __launch_bounds__(NT) void g_scatter(GArgs a, int s_arg) {
 
   // ---- tiles ------------------------------------------------------------
   for (;;) {
-    __syncthreads();
+    block_sync();
     if (t == 0) sh.tile = atomicAdd(&a.tile_ctr[s], 1u);
-    __syncthreads();
+    block_sync();
     const int tile = (int)sh.tile;
     if (tile >= a.tiles) break;
     const int64_t tb = (int64_t)tile * T;
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(NT) void g_scatter(GArgs a, int s_arg) {
     for (int b = lane; b < nb; b += kWave) cnt[w * kMaxBins + b] = 0;
 #pragma unroll
     for (int r = 0; r < K; ++r) rk[r] = rank_round(dg[r], nbits, cnt + w * kMaxBins);
-    __syncthreads();
+    block_sync();
     block_digit_offsets<NT>(cnt, kMaxBins, nb, sh.excl, sh.scan32);
 #pragma unroll
     for (int r = 0; r < K; ++r) rk[r] += sh.excl[dg[r]] + cnt[w * kMaxBins + dg[r]];
@@ -449,21 +449,21 @@ __global__ __launch_bounds__(NT) void g_scatter(GArgs a, int s_arg) {
         }
         sh.base[b] = sh.gbase[b] + (uint32_t)ex - sh.excl[b];
       }
-      __syncthreads();  // counters read, bases ready
+      block_sync();  // counters read, bases ready
       uint32_t jid[K];
       if (!packed) {
         uint32_t* sid = reinterpret_cast<uint32_t*>(sh.stage);
 #pragma unroll
         for (int r = 0; r < K; ++r) sid[rk[r]] = id[r];
-        __syncthreads();
+        block_sync();
 #pragma unroll
         for (int r = 0; r < K; ++r) jid[r] = sid[wb + r * kWave + lane];
-        __syncthreads();
+        block_sync();
       }
 #pragma unroll
       for (int r = 0; r < K; ++r)
         sh.stage[rk[r]] = packed ? ((key[r] << kc.W) | id[r]) : key[r];
-      __syncthreads();
+      block_sync();
 #pragma unroll
       for (int r = 0; r < K; ++r) {
         const int j = wb + r * kWave + lane;
@@ -481,21 +481,21 @@ __global__ __launch_bounds__(NT) void g_scatter(GArgs a, int s_arg) {
     }
 
     // ---- final pass: positions, waits and totals ------------------------
-    __syncthreads();  // counters read before the stage is written
+    block_sync();  // counters read before the stage is written
     uint32_t js[K];
     if (!packed) {
       uint32_t* sid = reinterpret_cast<uint32_t*>(sh.stage);
 #pragma unroll
       for (int r = 0; r < K; ++r) sid[rk[r]] = id[r];
-      __syncthreads();
+      block_sync();
 #pragma unroll
       for (int r = 0; r < K; ++r) js[r] = sid[wb + r * kWave + lane];
-      __syncthreads();
+      block_sync();
     }
 #pragma unroll
     for (int r = 0; r < K; ++r)
       sh.stage[rk[r]] = packed ? ((key[r] << kc.W) | id[r]) : key[r];
-    __syncthreads();
+    block_sync();
     uint64_t ks[K], ls[K];
     uint64_t wsum = 0;
 #pragma unroll
@@ -527,7 +527,7 @@ __global__ __launch_bounds__(NT) void g_scatter(GArgs a, int s_arg) {
       const int j = wb + r * kWave + lane;
       if (j < cv && (uint32_t)j == sh.excl[dg[r]]) sh.u.fin.wfirst[dg[r]] = ex_w[r];
     }
-    __syncthreads();
+    block_sync();
 #pragma unroll
     for (int r = 0; r < K; ++r) {
       const int j = wb + r * kWave + lane;
@@ -536,7 +536,7 @@ __global__ __launch_bounds__(NT) void g_scatter(GArgs a, int s_arg) {
         if (j == last) sh.u.fin.wagg[dg[r]] = ex_w[r] + ls[r] - sh.u.fin.wfirst[dg[r]];
       }
     }
-    __syncthreads();
+    block_sync();
     for (int b = t; b < nb; b += NT) {
       const uint32_t e0 = sh.excl[b], e1 = sh.excl[b + 1];
       const bool any = min((int)e0, cv) < min((int)e1, cv);
@@ -571,7 +571,7 @@ __global__ __launch_bounds__(NT) void g_scatter(GArgs a, int s_arg) {
       sh.base[b] = sh.gbase[b] + (uint32_t)cex - e0;
       sh.u.fin.wagg[b] = sh.u.fin.gw[b] + wex - (any ? sh.u.fin.wfirst[b] : 0ull);
     }
-    __syncthreads();
+    block_sync();
     int cur = -1;
     U128 acc = {0, 0};
 #pragma unroll
@@ -598,7 +598,7 @@ __global__ __launch_bounds__(NT) void g_scatter(GArgs a, int s_arg) {
   }
 
   // ---- per-kernel teardown ------------------------------------------------
-  __syncthreads();
+  block_sync();
   if (!FINAL) {
     for (int b = t; b < nb_next; b += NT) {
       const uint32_t c = sh.u.mid.ncnt[b];

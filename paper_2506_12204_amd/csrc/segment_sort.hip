@@ -106,7 +106,7 @@ __global__ __launch_bounds__(NT) void segment_schedule_kernel(SegArgs a) {
     pmin = wave_min_u32(pmin);
     pmax = wave_max_u32(pmax);
     bad = wave_or_u32(bad);
-    __syncthreads();  // previous segment's use of `red` is over
+    block_sync();  // previous segment's use of `red` is over
     if (lane == 0) {
       sh.red[0][w] = lmin;
       sh.red[1][w] = lmax;
@@ -114,7 +114,7 @@ __global__ __launch_bounds__(NT) void segment_schedule_kernel(SegArgs a) {
       sh.red[3][w] = pmax | (bad << 31);
     }
     for (int c = threadIdx.x; c < 256; c += NT) sh.cls_lo[c] = sh.cls_hi[c] = 0;
-    __syncthreads();
+    block_sync();
     lmin = 0xffffffffu;
     lmax = 0;
     pmin = 0xffu;
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(NT) void segment_schedule_kernel(SegArgs a) {
       const int shift = q * dstep;
       const int nb = min(dstep, (int)kb - shift);
       const int nbins = 1 << nb;
-      __syncthreads();  // the stage (aliased by the counters) is free
+      block_sync();  // the stage (aliased by the counters) is free
       for (int b = lane; b < nbins; b += kWave) cnt[w * STRIDE + b] = 0;
       // a wave only touches its own counter row until the next barrier
       uint32_t dg[K], rk[K];
@@ -166,16 +166,16 @@ __global__ __launch_bounds__(NT) void segment_schedule_kernel(SegArgs a) {
           rk[r] = rank_round(dg[r], nb, cnt + w * STRIDE);
         }
       }
-      __syncthreads();
+      block_sync();
       block_digit_offsets<NT>(cnt, STRIDE, nbins, sh.excl, sh.scan32);
 #pragma unroll
       for (int r = 0; r < K; ++r)
         if (r < kr) rk[r] += sh.excl[dg[r]] + cnt[w * STRIDE + dg[r]];
-      __syncthreads();  // every counter read happens before the stage writes
+      block_sync();  // every counter read happens before the stage writes
 #pragma unroll
       for (int r = 0; r < K; ++r)
         if (r < kr) sh.stage[rk[r]] = el[r];
-      __syncthreads();
+      block_sync();
 #pragma unroll
       for (int r = 0; r < K; ++r)
         if (r < kr) el[r] = sh.stage[wbase + r * kWave + lane];
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(NT) void segment_schedule_kernel(SegArgs a) {
       }
     }
     flush_run(sh.cls_lo, sh.cls_hi, cur, acc);
-    __syncthreads();
+    block_sync();
 
     // ---- totals of this queue ------------------------------------------------
     for (int c = threadIdx.x; c < a.num_classes; c += NT) {
