@@ -23,24 +23,24 @@ constexpr size_t kHeaderBytes = 256;  // flags, counters, ranges, plan
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  size_t flags = 0, done = 4, minmax = 16, tile_ctr = 32, plan = 64;
-  size_t hist_cnt = 0, hist_w = 0, cstat0 = 0, cstat1 = 0, wstat = 0;
+  size_t flags = 0, done = 4, barrier = 8, minmax = 16, plan = 64;
+  size_t hist_cnt = 0, hist_w = 0, block_hist = 0, block_histw = 0;
   size_t keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0;
   size_t total = kHeaderBytes;
   int64_t tiles = 0;
-  bool wide_status = false;
 };
 
 static_assert(sizeof(Plan) <= kHeaderBytes - 64, "plan must fit in the header");
 
 bool needs_global(int64_t n) { return n > kSegLargeCap; }
 
+// Sizes depend on n only (not on the device), so the workspace size can be
+// asked for anywhere.
 Layout layout_for(int64_t n) {
   Layout L;
   if (!needs_global(n)) return L;
   L.tiles = (n + kGlobalTile - 1) / kGlobalTile;
-  L.wide_status = n >= (int64_t(1) << 30);
-  const size_t st = L.wide_status ? 8 : 4;
+  const size_t blocks = (size_t)std::min<int64_t>(L.tiles, kMaxBlocks);
   size_t off = kHeaderBytes;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -48,10 +48,9 @@ Layout layout_for(int64_t n) {
     return at;
   };
   L.hist_cnt = take(sizeof(uint32_t) * kMaxScatter * kMaxBins);
-  L.hist_w = take(sizeof(uint64_t) * kMaxScatter * kMaxBins);
-  L.cstat0 = take(st * L.tiles * kMaxBins);
-  L.cstat1 = take(st * L.tiles * kMaxBins);
-  L.wstat = take(8 * L.tiles * kMaxBins);
+  L.hist_w = take(sizeof(uint64_t) * kMaxBins);
+  L.block_hist = take(sizeof(uint32_t) * kMaxBins * blocks);
+  L.block_histw = take(sizeof(uint64_t) * kMaxBins * blocks);
   L.keys0 = take(8 * (size_t)n);
   L.keys1 = take(8 * (size_t)n);
   L.ids0 = take(4 * (size_t)n);
@@ -60,8 +59,6 @@ Layout layout_for(int64_t n) {
   return L;
 }
 
-// Width of the first (low-length) digit of the global path, 8..10 bits.
-// SEMSCHED_D0 overrides the default; it is read on every call.
 int d0_bits() {
   const char* e = std::getenv("SEMSCHED_D0");
   const int d = e ? std::atoi(e) : 8;
@@ -88,6 +85,7 @@ int num_cus() {
 }
 
 int map_flags(uint32_t f) {
+  if (f & kFlagDevice) return SEM_EDEVICE;
   if (f & kFlagInval) return SEM_EINVAL;
   if (f & kFlagRange) return SEM_ERANGE;
   return SEM_OK;
@@ -190,18 +188,18 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   g.num_classes = num_classes;
   g.d0 = d0_bits();
   g.tiles = (int32_t)L.tiles;
-  g.wide_status = L.wide_status ? 1 : 0;
   g.force_wide = force_wide();
+  g.main = global_split(n);
+  g.mid = global_mid_split(n);
   g.flags = reinterpret_cast<uint32_t*>(base + L.flags);
   g.done = reinterpret_cast<uint32_t*>(base + L.done);
+  g.barrier = reinterpret_cast<uint32_t*>(base + L.barrier);
   g.minmax = reinterpret_cast<uint32_t*>(base + L.minmax);
-  g.tile_ctr = reinterpret_cast<uint32_t*>(base + L.tile_ctr);
   g.plan = reinterpret_cast<Plan*>(base + L.plan);
   g.hist_cnt = reinterpret_cast<uint32_t*>(base + L.hist_cnt);
   g.hist_w = reinterpret_cast<uint64_t*>(base + L.hist_w);
-  g.cstat[0] = base + L.cstat0;
-  g.cstat[1] = base + L.cstat1;
-  g.wstat = reinterpret_cast<uint64_t*>(base + L.wstat);
+  g.block_hist = reinterpret_cast<uint32_t*>(base + L.block_hist);
+  g.block_histw = reinterpret_cast<uint64_t*>(base + L.block_histw);
   g.keys[0] = reinterpret_cast<uint64_t*>(base + L.keys0);
   g.keys[1] = reinterpret_cast<uint64_t*>(base + L.keys1);
   g.ids[0] = reinterpret_cast<uint32_t*>(base + L.ids0);

@@ -9,6 +9,7 @@ namespace semsched {
 // Device-detected error bits, OR-ed into the workspace's first word.
 constexpr uint32_t kFlagInval = 1u;  // bad offsets / queue longer than promised
 constexpr uint32_t kFlagRange = 2u;  // length < 0 or priority >= num_classes
+constexpr uint32_t kFlagDevice = 4u; // a grid barrier timed out (workgroups not co-resident)
 
 // Queue-size classes of the LDS path (one workgroup per queue).
 constexpr int kSegTinyCap = 256;      // 64 threads x 4 rounds
@@ -40,8 +41,9 @@ hipError_t launch_segment_schedule(SegArgs a, SegSize size, int grid, hipStream_
 constexpr int kMaxBins = 1024;   // digit bins of every scatter pass
 constexpr int kMaxScatter = 5;   // scatter passes: first, up to 3 middle, final
 constexpr int kGlobalThreads = 512;
-constexpr int kGlobalRounds = 16;
+constexpr int kGlobalRounds = 8;
 constexpr int kGlobalTile = kGlobalThreads * kGlobalRounds;
+constexpr int kMaxBlocks = 4096; // upper bound on workgroups of a pass
 
 // Decided on the device by the histogram pass once the ranges are known.
 struct Plan {
@@ -59,6 +61,12 @@ struct Plan {
   uint32_t nbins[kMaxScatter];
 };
 
+// A pass's work split: workgroup g owns tiles [g*tpb, min(tiles, (g+1)*tpb)).
+struct Split {
+  int32_t blocks;
+  int32_t tpb;
+};
+
 struct GArgs {
   const uint8_t* priority;
   const int32_t* length;
@@ -69,17 +77,18 @@ struct GArgs {
   int32_t num_classes;
   int32_t d0;           // width of the first (low-length) digit
   int32_t tiles;
-  int32_t wide_status;  // 1: count status words are u64
   int32_t force_wide;   // 1: never pack the id into the key word
+  Split main;           // histogram, first and final passes
+  Split mid;            // the cooperative middle-pass kernel
   uint32_t* flags;
   uint32_t* done;
+  uint32_t* barrier;    // arrivals at the middle-pass grid barriers
   uint32_t* minmax;     // pmin, pmax, lmin, lmax
-  uint32_t* tile_ctr;   // one per scatter pass
   Plan* plan;
-  uint32_t* hist_cnt;   // [kMaxScatter][kMaxBins]
-  uint64_t* hist_w;     // [kMaxScatter][kMaxBins]
-  void* cstat[2];       // count look-back status, tiles * kMaxBins words each
-  uint64_t* wstat;      // weight look-back status, tiles * kMaxBins
+  uint32_t* hist_cnt;   // [kMaxScatter][kMaxBins] digit totals of every pass
+  uint64_t* hist_w;     // [kMaxBins] length sums of the final digit
+  uint32_t* block_hist; // [blocks][kMaxBins] digit counts per block, then offsets
+  uint64_t* block_histw;// [blocks][kMaxBins] final-digit length sums, then offsets
   uint64_t* keys[2];
   uint32_t* ids[2];
 };
@@ -90,6 +99,9 @@ struct StageEvents {
   hipEvent_t after[3];
 };
 
+// Work splits of the passes for n requests (device-dependent occupancy).
+Split global_split(int64_t n);
+Split global_mid_split(int64_t n);
 hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEvents* ev);
 
 // Zeroes `count` 32-bit words (graph-safe replacement for a memset).
