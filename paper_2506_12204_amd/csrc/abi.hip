@@ -23,8 +23,8 @@ constexpr size_t kHeaderBytes = 256;  // flags, counters, ranges, plan
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  size_t flags = 0, done = 4, barrier = 8, minmax = 16, plan = 64;
-  size_t hist_cnt = 0, hist_w = 0, block_hist = 0, block_histw = 0;
+  size_t flags = 0, barrier = 8, plan = 64;
+  size_t hist_cnt = 0, hist_w = 0, block_hist = 0, block_histw = 0, block_ranges = 0;
   size_t keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0;
   size_t total = kHeaderBytes;
   int64_t tiles = 0;
@@ -51,6 +51,7 @@ Layout layout_for(int64_t n) {
   L.hist_w = take(sizeof(uint64_t) * kMaxBins);
   L.block_hist = take(sizeof(uint32_t) * kMaxBins * blocks);
   L.block_histw = take(sizeof(uint64_t) * kMaxBins * blocks);
+  L.block_ranges = take(sizeof(uint32_t) * 4 * blocks);
   L.keys0 = take(8 * (size_t)n);
   L.keys1 = take(8 * (size_t)n);
   L.ids0 = take(4 * (size_t)n);
@@ -192,9 +193,8 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   g.main = global_split(n);
   g.mid = global_mid_split(n);
   g.flags = reinterpret_cast<uint32_t*>(base + L.flags);
-  g.done = reinterpret_cast<uint32_t*>(base + L.done);
   g.barrier = reinterpret_cast<uint32_t*>(base + L.barrier);
-  g.minmax = reinterpret_cast<uint32_t*>(base + L.minmax);
+  g.block_ranges = reinterpret_cast<uint32_t*>(base + L.block_ranges);
   g.plan = reinterpret_cast<Plan*>(base + L.plan);
   g.hist_cnt = reinterpret_cast<uint32_t*>(base + L.hist_cnt);
   g.hist_w = reinterpret_cast<uint64_t*>(base + L.hist_w);

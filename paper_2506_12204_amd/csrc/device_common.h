@@ -34,10 +34,13 @@ __device__ __forceinline__ uint64_t lanes_below() { return __lanemask_lt(); }
 // every caller: invalid items carry a sentinel digit instead of idling).
 __device__ __forceinline__ uint64_t match_digit(uint32_t d, int nbits) {
   uint64_t peers = ~0ull;
-  for (int b = 0; b < nbits; ++b) {
-    const bool set = (d >> b) & 1u;
-    const uint64_t m = __ballot(set);
-    peers &= set ? m : ~m;
+#pragma unroll
+  for (int b = 0; b < 10; ++b) {  // digits have at most 10 bits
+    if (b < nbits) {
+      const bool set = (d >> b) & 1u;
+      const uint64_t m = __ballot(set);
+      peers &= set ? m : ~m;
+    }
   }
   return peers;
 }
@@ -57,6 +60,35 @@ __device__ __forceinline__ uint32_t rank_round(uint32_t d, int nbits,
   return base + below;
 }
 
+// Inclusive scan of a 32-bit value over the wave with DPP lane moves: four
+// row_shr steps scan each row of 16 lanes, then row_bcast:15 and
+// row_bcast:31 carry the row totals into the rows above. Lanes whose source
+// is outside the row (or whose row is masked off) add 0.
+__device__ __forceinline__ uint32_t wave_incl_scan_dpp(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+
+// Exact inclusive wave scan of 32-bit values (lengths) into 64 bits: the low
+// and high 16-bit halves are scanned separately, each sum staying below 2^22.
+__device__ __forceinline__ uint64_t wave_incl_scan_len(uint32_t v) {
+  const uint32_t lo = wave_incl_scan_dpp(v & 0xffffu);
+  const uint32_t hi = wave_incl_scan_dpp(v >> 16);
+  return ((uint64_t)hi << 16) + lo;
+}
+
+// Value of lane 63 (the wave total after an inclusive scan).
+__device__ __forceinline__ uint64_t last_lane_u64(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+  return ((uint64_t)hi << 32) | lo;
+}
+
 // Inclusive wave scan of a 64-bit value.
 __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
 #pragma unroll
@@ -67,14 +99,7 @@ __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
   return v;
 }
 
-__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const uint32_t o = __shfl_up(v, off, kWave);
-    if (lane_id() >= off) v += o;
-  }
-  return v;
-}
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) { return wave_incl_scan_dpp(v); }
 
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
 #pragma unroll

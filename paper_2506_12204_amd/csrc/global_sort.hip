@@ -17,8 +17,10 @@
 //   g_hist0   read (priority, length) once: validate, find the ranges and
 //             count the low `d0` bits of every length per block. That digit
 //             does not depend on the ranges, so no separate min/max pass is
-//             needed. The last workgroup writes the Plan.
-//   g_scan    per-block digit offsets of one pass (column scans).
+//             needed.
+//   g_scan    per-block digit offsets of one pass (column scans); for the
+//             first pass one more workgroup reduces the block ranges into
+//             the Plan.
 //   g_first   first scatter pass: packs every request into one u64 element
 //               (p - pmin | (len >> d0) - hmin | len & (2^d0 - 1) | id)
 //             and scatters it by the low length digit.
@@ -50,12 +52,7 @@ __global__ __launch_bounds__(1024) void g_reset(GArgs a) {
   const int t = threadIdx.x;
   if (t == 0) {
     a.flags[0] = 0;
-    a.done[0] = 0;
     a.barrier[0] = 0;
-    a.minmax[0] = 0xffu;        // pmin
-    a.minmax[1] = 0;            // pmax
-    a.minmax[2] = 0xffffffffu;  // lmin
-    a.minmax[3] = 0;            // lmax
     a.plan->ok = 0;
   }
   for (int i = t; i < kMaxScatter * kMaxBins; i += 1024) a.hist_cnt[i] = 0;
@@ -67,6 +64,8 @@ __global__ __launch_bounds__(1024) void g_reset(GArgs a) {
 // Pass 0: ranges, validation and the first digit's per-block histogram.
 
 constexpr int HT = 512;  // threads of the histogram passes
+constexpr int SCT = 256;  // threads of the column scans
+constexpr int SCT_WAVES = SCT / kWave;
 constexpr int HU = 8;    // loads in flight per thread
 
 struct Ranges {
@@ -83,14 +82,39 @@ struct Ranges {
   }
 };
 
-__device__ void write_plan(const GArgs& a) {
-  const uint32_t fl = load_agent(a.flags);
-  const uint32_t gpmin = load_agent(&a.minmax[0]);
-  const uint32_t gpmax = load_agent(&a.minmax[1]);
-  const uint32_t glmin = load_agent(&a.minmax[2]);
-  const uint32_t glmax = load_agent(&a.minmax[3]);
+// Reduce the block ranges and turn them into the Plan (one workgroup).
+__device__ void write_plan(const GArgs& a, int G) {
+  __shared__ uint32_t s_red[4][SCT_WAVES];
+  uint32_t pl_ = 0xffu, ph = 0, ll = 0xffffffffu, lh = 0;
+  for (int g = threadIdx.x; g < G; g += SCT) {
+    const uint32_t* r = a.block_ranges + 4 * (size_t)g;
+    pl_ = min(pl_, r[0]);
+    ph = max(ph, r[1]);
+    ll = min(ll, r[2]);
+    lh = max(lh, r[3]);
+  }
+  pl_ = wave_min_u32(pl_);
+  ph = wave_max_u32(ph);
+  ll = wave_min_u32(ll);
+  lh = wave_max_u32(lh);
+  const int w = threadIdx.x / kWave;
+  if (lane_id() == 0) {
+    s_red[0][w] = pl_;
+    s_red[1][w] = ph;
+    s_red[2][w] = ll;
+    s_red[3][w] = lh;
+  }
+  block_sync();
+  if (threadIdx.x != 0) return;
+  uint32_t gpmin = 0xffu, gpmax = 0, glmin = 0xffffffffu, glmax = 0;
+  for (int i = 0; i < SCT_WAVES; ++i) {
+    gpmin = min(gpmin, s_red[0][i]);
+    gpmax = max(gpmax, s_red[1][i]);
+    glmin = min(glmin, s_red[2][i]);
+    glmax = max(glmax, s_red[3][i]);
+  }
   Plan* pl = a.plan;
-  if (fl != 0) {
+  if (load_agent(a.flags) != 0) {
     pl->ok = 0;
     return;
   }
@@ -136,7 +160,6 @@ __global__ __launch_bounds__(HT) void g_hist0(GArgs a, int vec_ok) {
   constexpr int HW = HT / kWave;
   __shared__ uint32_t s_hist[kMaxBins];
   __shared__ uint32_t s_red[4][HW];
-  __shared__ uint32_t s_last;
   const int t = threadIdx.x;
   const int g = blockIdx.x;
   const int nb = 1 << a.d0;
@@ -197,31 +220,19 @@ __global__ __launch_bounds__(HT) void g_hist0(GArgs a, int vec_ok) {
       bb |= s_red[3][i] >> 31;
     }
     if (bb) atomicOr(a.flags, kFlagRange);
-    if (hi > lo) {
-      atomicMin(&a.minmax[0], pl);
-      atomicMax(&a.minmax[1], ph);
-      atomicMin(&a.minmax[2], bl);
-      atomicMax(&a.minmax[3], bh);
-    }
+    uint32_t* r = a.block_ranges + 4 * (size_t)g;
+    r[0] = pl;  // an empty block leaves the neutral values
+    r[1] = ph;
+    r[2] = bl;
+    r[3] = bh;
   }
   for (int b = t; b < nb; b += HT) a.block_hist[(size_t)g * kMaxBins + b] = s_hist[b];
-
-  // The last workgroup to finish turns the ranges into the Plan.
-  __threadfence();
-  block_sync();
-  if (t == 0) s_last = (atomicAdd(a.done, 1u) == gridDim.x - 1) ? 1u : 0u;
-  block_sync();
-  if (!s_last || t != 0) return;
-  __threadfence();
-  write_plan(a);
 }
 
 // ------------------------------------------------------------------------
 // Column scans: block_hist[g][b] becomes the count of digit b in blocks
 // before g (block_histw likewise for length sums); the totals go to
 // hist_cnt[s][b] (and hist_w[b]).
-
-constexpr int SCT = 256;
 
 template <int THREADS>
 __device__ void column_scan(const GArgs& a, int s, int b, bool weights, int G,
@@ -265,15 +276,25 @@ __device__ void column_scan(const GArgs& a, int s, int b, bool weights, int G,
 }
 
 // final != 0: scan the final pass (its index and bin count come from the Plan).
-__global__ __launch_bounds__(SCT) void g_scan(GArgs a, int s_arg, int final) {
+// Pass 0 (final == 0): workgroups 0 .. 2^d0-1 scan the first digit's bins
+// and workgroup 2^d0 writes the Plan. Final pass: one workgroup per bin.
+__global__ __launch_bounds__(SCT) void g_scan(GArgs a, int final) {
   __shared__ uint32_t scan32[SCT / kWave + 1];
   __shared__ uint64_t scan64[SCT / kWave + 1];
+  const int b = blockIdx.x;
+  if (!final) {
+    if (b == (1 << a.d0)) {
+      write_plan(a, a.main.blocks);
+      return;
+    }
+    column_scan<SCT>(a, 0, b, false, a.main.blocks, scan32, scan64);
+    return;
+  }
   const Plan* pl = a.plan;
   if (!pl->ok) return;
-  const int s = final ? (int)pl->nscatter - 1 : s_arg;
-  const int b = blockIdx.x;
+  const int s = (int)pl->nscatter - 1;
   if (b >= (int)pl->nbins[s]) return;
-  column_scan<SCT>(a, s, b, final != 0, a.main.blocks, scan32, scan64);
+  column_scan<SCT>(a, s, b, true, a.main.blocks, scan32, scan64);
 }
 
 // ------------------------------------------------------------------------
@@ -736,7 +757,7 @@ __global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
       if (j < cv) wsum += kc.len(packed ? (el[r] >> kc.W) : el[r]);
     }
     uint64_t wtot = wave_incl_scan_u64(wsum);
-    wtot = __shfl(wtot, kWave - 1, kWave);
+    wtot = last_lane_u64(wtot);
     uint64_t dummy;
     uint64_t run = block_excl_scan_u64<NT>(lane == 0 ? wtot : 0, sh.scan64, dummy);
     run = __shfl(run, 0, kWave);
@@ -747,10 +768,10 @@ __global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
       const int j = wb + r * kWave + lane;
       const bool valid = j < cv;
       const uint64_t key = packed ? (el[r] >> kc.W) : el[r];
-      const uint64_t ls = valid ? kc.len(key) : 0ull;
-      const uint64_t incl = wave_incl_scan_u64(ls);
+      const uint32_t ls = valid ? kc.len(key) : 0u;
+      const uint64_t incl = wave_incl_scan_len(ls);
       const uint64_t ex = run + incl - ls;
-      run += __shfl(incl, kWave - 1, kWave);
+      run += last_lane_u64(incl);
       if (valid) {
         const uint32_t d = digit_of(key);
         const uint32_t pos = sh.excl[d] + (uint32_t)j;
@@ -843,13 +864,13 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   mark(ev, 0, false, st);
   hipLaunchKernelGGL(g_hist0, gm, dim3(HT), 0, st, a, vec_ok);
   mark(ev, 0, true, st);
-  hipLaunchKernelGGL(g_scan, dim3(1u << a.d0), dim3(SCT), 0, st, a, 0, 0);
+  hipLaunchKernelGGL(g_scan, dim3((1u << a.d0) + 1), dim3(SCT), 0, st, a, 0);
   mark(ev, 1, false, st);
   hipLaunchKernelGGL(g_first<>, gm, dim3(NT), 0, st, a);
   mark(ev, 1, true, st);
   hipLaunchKernelGGL(g_mid, dim3(a.mid.blocks), dim3(NT), 0, st, a);
   hipLaunchKernelGGL(g_histF, gm, dim3(HT), 0, st, a);
-  hipLaunchKernelGGL(g_scan, dim3(kMaxBins), dim3(SCT), 0, st, a, 0, 1);
+  hipLaunchKernelGGL(g_scan, dim3(kMaxBins), dim3(SCT), 0, st, a, 1);
   mark(ev, 2, false, st);
   hipLaunchKernelGGL(g_final<>, gm, dim3(NT), 0, st, a);
   mark(ev, 2, true, st);

@@ -81,9 +81,8 @@ struct GArgs {
   Split main;           // histogram, first and final passes
   Split mid;            // the cooperative middle-pass kernel
   uint32_t* flags;
-  uint32_t* done;
   uint32_t* barrier;    // arrivals at the middle-pass grid barriers
-  uint32_t* minmax;     // pmin, pmax, lmin, lmax
+  uint32_t* block_ranges;  // [blocks][4] pmin, pmax, lmin, lmax of every block
   Plan* plan;
   uint32_t* hist_cnt;   // [kMaxScatter][kMaxBins] digit totals of every pass
   uint64_t* hist_w;     // [kMaxBins] length sums of the final digit

@@ -194,7 +194,7 @@ __global__ __launch_bounds__(NT) void segment_schedule_kernel(SegArgs a) {
     }
     // wave totals -> exclusive offsets of the waves
     uint64_t wtot = wave_incl_scan_u64(wsum);
-    wtot = __shfl(wtot, kWave - 1, kWave);
+    wtot = last_lane_u64(wtot);
     uint64_t dummy;
     uint64_t run = block_excl_scan_u64<NT>(lane == 0 ? wtot : 0, sh.scan64, dummy);
     run = __shfl(run, 0, kWave);
@@ -205,9 +205,9 @@ __global__ __launch_bounds__(NT) void segment_schedule_kernel(SegArgs a) {
     for (int r = 0; r < K; ++r) {
       if (r < kr) {
         const int j = wbase + r * kWave + lane;
-        const uint64_t incl = wave_incl_scan_u64(len_s[r]);
+        const uint64_t incl = wave_incl_scan_len((uint32_t)len_s[r]);
         const uint64_t wt = run + incl - len_s[r];
-        run += __shfl(incl, kWave - 1, kWave);
+        run += last_lane_u64(incl);
         if (j < m) {
           const uint64_t key = el[r] >> kIdBits;
           const int cls = (int)((key >> wl) + pmin);
