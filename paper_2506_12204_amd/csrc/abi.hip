@@ -62,7 +62,7 @@ Layout layout_for(int64_t n) {
 
 int d0_bits() {
   const char* e = std::getenv("SEMSCHED_D0");
-  const int d = e ? std::atoi(e) : 8;
+  const int d = e ? std::atoi(e) : 10;
   return std::min(10, std::max(8, d));
 }
 
@@ -190,7 +190,8 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   g.d0 = d0_bits();
   g.tiles = (int32_t)L.tiles;
   g.force_wide = force_wide();
-  g.main = global_split(n);
+  g.main = global_first_split(n);
+  g.fin = global_final_split(n);
   g.mid = global_mid_split(n);
   g.flags = reinterpret_cast<uint32_t*>(base + L.flags);
   g.barrier = reinterpret_cast<uint32_t*>(base + L.barrier);

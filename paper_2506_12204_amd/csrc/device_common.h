@@ -10,6 +10,15 @@ namespace semsched {
 
 constexpr int kWave = 64;
 
+// Integer types that may alias any other type. LDS buffers are reused with
+// different element widths (u16 counters in a u64 stage, u16 counters cleared
+// a u64 at a time, two u16 counters read as one u32); accesses through these
+// types keep the compiler from reordering them past accesses of the other
+// width, which strict aliasing would otherwise allow.
+typedef uint64_t __attribute__((may_alias)) u64_alias;
+typedef uint32_t __attribute__((may_alias)) u32_alias;
+typedef uint16_t __attribute__((may_alias)) u16_alias;
+
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
 // Workgroup barrier that first drains this wave's outstanding LDS operations.
@@ -60,6 +69,49 @@ __device__ __forceinline__ uint32_t rank_round(uint32_t d, int nbits,
   return base + below;
 }
 
+// match_digit for a digit width known at compile time. Per bit: the lane's
+// bit as a 0/-1 mask, its ballot, and one three-input bit operation per half
+// that ORs (ballot XOR mask) -- the lanes whose bit differs -- into the
+// accumulated mismatch set. Four VALU operations per bit. The empty asm keeps
+// the compiler from recomputing the ballot's predicate by other means.
+template <int NB>
+__device__ __forceinline__ uint64_t match_digit_c(uint32_t d) {
+  uint32_t lo = 0, hi = 0;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)d, b, 1);
+    asm("" : "+v"(m));
+    const uint64_t bal = __builtin_amdgcn_ballot_w64(m != 0);
+    // 0xF6 = A | (B ^ C) for sources (A, B, C)
+    lo = __builtin_amdgcn_bitop3_b32(lo, (uint32_t)bal, m, 0xF6);
+    hi = __builtin_amdgcn_bitop3_b32(hi, (uint32_t)(bal >> 32), m, 0xF6);
+  }
+  return ~(((uint64_t)hi << 32) | lo);
+}
+
+// rank_round for a compile-time digit width. Every peer writes the same new
+// count, so no lane has to be singled out for the update.
+template <int NB>
+__device__ __forceinline__ uint32_t rank_round_c(uint32_t d, uint16_t* cnt) {
+  const uint64_t peers = match_digit_c<NB>(d);
+  const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+      (uint32_t)(peers >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
+  const uint32_t base = cnt[d];
+  cnt[d] = (uint16_t)(base + (uint32_t)__popcll(peers));
+  uint32_t rank = base + below;
+  // settle the rank now: left to itself the compiler keeps the count, the
+  // peer mask and the address of every round alive until their last use
+  asm volatile("" : "+v"(rank));
+  return rank;
+}
+
+// Hides a value's origin from the optimiser, so that an address derived from
+// it is recomputed after a barrier instead of being kept in a register.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 // Inclusive scan of a 32-bit value over the wave with DPP lane moves: four
 // row_shr steps scan each row of 16 lanes, then row_bcast:15 and
 // row_bcast:31 carry the row totals into the rows above. Lanes whose source
@@ -80,6 +132,14 @@ __device__ __forceinline__ uint64_t wave_incl_scan_len(uint32_t v) {
   const uint32_t lo = wave_incl_scan_dpp(v & 0xffffu);
   const uint32_t hi = wave_incl_scan_dpp(v >> 16);
   return ((uint64_t)hi << 16) + lo;
+}
+
+// Exact inclusive wave scan of values below 2^40 (per-thread sums of a few
+// bins' length totals): two 20-bit parts, each sum staying below 2^26.
+__device__ __forceinline__ uint64_t wave_incl_scan_u40(uint64_t v) {
+  const uint32_t lo = wave_incl_scan_dpp((uint32_t)v & 0xfffffu);
+  const uint32_t hi = wave_incl_scan_dpp((uint32_t)(v >> 20));
+  return ((uint64_t)hi << 20) + lo;
 }
 
 // Value of lane 63 (the wave total after an inclusive scan).

@@ -124,15 +124,19 @@ __device__ void write_plan(const GArgs& a, int G) {
   const uint32_t H = (glmax >> d0) - hmin + 1;
   const uint32_t wp = bit_width32(P - 1);
   const uint32_t wh = bit_width32(H - 1);
-  const uint32_t W = bit_width32((uint32_t)(a.n - 1));
+  const uint32_t wid = bit_width32((uint32_t)(a.n - 1));
+  const uint32_t kb = wp + wh + d0;  // live key bits
   pl->pmin = gpmin;
   pl->P = P;
   pl->hmin = hmin;
   pl->H = H;
   pl->wp = wp;
   pl->wh = wh;
-  pl->W = W;
-  pl->packed = (!a.force_wide && wp + wh + d0 + W <= 64) ? 1u : 0u;
+  // A key of at most 32 bits sits in the high word above a 32-bit id, so no
+  // shifts across words are needed to take an element apart.
+  pl->W = (!a.force_wide && kb <= 32) ? 32u : wid;
+  pl->packed = (!a.force_wide && kb + pl->W <= 64) ? 1u : 0u;
+  pl->small = glmax < (1u << 26) ? 1u : 0u;
   const uint64_t R = (uint64_t)P * H;  // <= 2^31 because d0 >= 8
   pl->shift[0] = 0;
   pl->nbits[0] = d0;
@@ -294,7 +298,7 @@ __global__ __launch_bounds__(SCT) void g_scan(GArgs a, int final) {
   if (!pl->ok) return;
   const int s = (int)pl->nscatter - 1;
   if (b >= (int)pl->nbins[s]) return;
-  column_scan<SCT>(a, s, b, true, a.main.blocks, scan32, scan64);
+  column_scan<SCT>(a, s, b, true, a.fin.blocks, scan32, scan64);
 }
 
 // ------------------------------------------------------------------------
@@ -340,7 +344,7 @@ __device__ __forceinline__ void rank_tile(const uint32_t (&dg)[K], uint32_t (&rk
   const int w = threadIdx.x / kWave;
   for (int b = lane_id(); b < nb; b += kWave) cnt[w * kMaxBins + b] = 0;
 #pragma unroll
-  for (int r = 0; r < K; ++r) rk[r] = rank_round(dg[r], nbits, cnt + w * kMaxBins);
+  for (int r = 0; r < K; ++r) rk[r] = rank_round_c<10>(dg[r], cnt + w * kMaxBins);
   block_sync();
   block_digit_offsets<NT>(cnt, kMaxBins, nb, excl, scan32);
 #pragma unroll
@@ -382,7 +386,7 @@ __device__ __forceinline__ void stage_and_scatter(uint64_t* stage, const uint32_
   const int lane = lane_id();
   uint32_t jid[K];
   if (!packed) {
-    uint32_t* sid = reinterpret_cast<uint32_t*>(stage);
+    u32_alias* sid = reinterpret_cast<u32_alias*>(stage);
 #pragma unroll
     for (int r = 0; r < K; ++r) sid[rk[r]] = id[r];
     block_sync();
@@ -417,7 +421,7 @@ struct ScatterShared {
 // One block of a first (s == 0) or middle scatter pass.
 template <bool FIRST>
 __device__ void scatter_block(const GArgs& a, int s, int g, Split sp, ScatterShared& sh) {
-  uint16_t* cnt = reinterpret_cast<uint16_t*>(sh.stage);
+  u16_alias* cnt = reinterpret_cast<u16_alias*>(sh.stage);
   const Plan* pl = a.plan;
   const int t = threadIdx.x;
   const int lane = lane_id();
@@ -483,15 +487,213 @@ __device__ void scatter_block(const GArgs& a, int s, int g, Split sp, ScatterSha
   }
 }
 
+// ---- fast first pass --------------------------------------------------------
+// Keys of at most 32 bits (the element's high word), a first digit of D0 bits
+// known at compile time. The pass works on big tiles of kFirstTiles tiles
+// (16384 items, one workgroup per CU, a 128 KB stage): with up to 1024
+// digits a big tile still writes runs of about 16 consecutive elements per
+// digit, so the scattered writes mostly fill whole cache lines. Per big tile:
+// rank the R1 rounds of every wave against the wave's own counters, turn the
+// counters into tile offsets (owners of the digits scan them across the waves
+// and the block), stage the tile in digit order and write it out at the
+// running digit offsets. Four barriers per big tile; the next tile's inputs
+// are loaded while this one is offset, staged and written.
+
+constexpr int R1 = K * kFirstTiles;  // rounds per thread of a big tile
+constexpr int T1 = NT * R1;          // items of a big tile
+
+template <int D0>
+struct FirstFastShared {
+  uint64_t stage[T1];
+  uint16_t cnt[NW][1 << D0];  // wave counters, then the waves' tile offsets
+  uint32_t base[1 << D0];     // output position of the tile's first item of a digit
+  uint32_t part[NW + 1];      // wave totals of the block scans
+};
+
+// Index of this thread's wave, as a value the compiler knows to be uniform
+// (so that per-wave bases live in scalar registers and per-round addresses
+// are immediate offsets from one lane offset).
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+}
+
+// Buffer resource over `bytes` bytes at `base` (raw, untyped). Loads through
+// it return 0 past the end instead of touching memory there.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000 /* 32-bit data format, gfx9 */);
+}
+
+// Inputs of one big tile of `cnt` items starting at item tb, round-major per
+// wave (round r of wave w holds items w*64*R1 + r*64 + lane). Items past the
+// tile's end read as zero.
+__device__ __forceinline__ void load_first(const GArgs& a, int64_t tb, int cnt,
+                                           uint32_t (&pv)[R1], uint32_t (&lv)[R1]) {
+  const int wb = wave_id() * kWave * R1;
+  // items of this wave's share (uniform; stated so the descriptor stays scalar)
+  const int lim = __builtin_amdgcn_readfirstlane(max(0, min(cnt - wb, kWave * R1)));
+  const __amdgpu_buffer_rsrc_t rp = raw_rsrc(a.priority + tb + wb, (uint32_t)lim);
+  const __amdgpu_buffer_rsrc_t rl = raw_rsrc(a.length + tb + wb, (uint32_t)lim * 4u);
+  const int lane = lane_id();
+#pragma unroll
+  for (int r = 0; r < R1; ++r) {
+    // the whole offset goes in the vector operand: only that part (with the
+    // immediate) is range-checked, the scalar offset is not
+    pv[r] = __builtin_amdgcn_raw_buffer_load_b8(rp, lane + r * kWave, 0, 0);
+    lv[r] = __builtin_amdgcn_raw_buffer_load_b32(rl, (lane + r * kWave) * 4, 0, 0);
+  }
+}
+
+// Clears this wave's NBIN u16 counters.
+template <int NBIN>
+__device__ __forceinline__ void clear_wave_counters(uint16_t* cnt) {
+  static_assert(NBIN % (kWave * 4) == 0, "whole u64 words per lane");
+  u64_alias* c64 = reinterpret_cast<u64_alias*>(cnt);
+#pragma unroll
+  for (int i = 0; i < NBIN / (kWave * 4); ++i) c64[i * kWave + lane_id()] = 0;
+}
+
+template <int D0>
+__device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
+  constexpr int NBIN = 1 << D0;
+  constexpr uint32_t M0 = NBIN - 1;
+  constexpr int OWN = NBIN > NT ? NBIN / NT : 1;  // digits per owning thread
+  constexpr int OWNERS = NBIN / OWN;
+  const int t = threadIdx.x;
+  const int lane = lane_id();
+  const int w = wave_id();
+  const int wb = w * kWave * R1;
+  const bool owner = t < OWNERS;
+  const Plan* pl = a.plan;
+  const uint32_t pmin = pl->pmin;
+  const uint32_t psh = pl->wh + D0;
+  const uint32_t hoff = pl->hmin << D0;
+  uint64_t* out = a.keys[0];
+  uint16_t* mycnt = sh.cnt[w];
+  clear_wave_counters<NBIN>(mycnt);
+
+  // running output offset of each owned digit: its global base plus the
+  // counts of the blocks before this one
+  uint32_t carry[OWN];
+  {
+    uint32_t c[OWN];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      c[i] = owner ? a.hist_cnt[t * OWN + i] : 0u;
+      sum += c[i];
+    }
+    uint32_t tot;
+    uint32_t ex = block_excl_scan_u32<NT>(sum, sh.part, tot);
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      carry[i] = ex + (owner ? a.block_hist[(size_t)g * kMaxBins + t * OWN + i] : 0u);
+      ex += c[i];
+    }
+  }
+
+  // this block's items: tiles [g * tpb, (g + 1) * tpb), tpb a multiple of kFirstTiles
+  const int64_t lo = (int64_t)g * a.main.tpb * T;
+  const int64_t hi = min(a.n, lo + (int64_t)a.main.tpb * T);
+  uint32_t pv[R1], lv[R1];
+  load_first(a, lo, (int)min((int64_t)T1, hi - lo), pv, lv);
+  for (int64_t tb = lo; tb < hi; tb += T1) {
+    const int cv = (int)min((int64_t)T1, hi - tb);
+    // key = (p - pmin) << (wh + d0) | ((l >> d0) - hmin) << d0 | (l & M0); its
+    // low D0 bits are the digit
+    uint32_t key[R1], rk[R1];
+#pragma unroll
+    for (int r = 0; r < R1; ++r) key[r] = ((pv[r] - pmin) << psh) + (lv[r] - hoff);
+    if (cv < T1) {
+      // items past the end take the last digit: they rank after every real
+      // item of it, i.e. at the tile positions >= cv, which are not written
+#pragma unroll
+      for (int r = 0; r < R1; ++r)
+        if (wb + r * kWave + lane >= cv) key[r] |= M0;
+    }
+
+#pragma unroll
+    for (int r = 0; r < R1; ++r) rk[r] = rank_round_c<D0>(key[r] & M0, mycnt);
+    // the next tile's inputs load while this one is offset, staged and written
+    if (tb + T1 < hi) load_first(a, tb + T1, (int)min((int64_t)T1, hi - tb - T1), pv, lv);
+    block_sync();  // every wave's counters are complete
+
+    uint32_t cw[OWN][NW], tot[OWN];
+    uint32_t local = 0;
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      tot[i] = 0;
+#pragma unroll
+      for (int v = 0; v < NW; ++v) {
+        cw[i][v] = owner ? sh.cnt[v][t * OWN + i] : 0u;
+        tot[i] += cw[i][v];
+      }
+      local += tot[i];
+    }
+    const uint32_t incl = wave_incl_scan_u32(local);
+    if (lane == kWave - 1) sh.part[w] = incl;
+    block_sync();
+    uint32_t ex = incl - local;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) ex += v < w ? sh.part[v] : 0u;
+    if (owner) {
+#pragma unroll
+      for (int i = 0; i < OWN; ++i) {
+        const int b = t * OWN + i;
+        uint32_t run = ex;
+#pragma unroll
+        for (int v = 0; v < NW; ++v) {
+          sh.cnt[v][b] = (uint16_t)run;
+          run += cw[i][v];
+        }
+        sh.base[b] = carry[i] - ex;
+        carry[i] += tot[i];
+        ex += tot[i];
+      }
+    }
+    block_sync();  // tile offsets and bases are written
+
+#pragma unroll
+    for (int r = 0; r < R1; ++r) rk[r] += mycnt[opaque(key[r]) & M0];
+    clear_wave_counters<NBIN>(mycnt);  // only this wave reads them until the next ranking
+#pragma unroll
+    for (int r = 0; r < R1; ++r)
+      sh.stage[rk[r]] = ((uint64_t)key[r] << 32) | (uint32_t)(tb + wb + r * kWave + lane);
+    block_sync();  // the tile is staged in digit order
+
+    const bool full = cv == T1;
+#pragma unroll
+    for (int r = 0; r < R1; ++r) {
+      const int j = wb + r * kWave + lane;
+      if (full || j < cv) {
+        const uint64_t e = sh.stage[j];
+        const uint32_t pos = sh.base[(uint32_t)(e >> 32) & M0] + (uint32_t)j;
+        if (pos < (uint64_t)a.n) out[pos] = e;  // always true for consistent counts
+      }
+      // keep the scheduler from hoisting every round's loads at once, which
+      // would hold ~5 registers per round live
+      if (r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
 // 4 waves per SIMD: two 8-wave workgroups per CU, so one can compute while
 // the other waits on memory.
 constexpr int kScatterWavesPerSimd = 4;
 
-template <typename unused = void>
-__global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_first(GArgs a) {
-  __shared__ ScatterShared sh;
-  if (!a.plan->ok) return;
-  scatter_block<true>(a, 0, blockIdx.x, a.main, sh);
+// The first pass's 148 KB of LDS allow one workgroup per CU: 2 waves per SIMD.
+template <int D0>
+__global__ __launch_bounds__(NT, 2) void g_first(GArgs a) {
+  __shared__ union {
+    ScatterShared generic;
+    FirstFastShared<D0> fast;
+  } sh;
+  const Plan* pl = a.plan;
+  if (!pl->ok) return;
+  if (pl->packed && pl->W == 32)
+    first_fast<D0>(a, blockIdx.x, sh.fast);
+  else
+    scatter_block<true>(a, 0, blockIdx.x, a.main, sh.generic);
 }
 
 // Per-block digit counts (and length sums) of pass s over its input elements.
@@ -551,7 +753,7 @@ __global__ __launch_bounds__(HT) void g_histF(GArgs a) {
   __shared__ CountShared sh;
   const Plan* pl = a.plan;
   if (!pl->ok) return;
-  count_block(a, (int)pl->nscatter - 1, blockIdx.x, a.main, true, sh, HT);
+  count_block(a, (int)pl->nscatter - 1, blockIdx.x, a.fin, true, sh, HT);
 }
 
 // ---- middle passes: one launch of co-resident workgroups, grid barriers ----
@@ -620,16 +822,12 @@ struct FinalShared {
   uint32_t scan32[NW + 1];
 };
 
-template <typename unused = void>
-__global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
-  __shared__ FinalShared sh;
-  uint16_t* cnt = reinterpret_cast<uint16_t*>(sh.stage);
+__device__ void final_generic(const GArgs& a, int g, FinalShared& sh) {
+  u16_alias* cnt = reinterpret_cast<u16_alias*>(sh.stage);
   const Plan* pl = a.plan;
-  if (!pl->ok) return;
   const int t = threadIdx.x;
   const int lane = lane_id();
   const int w = t / kWave;
-  const int g = blockIdx.x;
   const int s = (int)pl->nscatter - 1;
   const int nb = (int)pl->nbins[s];
   const int nbits = (int)pl->nbits[s];
@@ -667,8 +865,8 @@ __global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
     }
   }
 
-  const int tile0 = g * a.main.tpb;
-  const int tile1 = min(a.tiles, tile0 + a.main.tpb);
+  const int tile0 = g * a.fin.tpb;
+  const int tile1 = min(a.tiles, tile0 + a.fin.tpb);
   for (int tile = tile0; tile < tile1; ++tile) {
     block_sync();
     const int64_t tb = (int64_t)tile * T;
@@ -704,7 +902,7 @@ __global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
       rank_tile(dg, rk, nb, nbits, cnt, sh.excl, sh.scan32);
       block_sync();  // counters read before the stage is reused
       if (!packed) {
-        uint32_t* sid = reinterpret_cast<uint32_t*>(sh.stage);
+        u32_alias* sid = reinterpret_cast<u32_alias*>(sh.stage);
 #pragma unroll
         for (int r = 0; r < K; ++r) sid[rk[r]] = id[r];
         block_sync();
@@ -810,6 +1008,314 @@ __global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
   }
 }
 
+// ---- fast final pass ----------------------------------------------------------
+// Keys of at most 32 bits, two scatter passes (the final digit is the whole
+// mixed-radix value u2 = (p - pmin) * H + h, so a digit holds one class),
+// lengths below 2^26. Per tile:
+//   phase 1   digit and length of every item; per-digit length sums of the
+//             tile (LDS atomics); stable ranks against the wave counters.
+//   offsets   owners of the bins scan counts and length sums across waves
+//             and the block: tile offsets for the ranks, and for every digit
+//             the output position of its first item in this tile and the
+//             wait base = running length offset - tile length prefix at the
+//             digit's start.
+//   stage     the tile in digit order (its sorted order).
+//   phase 2   exclusive length prefix P of the sorted tile (DPP scans within
+//             rounds, round and wave totals across); every item writes
+//             order and wait = wait base of its digit + P, and adds P to its
+//             digit's sum for the class totals.
+// A digit's waits in a tile add up to (items) * (wait base) + (sum of P);
+// the owners fold that into per-digit 128-bit totals, which become class
+// totals at the end. Five barriers per tile.
+
+struct FinalFastShared {
+  uint64_t stage[T];
+  uint16_t cnt[NW][kMaxBins];  // wave counters, then the waves' tile offsets
+  uint32_t base_c[kMaxBins];   // output position of the tile's first item of a digit
+  uint64_t base_w[kMaxBins];   // wait base of a digit in this tile
+  uint64_t wsum[kMaxBins];     // length sums of the tile's digits
+  uint64_t binp[kMaxBins];     // sums of the tile prefix P over a digit's items
+  uint32_t part_c[NW + 1];
+  uint64_t part_w[NW + 1];
+  uint64_t chunk[NW];          // length sum of every wave's share of the sorted tile
+};
+
+// 128-bit product of a count and a 64-bit value.
+__device__ __forceinline__ U128 mul_u32_u64(uint32_t c, uint64_t x) {
+  const uint64_t p0 = (uint64_t)c * (uint32_t)x;
+  const uint64_t p1 = (uint64_t)c * (uint32_t)(x >> 32);
+  U128 r;
+  r.lo = p0 + (p1 << 32);
+  r.hi = (p1 >> 32) + (r.lo < p0 ? 1u : 0u);
+  return r;
+}
+
+// Elements of one tile, round-major per wave; items past the end read as zero.
+__device__ __forceinline__ void load_final(const uint64_t* keys, int64_t n, int tile,
+                                           uint64_t (&e)[K]) {
+  const int64_t tb = (int64_t)tile * T;
+  const int wb = wave_id() * kWave * K;
+  const int lim =
+      __builtin_amdgcn_readfirstlane((int)max((int64_t)0, min(n - tb - wb, (int64_t)kWave * K)));
+  const __amdgpu_buffer_rsrc_t rk = raw_rsrc(keys + tb + wb, (uint32_t)lim * 8u);
+  const int lane = lane_id();
+#pragma unroll
+  for (int r = 0; r < K; ++r) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rk, (lane + r * kWave) * 8, 0, 0);
+    e[r] = ((uint64_t)v[1] << 32) | v[0];
+  }
+}
+
+template <int NB>  // bits ranked: the final digit has fewer than 2^NB values
+__device__ void final_fast(const GArgs& a, int g, FinalFastShared& sh) {
+  constexpr int OWN = kMaxBins / NT;  // bins t*OWN .. t*OWN+OWN-1 belong to thread t
+  static_assert(OWN == 2, "two bins per thread");
+  const int t = threadIdx.x;
+  const int lane = lane_id();
+  const int w = t / kWave;
+  const int wb = w * kWave * K;
+  const Plan* pl = a.plan;
+  const int nb = (int)pl->nbins[1];
+  const uint32_t d0 = (uint32_t)a.d0;
+  const uint32_t psh = pl->wh + d0;
+  const uint32_t H = pl->H;
+  const uint32_t mh = (1u << pl->wh) - 1;
+  const uint32_t lenmask = (1u << psh) - 1;
+  const uint32_t hoff = pl->hmin << d0;
+  const uint64_t* keys_in = a.keys[0];
+  uint16_t* mycnt = sh.cnt[w];
+  auto digit = [&](uint32_t key) { return __umul24(key >> psh, H) + ((key >> d0) & mh); };
+  auto len = [&](uint32_t key) { return (key & lenmask) + hoff; };
+
+  clear_wave_counters<kMaxBins>(mycnt);
+#pragma unroll
+  for (int i = 0; i < OWN; ++i) {
+    sh.wsum[t * OWN + i] = 0;
+    sh.binp[t * OWN + i] = 0;
+  }
+  // running position and wait offsets of the owned digits
+  uint32_t carry_c[OWN];
+  start_offsets(a, 1, nb, g, carry_c, sh.part_c);
+  uint64_t carry_w[OWN];
+  {
+    uint64_t wv[OWN];
+    uint64_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      const int b = t * OWN + i;
+      wv[i] = b < nb ? a.hist_w[b] : 0ull;
+      sum += wv[i];
+    }
+    uint64_t tot;
+    uint64_t ex = block_excl_scan_u64<NT>(sum, sh.part_w, tot);
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      const int b = t * OWN + i;
+      carry_w[i] = ex + (b < nb ? a.block_histw[(size_t)g * kMaxBins + b] : 0ull);
+      ex += wv[i];
+    }
+  }
+  // the previous tile's item count and wait base of each owned digit, and
+  // the digit's wait total so far
+  uint32_t pc[OWN];
+  uint64_t pbw[OWN];
+  U128 acc[OWN];
+#pragma unroll
+  for (int i = 0; i < OWN; ++i) {
+    pc[i] = 0;
+    pbw[i] = 0;
+    acc[i] = {0, 0};
+  }
+
+  const int tile0 = g * a.fin.tpb;
+  const int tile1 = min(a.tiles, tile0 + a.fin.tpb);
+  uint64_t e[K];
+  load_final(keys_in, a.n, tile0, e);
+  for (int tile = tile0; tile < tile1; ++tile) {
+    const int64_t tb = (int64_t)tile * T;
+    const int cv = (int)min((int64_t)T, a.n - tb);
+    const bool full = cv == T;
+
+    // ---- phase 1: digits, tile length sums per digit, ranks -------------
+    uint32_t dg[K], rk[K];
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+      const uint32_t key = (uint32_t)(e[r] >> 32);
+      dg[r] = digit(key);
+      uint32_t ls = len(key);
+      if (!full && wb + r * kWave + lane >= cv) {  // past the end: last digit, no length
+        dg[r] = (uint32_t)nb - 1;
+        ls = 0;
+      }
+      atomicAdd((unsigned long long*)&sh.wsum[dg[r]], (unsigned long long)ls);
+    }
+#pragma unroll
+    for (int r = 0; r < K; ++r) rk[r] = rank_round_c<NB>(dg[r], mycnt);
+    block_sync();  // counters and length sums are complete; phase 2 of the last tile is over
+
+    // ---- offsets (owners) ---------------------------------------------------
+    // The two owned digits are adjacent, so one u32 holds both u16 counters
+    // of a wave; counts and offsets stay below 2^16, so packed sums of the
+    // pairs never carry from the low half into the high half.
+    uint32_t cw[NW];  // wave v's counts of the two owned digits
+    uint32_t totp = 0;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) {
+      cw[v] = *reinterpret_cast<const u32_alias*>(&sh.cnt[v][t * OWN]);
+      totp += cw[v];
+    }
+    const uint32_t tot[OWN] = {totp & 0xffffu, totp >> 16};
+    uint64_t ws[OWN];
+    uint32_t local_c = 0;
+    uint64_t local_w = 0;
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      const int b = t * OWN + i;
+      ws[i] = sh.wsum[b];
+      sh.wsum[b] = 0;
+      // the previous tile's waits of this digit: items * wait base + sum of P
+      const uint64_t bp = sh.binp[b];
+      sh.binp[b] = 0;
+      add128(acc[i], mul_u32_u64(pc[i], pbw[i]));
+      add128(acc[i], bp);
+      local_c += tot[i];
+      local_w += ws[i];
+    }
+    const uint32_t inc_c = wave_incl_scan_u32(local_c);
+    const uint64_t inc_w = wave_incl_scan_u40(local_w);
+    if (lane == kWave - 1) {
+      sh.part_c[w] = inc_c;
+      sh.part_w[w] = inc_w;
+    }
+    block_sync();
+    uint32_t ex_c = inc_c - local_c;
+    uint64_t ex_w = inc_w - local_w;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) {
+      ex_c += v < w ? sh.part_c[v] : 0u;
+      ex_w += v < w ? sh.part_w[v] : 0ull;
+    }
+    {
+      uint32_t run = ex_c | ((ex_c + tot[0]) << 16);
+#pragma unroll
+      for (int v = 0; v < NW; ++v) {
+        *reinterpret_cast<u32_alias*>(&sh.cnt[v][t * OWN]) = run;
+        run += cw[v];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      const int b = t * OWN + i;
+      const uint64_t bw = carry_w[i] - ex_w;
+      sh.base_c[b] = carry_c[i] - ex_c;
+      sh.base_w[b] = bw;
+      pc[i] = tot[i] - ((!full && b == nb - 1) ? (uint32_t)(T - cv) : 0u);
+      pbw[i] = bw;
+      carry_c[i] += tot[i];
+      carry_w[i] += ws[i];
+      ex_c += tot[i];
+      ex_w += ws[i];
+    }
+    block_sync();  // tile offsets and bases are written
+
+    // ---- stage in digit order; load the next tile -------------------------
+#pragma unroll
+    for (int r = 0; r < K; ++r) rk[r] += mycnt[opaque(dg[r])];
+    clear_wave_counters<kMaxBins>(mycnt);
+#pragma unroll
+    for (int r = 0; r < K; ++r) sh.stage[rk[r]] = e[r];
+    if (tile + 1 < tile1) load_final(keys_in, a.n, tile + 1, e);
+    block_sync();  // the tile is staged
+
+    // ---- phase 2: tile length prefix, order, waits ---------------------------
+    uint32_t lsr[K], inc[K], rt[K];
+    uint64_t chunk = 0;
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+      const int j = wb + r * kWave + lane;
+      uint32_t ls = 0;
+      if (full || j < cv) ls = len((uint32_t)(sh.stage[j] >> 32));
+      lsr[r] = ls;
+      inc[r] = wave_incl_scan_u32(ls);  // below 2^32: 64 lengths < 2^26
+      rt[r] = (uint32_t)__builtin_amdgcn_readlane((int)inc[r], kWave - 1);
+      chunk += rt[r];
+    }
+    if (lane == 0) sh.chunk[w] = chunk;
+    block_sync();
+    uint64_t run = 0;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) run += v < w ? sh.chunk[v] : 0ull;
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+      const int j = wb + r * kWave + lane;
+      if (full || j < cv) {
+        const uint64_t x = sh.stage[j];
+        const uint32_t d = digit((uint32_t)(x >> 32));
+        const uint64_t P = run + (inc[r] - lsr[r]);
+        const uint32_t pos = sh.base_c[d] + (uint32_t)j;
+        if (pos < (uint64_t)a.n) {  // always true for consistent counts
+          a.order[pos] = (int32_t)(uint32_t)x;
+          a.wait[pos] = (int64_t)(sh.base_w[d] + P);
+        }
+        atomicAdd((unsigned long long*)&sh.binp[d], (unsigned long long)P);
+      }
+      run += rt[r];
+    }
+  }
+
+  block_sync();  // the last tile's sums of P are complete
+#pragma unroll
+  for (int i = 0; i < OWN; ++i) {
+    add128(acc[i], mul_u32_u64(pc[i], pbw[i]));
+    add128(acc[i], sh.binp[t * OWN + i]);
+  }
+  // digit totals -> class totals (a digit holds one class: u2 / H)
+  uint64_t* clo = sh.stage;
+  uint64_t* chi = sh.stage + 256;
+  for (int c = t; c < 256; c += NT) clo[c] = chi[c] = 0;
+  block_sync();
+#pragma unroll
+  for (int i = 0; i < OWN; ++i) {
+    const int b = t * OWN + i;
+    if (b < nb && (acc[i].lo | acc[i].hi)) {
+      const uint32_t c = (uint32_t)b / H;
+      atomic_add128(clo + c, chi + c, acc[i]);
+    }
+  }
+  block_sync();
+  const int P = (int)pl->P;
+  for (int c = t; c < P; c += NT) {
+    U128 v = {clo[c], chi[c]};
+    const int cls = c + (int)pl->pmin;
+    if (v.lo | v.hi) atomic_add128(a.totals + 2 * (1 + cls), a.totals + 2 * (1 + cls) + 1, v);
+  }
+  if (t == 0) {
+    U128 gsum = {0, 0};
+    for (int c = 0; c < P; ++c) {
+      U128 v = {clo[c], chi[c]};
+      add128(gsum, v);
+    }
+    if (gsum.lo | gsum.hi) atomic_add128(a.totals, a.totals + 1, gsum);
+  }
+}
+
+template <typename unused = void>
+__global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
+  __shared__ union {
+    FinalShared generic;
+    FinalFastShared fast;
+  } sh;
+  const Plan* pl = a.plan;
+  if (!pl->ok) return;
+  if (pl->packed && pl->W == 32 && pl->nscatter == 2 && pl->small) {
+    if (pl->nbits[1] <= 8)
+      final_fast<8>(a, blockIdx.x, sh.fast);
+    else
+      final_fast<10>(a, blockIdx.x, sh.fast);
+  } else
+    final_generic(a, blockIdx.x, sh.generic);
+}
+
 __global__ void g_fill_zero(uint32_t* p, size_t count) {
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) p[i] = 0;
@@ -827,14 +1333,17 @@ int resident_blocks(const void* kernel, int threads) {
   return cus * occ;
 }
 
-Split make_split(int64_t n, int resident) {
+// Blocks of whole tiles, tpb a multiple of `mult` tiles, at most `resident`
+// blocks (the workgroups that fit on the device at once).
+Split make_split(int64_t n, int resident, int mult) {
   const int64_t tiles = (n + T - 1) / T;
+  const int64_t chunks = (tiles + mult - 1) / mult;
   int64_t g = resident;
   if (g > kMaxBlocks) g = kMaxBlocks;
-  if (g > tiles) g = tiles;
+  if (g > chunks) g = chunks;
   if (g < 1) g = 1;
   Split s;
-  s.tpb = (int32_t)((tiles + g - 1) / g);
+  s.tpb = (int32_t)((chunks + g - 1) / g * mult);
   s.blocks = (int32_t)((tiles + s.tpb - 1) / s.tpb);
   return s;
 }
@@ -847,14 +1356,19 @@ void mark(const StageEvents* ev, int stage, bool after, hipStream_t st) {
 
 }  // namespace
 
-Split global_split(int64_t n) {
+Split global_first_split(int64_t n) {
+  static const int r = resident_blocks(reinterpret_cast<const void*>(g_first<10>), NT);
+  return make_split(n, r, kFirstTiles);
+}
+
+Split global_final_split(int64_t n) {
   static const int r = resident_blocks(reinterpret_cast<const void*>(g_final<>), NT);
-  return make_split(n, r);
+  return make_split(n, r, 1);
 }
 
 Split global_mid_split(int64_t n) {
   static const int r = resident_blocks(reinterpret_cast<const void*>(g_mid), NT);
-  return make_split(n, r);
+  return make_split(n, r, 1);
 }
 
 hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEvents* ev) {
@@ -866,13 +1380,19 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   mark(ev, 0, true, st);
   hipLaunchKernelGGL(g_scan, dim3((1u << a.d0) + 1), dim3(SCT), 0, st, a, 0);
   mark(ev, 1, false, st);
-  hipLaunchKernelGGL(g_first<>, gm, dim3(NT), 0, st, a);
+  if (a.d0 == 9)
+    hipLaunchKernelGGL(g_first<9>, gm, dim3(NT), 0, st, a);
+  else if (a.d0 == 10)
+    hipLaunchKernelGGL(g_first<10>, gm, dim3(NT), 0, st, a);
+  else
+    hipLaunchKernelGGL(g_first<8>, gm, dim3(NT), 0, st, a);
   mark(ev, 1, true, st);
   hipLaunchKernelGGL(g_mid, dim3(a.mid.blocks), dim3(NT), 0, st, a);
-  hipLaunchKernelGGL(g_histF, gm, dim3(HT), 0, st, a);
+  const dim3 gf(a.fin.blocks);
+  hipLaunchKernelGGL(g_histF, gf, dim3(HT), 0, st, a);
   hipLaunchKernelGGL(g_scan, dim3(kMaxBins), dim3(SCT), 0, st, a, 1);
   mark(ev, 2, false, st);
-  hipLaunchKernelGGL(g_final<>, gm, dim3(NT), 0, st, a);
+  hipLaunchKernelGGL(g_final<>, gf, dim3(NT), 0, st, a);
   mark(ev, 2, true, st);
   return hipGetLastError();
 }

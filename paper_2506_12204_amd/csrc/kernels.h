@@ -43,6 +43,7 @@ constexpr int kMaxScatter = 5;   // scatter passes: first, up to 3 middle, final
 constexpr int kGlobalThreads = 512;
 constexpr int kGlobalRounds = 8;
 constexpr int kGlobalTile = kGlobalThreads * kGlobalRounds;
+constexpr int kFirstTiles = 4;   // the first pass works on 4 tiles at a time
 constexpr int kMaxBlocks = 4096; // upper bound on workgroups of a pass
 
 // Decided on the device by the histogram pass once the ranges are known.
@@ -53,8 +54,11 @@ struct Plan {
   uint32_t H;         // (largest length >> d0) - hmin + 1
   uint32_t P;         // largest priority - pmin + 1
   uint32_t wh, wp;    // bit widths of the h and p fields of a key
-  uint32_t W;         // bit width of a request id
+  uint32_t W;         // bits below the key in a packed element: 32 when the
+                      // key fits 32 bits (key in the high word), else the
+                      // bit width of a request id
   uint32_t packed;    // 1: element = key << W | id in one u64
+  uint32_t small;     // 1: every length < 2^26 (64-lane length sums fit 32 bits)
   uint32_t nscatter;  // number of scatter passes (>= 2)
   uint32_t shift[kMaxScatter];  // digit = (u2 >> shift) & (bins - 1), passes >= 1
   uint32_t nbits[kMaxScatter];
@@ -78,7 +82,8 @@ struct GArgs {
   int32_t d0;           // width of the first (low-length) digit
   int32_t tiles;
   int32_t force_wide;   // 1: never pack the id into the key word
-  Split main;           // histogram, first and final passes
+  Split main;           // first histogram and first pass (tpb a multiple of kFirstTiles)
+  Split fin;            // final histogram and final pass
   Split mid;            // the cooperative middle-pass kernel
   uint32_t* flags;
   uint32_t* barrier;    // arrivals at the middle-pass grid barriers
@@ -99,7 +104,8 @@ struct StageEvents {
 };
 
 // Work splits of the passes for n requests (device-dependent occupancy).
-Split global_split(int64_t n);
+Split global_first_split(int64_t n);
+Split global_final_split(int64_t n);
 Split global_mid_split(int64_t n);
 hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEvents* ev);
 

@@ -50,7 +50,7 @@ __global__ __launch_bounds__(NT) void segment_schedule_kernel(SegArgs a) {
   constexpr int NW = SH::NW;
   constexpr int STRIDE = SH::STRIDE;
   __shared__ SH sh;
-  uint16_t* cnt = reinterpret_cast<uint16_t*>(sh.stage);
+  u16_alias* cnt = reinterpret_cast<u16_alias*>(sh.stage);
 
   const int lane = lane_id();
   const int w = threadIdx.x / kWave;
