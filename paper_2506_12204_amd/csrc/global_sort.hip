@@ -1022,11 +1022,11 @@ __device__ void final_generic(const GArgs& a, int g, FinalShared& sh) {
 //   stage     the tile in digit order (its sorted order).
 //   phase 2   exclusive length prefix P of the sorted tile (DPP scans within
 //             rounds, round and wave totals across); every item writes
-//             order and wait = wait base of its digit + P, and adds P to its
-//             digit's sum for the class totals.
-// A digit's waits in a tile add up to (items) * (wait base) + (sum of P);
-// the owners fold that into per-digit 128-bit totals, which become class
-// totals at the end. Five barriers per tile.
+//             order and wait = wait base of its digit + P.
+// Class totals: a digit holds one class and the sorted tile is class-major,
+// so the classes a lane meets over its rounds never decrease. Each lane sums
+// its waits in a 128-bit register total and adds it to the class's LDS total
+// only when its class changes (and once at the end). Five barriers per tile.
 
 struct FinalFastShared {
   uint64_t stage[T];
@@ -1034,21 +1034,11 @@ struct FinalFastShared {
   uint32_t base_c[kMaxBins];   // output position of the tile's first item of a digit
   uint64_t base_w[kMaxBins];   // wait base of a digit in this tile
   uint64_t wsum[kMaxBins];     // length sums of the tile's digits
-  uint64_t binp[kMaxBins];     // sums of the tile prefix P over a digit's items
+  uint64_t clo[256], chi[256]; // class totals, low and high words
   uint32_t part_c[NW + 1];
   uint64_t part_w[NW + 1];
   uint64_t chunk[NW];          // length sum of every wave's share of the sorted tile
 };
-
-// 128-bit product of a count and a 64-bit value.
-__device__ __forceinline__ U128 mul_u32_u64(uint32_t c, uint64_t x) {
-  const uint64_t p0 = (uint64_t)c * (uint32_t)x;
-  const uint64_t p1 = (uint64_t)c * (uint32_t)(x >> 32);
-  U128 r;
-  r.lo = p0 + (p1 << 32);
-  r.hi = (p1 >> 32) + (r.lo < p0 ? 1u : 0u);
-  return r;
-}
 
 // Elements of one tile, round-major per wave; items past the end read as zero.
 __device__ __forceinline__ void load_final(const uint64_t* keys, int64_t n, int tile,
@@ -1089,10 +1079,8 @@ __device__ void final_fast(const GArgs& a, int g, FinalFastShared& sh) {
 
   clear_wave_counters<kMaxBins>(mycnt);
 #pragma unroll
-  for (int i = 0; i < OWN; ++i) {
-    sh.wsum[t * OWN + i] = 0;
-    sh.binp[t * OWN + i] = 0;
-  }
+  for (int i = 0; i < OWN; ++i) sh.wsum[t * OWN + i] = 0;
+  for (int c = t; c < 256; c += NT) sh.clo[c] = sh.chi[c] = 0;
   // running position and wait offsets of the owned digits
   uint32_t carry_c[OWN];
   start_offsets(a, 1, nb, g, carry_c, sh.part_c);
@@ -1115,17 +1103,9 @@ __device__ void final_fast(const GArgs& a, int g, FinalFastShared& sh) {
       ex += wv[i];
     }
   }
-  // the previous tile's item count and wait base of each owned digit, and
-  // the digit's wait total so far
-  uint32_t pc[OWN];
-  uint64_t pbw[OWN];
-  U128 acc[OWN];
-#pragma unroll
-  for (int i = 0; i < OWN; ++i) {
-    pc[i] = 0;
-    pbw[i] = 0;
-    acc[i] = {0, 0};
-  }
+  // this lane's running wait total and the (relative) class it belongs to
+  uint32_t cur = ~0u;
+  U128 acc = {0, 0};
 
   const int tile0 = g * a.fin.tpb;
   const int tile1 = min(a.tiles, tile0 + a.fin.tpb);
@@ -1173,11 +1153,6 @@ __device__ void final_fast(const GArgs& a, int g, FinalFastShared& sh) {
       const int b = t * OWN + i;
       ws[i] = sh.wsum[b];
       sh.wsum[b] = 0;
-      // the previous tile's waits of this digit: items * wait base + sum of P
-      const uint64_t bp = sh.binp[b];
-      sh.binp[b] = 0;
-      add128(acc[i], mul_u32_u64(pc[i], pbw[i]));
-      add128(acc[i], bp);
       local_c += tot[i];
       local_w += ws[i];
     }
@@ -1209,8 +1184,6 @@ __device__ void final_fast(const GArgs& a, int g, FinalFastShared& sh) {
       const uint64_t bw = carry_w[i] - ex_w;
       sh.base_c[b] = carry_c[i] - ex_c;
       sh.base_w[b] = bw;
-      pc[i] = tot[i] - ((!full && b == nb - 1) ? (uint32_t)(T - cv) : 0u);
-      pbw[i] = bw;
       carry_c[i] += tot[i];
       carry_w[i] += ws[i];
       ex_c += tot[i];
@@ -1250,39 +1223,30 @@ __device__ void final_fast(const GArgs& a, int g, FinalFastShared& sh) {
       const int j = wb + r * kWave + lane;
       if (full || j < cv) {
         const uint64_t x = sh.stage[j];
-        const uint32_t d = digit((uint32_t)(x >> 32));
-        const uint64_t P = run + (inc[r] - lsr[r]);
+        const uint32_t key = (uint32_t)(x >> 32);
+        const uint32_t c = key >> psh;  // class - pmin
+        const uint32_t d = __umul24(c, H) + ((key >> d0) & mh);
+        const uint64_t wt = sh.base_w[d] + run + (inc[r] - lsr[r]);
         const uint32_t pos = sh.base_c[d] + (uint32_t)j;
         if (pos < (uint64_t)a.n) {  // always true for consistent counts
           a.order[pos] = (int32_t)(uint32_t)x;
-          a.wait[pos] = (int64_t)(sh.base_w[d] + P);
+          a.wait[pos] = (int64_t)wt;
         }
-        atomicAdd((unsigned long long*)&sh.binp[d], (unsigned long long)P);
+        if (c != cur) {
+          if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
+          cur = c;
+          acc = {0, 0};
+        }
+        add128(acc, wt);
       }
       run += rt[r];
     }
   }
+  if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
 
-  block_sync();  // the last tile's sums of P are complete
-#pragma unroll
-  for (int i = 0; i < OWN; ++i) {
-    add128(acc[i], mul_u32_u64(pc[i], pbw[i]));
-    add128(acc[i], sh.binp[t * OWN + i]);
-  }
-  // digit totals -> class totals (a digit holds one class: u2 / H)
-  uint64_t* clo = sh.stage;
-  uint64_t* chi = sh.stage + 256;
-  for (int c = t; c < 256; c += NT) clo[c] = chi[c] = 0;
-  block_sync();
-#pragma unroll
-  for (int i = 0; i < OWN; ++i) {
-    const int b = t * OWN + i;
-    if (b < nb && (acc[i].lo | acc[i].hi)) {
-      const uint32_t c = (uint32_t)b / H;
-      atomic_add128(clo + c, chi + c, acc[i]);
-    }
-  }
-  block_sync();
+  block_sync();  // every lane's total is in
+  uint64_t* clo = sh.clo;
+  uint64_t* chi = sh.chi;
   const int P = (int)pl->P;
   for (int c = t; c < P; c += NT) {
     U128 v = {clo[c], chi[c]};
@@ -1299,6 +1263,233 @@ __device__ void final_fast(const GArgs& a, int g, FinalFastShared& sh) {
   }
 }
 
+// ---- big-tile final pass -----------------------------------------------------
+// The fast final pass again, for final digits of at most 256 values (the
+// n = 2^26 workload has 160): tiles of 16384 items handled by 1024 threads
+// (16 waves x 16 rounds), one workgroup per CU. Four times the items per tile
+// means four times longer runs per digit in the scattered writes of order and
+// wait, which is what their cost depends on. The thread t < digits owns
+// digit t.
+
+constexpr int NTB = 1024;
+constexpr int NWB = NTB / kWave;
+constexpr int KB = 16;
+constexpr int TB = NTB * KB;
+constexpr int MAXB = 256;
+static_assert(TB == T * kFirstTiles, "blocks of the final split are whole big tiles");
+
+struct FinalBigShared {
+  uint64_t stage[TB];
+  uint16_t cnt[NWB][MAXB];     // wave counters, then the waves' tile offsets
+  uint32_t base_c[MAXB];       // output position of the tile's first item of a digit
+  uint64_t base_w[MAXB];       // wait base of a digit in this tile
+  uint64_t wsum[MAXB];         // length sums of the tile's digits
+  uint64_t clo[256], chi[256]; // class totals, low and high words
+  uint32_t part_c[NWB + 1];
+  uint64_t part_w[NWB + 1];
+  uint64_t chunk[NWB];
+};
+
+__device__ __forceinline__ bool use_big_final(const Plan* pl) {
+  return pl->packed && pl->W == 32 && pl->nscatter == 2 && pl->small && pl->nbins[1] <= MAXB;
+}
+
+// Elements of one big tile of `cnt` items at item tb, round-major per wave.
+__device__ __forceinline__ void load_final_big(const uint64_t* keys, int64_t tb, int cnt,
+                                               uint64_t (&e)[KB]) {
+  const int wb = wave_id() * kWave * KB;
+  const int lim = __builtin_amdgcn_readfirstlane(max(0, min(cnt - wb, kWave * KB)));
+  const __amdgpu_buffer_rsrc_t rk = raw_rsrc(keys + tb + wb, (uint32_t)lim * 8u);
+  const int lane = lane_id();
+#pragma unroll
+  for (int r = 0; r < KB; ++r) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rk, (lane + r * kWave) * 8, 0, 0);
+    e[r] = ((uint64_t)v[1] << 32) | v[0];
+  }
+}
+
+__device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
+  const int t = threadIdx.x;
+  const int lane = lane_id();
+  const int w = wave_id();
+  const int wb = w * kWave * KB;
+  const Plan* pl = a.plan;
+  const int nb = (int)pl->nbins[1];
+  const bool owner = t < nb;
+  const uint32_t d0 = (uint32_t)a.d0;
+  const uint32_t psh = pl->wh + d0;
+  const uint32_t H = pl->H;
+  const uint32_t mh = (1u << pl->wh) - 1;
+  const uint32_t lenmask = (1u << psh) - 1;
+  const uint32_t hoff = pl->hmin << d0;
+  const uint64_t* keys_in = a.keys[0];
+  uint16_t* mycnt = sh.cnt[w];
+  auto digit = [&](uint32_t key) { return __umul24(key >> psh, H) + ((key >> d0) & mh); };
+  auto len = [&](uint32_t key) { return (key & lenmask) + hoff; };
+
+  clear_wave_counters<MAXB>(mycnt);
+  if (t < MAXB) sh.wsum[t] = 0;
+  if (t < 256) sh.clo[t] = sh.chi[t] = 0;
+  // running position and wait offsets of the owned digit: its global base
+  // (exclusive scan of the digit totals) plus the blocks before this one
+  uint32_t carry_c;
+  uint64_t carry_w;
+  {
+    const uint32_t c = owner ? a.hist_cnt[kMaxBins + t] : 0u;
+    const uint64_t wv = owner ? a.hist_w[t] : 0ull;
+    uint32_t tc;
+    uint64_t tw;
+    carry_c = block_excl_scan_u32<NTB>(c, sh.part_c, tc);
+    carry_w = block_excl_scan_u64<NTB>(wv, sh.part_w, tw);
+    if (owner) {
+      carry_c += a.block_hist[(size_t)g * kMaxBins + t];
+      carry_w += a.block_histw[(size_t)g * kMaxBins + t];
+    }
+  }
+  uint32_t cur = ~0u;  // this lane's running wait total and its class - pmin
+  U128 acc = {0, 0};
+
+  const int64_t lo = (int64_t)g * a.fin.tpb * T;
+  const int64_t hi = min(a.n, lo + (int64_t)a.fin.tpb * T);
+  uint64_t e[KB];
+  load_final_big(keys_in, lo, (int)min((int64_t)TB, hi - lo), e);
+  for (int64_t tb = lo; tb < hi; tb += TB) {
+    const int cv = (int)min((int64_t)TB, hi - tb);
+    const bool full = cv == TB;
+
+    // ---- phase 1: digits, tile length sums per digit, ranks -------------
+    // (digits are recomputed where needed: 16 more registers would spill)
+    auto digit_of = [&](int r) {
+      const uint32_t dd = digit((uint32_t)(opaque((uint32_t)(e[r] >> 32))));
+      return (!full && wb + r * kWave + lane >= cv) ? (uint32_t)nb - 1 : dd;  // past the end: last digit
+    };
+    uint32_t rk[KB];
+#pragma unroll
+    for (int r = 0; r < KB; ++r) {
+      const uint32_t key = (uint32_t)(e[r] >> 32);
+      const bool past = !full && wb + r * kWave + lane >= cv;
+      const uint32_t d = past ? (uint32_t)nb - 1 : digit(key);
+      const uint32_t ls = past ? 0u : len(key);
+      atomicAdd((unsigned long long*)&sh.wsum[d], (unsigned long long)ls);
+      rk[r] = rank_round_c<8>(d, mycnt);
+    }
+    block_sync();  // counters and length sums are complete; phase 2 of the last tile is over
+
+    // ---- offsets (owners) ---------------------------------------------------
+    uint32_t tot = 0;
+    uint64_t ws = 0;
+    if (owner) {
+#pragma unroll
+      for (int v = 0; v < NWB; ++v) tot += sh.cnt[v][t];
+      ws = sh.wsum[t];
+      sh.wsum[t] = 0;
+    }
+    const uint32_t inc_c = wave_incl_scan_u32(tot);
+    const uint64_t inc_w = wave_incl_scan_u40(ws);  // a tile's lengths add up to < 2^40
+    if (lane == kWave - 1) {
+      sh.part_c[w] = inc_c;
+      sh.part_w[w] = inc_w;
+    }
+    block_sync();
+    uint32_t ex_c = inc_c - tot;
+    uint64_t ex_w = inc_w - ws;
+#pragma unroll
+    for (int v = 0; v < NWB; ++v) {
+      ex_c += v < w ? sh.part_c[v] : 0u;
+      ex_w += v < w ? sh.part_w[v] : 0ull;
+    }
+    if (owner) {
+      uint32_t run = ex_c;  // counts read again rather than held in 16 registers
+#pragma unroll
+      for (int v = 0; v < NWB; ++v) {
+        const uint32_t c = sh.cnt[v][t];
+        sh.cnt[v][t] = (uint16_t)run;
+        run += c;
+      }
+      sh.base_c[t] = carry_c - ex_c;
+      sh.base_w[t] = carry_w - ex_w;
+      carry_c += tot;
+      carry_w += ws;
+    }
+    block_sync();  // tile offsets and bases are written
+
+    // ---- stage in digit order; load the next tile -------------------------
+#pragma unroll
+    for (int r = 0; r < KB; ++r) rk[r] += mycnt[digit_of(r)];
+    clear_wave_counters<MAXB>(mycnt);
+#pragma unroll
+    for (int r = 0; r < KB; ++r) sh.stage[rk[r]] = e[r];
+    if (tb + TB < hi) load_final_big(keys_in, tb + TB, (int)min((int64_t)TB, hi - tb - TB), e);
+    block_sync();  // the tile is staged
+
+    // ---- phase 2: tile length prefix, order, waits, class totals -----------
+    uint32_t lsr[KB], inc[KB], rt[KB];
+    uint64_t chunk = 0;
+#pragma unroll
+    for (int r = 0; r < KB; ++r) {
+      const int j = wb + r * kWave + lane;
+      uint32_t ls = 0;
+      if (full || j < cv) ls = len((uint32_t)(sh.stage[j] >> 32));
+      lsr[r] = ls;
+      inc[r] = wave_incl_scan_u32(ls);  // below 2^32: 64 lengths < 2^26
+      rt[r] = (uint32_t)__builtin_amdgcn_readlane((int)inc[r], kWave - 1);
+      chunk += rt[r];
+    }
+    if (lane == 0) sh.chunk[w] = chunk;
+    block_sync();
+    uint64_t run = 0;
+#pragma unroll
+    for (int v = 0; v < NWB; ++v) run += v < w ? sh.chunk[v] : 0ull;
+#pragma unroll
+    for (int r = 0; r < KB; ++r) {
+      const int j = wb + r * kWave + lane;
+      if (full || j < cv) {
+        const uint64_t x = sh.stage[j];
+        const uint32_t key = (uint32_t)(x >> 32);
+        const uint32_t c = key >> psh;  // class - pmin
+        const uint32_t d = __umul24(c, H) + ((key >> d0) & mh);
+        const uint64_t wt = sh.base_w[d] + run + (inc[r] - lsr[r]);
+        const uint32_t pos = sh.base_c[d] + (uint32_t)j;
+        if (pos < (uint64_t)a.n) {  // always true for consistent counts
+          a.order[pos] = (int32_t)(uint32_t)x;
+          a.wait[pos] = (int64_t)wt;
+        }
+        if (c != cur) {
+          if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
+          cur = c;
+          acc = {0, 0};
+        }
+        add128(acc, wt);
+      }
+      run += rt[r];
+    }
+  }
+  if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
+
+  block_sync();  // every lane's total is in
+  const int P = (int)pl->P;
+  for (int c = t; c < P; c += NTB) {
+    U128 v = {sh.clo[c], sh.chi[c]};
+    const int cls = c + (int)pl->pmin;
+    if (v.lo | v.hi) atomic_add128(a.totals + 2 * (1 + cls), a.totals + 2 * (1 + cls) + 1, v);
+  }
+  if (t == 0) {
+    U128 gsum = {0, 0};
+    for (int c = 0; c < P; ++c) {
+      U128 v = {sh.clo[c], sh.chi[c]};
+      add128(gsum, v);
+    }
+    if (gsum.lo | gsum.hi) atomic_add128(a.totals, a.totals + 1, gsum);
+  }
+}
+
+__global__ __launch_bounds__(NTB) void g_final_big(GArgs a) {
+  __shared__ FinalBigShared sh;
+  const Plan* pl = a.plan;
+  if (!pl->ok || !use_big_final(pl)) return;
+  final_big(a, blockIdx.x, sh);
+}
+
 template <typename unused = void>
 __global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
   __shared__ union {
@@ -1306,7 +1497,7 @@ __global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
     FinalFastShared fast;
   } sh;
   const Plan* pl = a.plan;
-  if (!pl->ok) return;
+  if (!pl->ok || use_big_final(pl)) return;
   if (pl->packed && pl->W == 32 && pl->nscatter == 2 && pl->small) {
     if (pl->nbits[1] <= 8)
       final_fast<8>(a, blockIdx.x, sh.fast);
@@ -1362,8 +1553,8 @@ Split global_first_split(int64_t n) {
 }
 
 Split global_final_split(int64_t n) {
-  static const int r = resident_blocks(reinterpret_cast<const void*>(g_final<>), NT);
-  return make_split(n, r, 1);
+  static const int r = resident_blocks(reinterpret_cast<const void*>(g_final_big), NTB);
+  return make_split(n, r, kFirstTiles);
 }
 
 Split global_mid_split(int64_t n) {
@@ -1392,6 +1583,8 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   hipLaunchKernelGGL(g_histF, gf, dim3(HT), 0, st, a);
   hipLaunchKernelGGL(g_scan, dim3(kMaxBins), dim3(SCT), 0, st, a, 1);
   mark(ev, 2, false, st);
+  // exactly one of the two does the work; the plan on the device decides
+  hipLaunchKernelGGL(g_final_big, gf, dim3(NTB), 0, st, a);
   hipLaunchKernelGGL(g_final<>, gf, dim3(NT), 0, st, a);
   mark(ev, 2, true, st);
   return hipGetLastError();
