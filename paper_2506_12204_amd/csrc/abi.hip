@@ -40,7 +40,9 @@ Layout layout_for(int64_t n) {
   Layout L;
   if (!needs_global(n)) return L;
   L.tiles = (n + kGlobalTile - 1) / kGlobalTile;
-  const size_t blocks = (size_t)std::min<int64_t>(L.tiles, kMaxBlocks);
+  // histogram rows: whole blocks of kHistRows rows, never more than kMaxBlocks
+  const size_t blocks = (size_t)std::min<int64_t>(
+      (L.tiles + kHistRows - 1) / kHistRows * kHistRows, kMaxBlocks);
   size_t off = kHeaderBytes;
   auto take = [&](size_t bytes) {
     const size_t at = off;

@@ -82,6 +82,17 @@ struct Ranges {
   }
 };
 
+// Items [lo, hi) counted by histogram row `row` of split `sp`: block
+// row / rows, its (row % rows)-th share of whole tiles (tpb is a multiple of
+// rows).
+__device__ __forceinline__ void row_range(const GArgs& a, const Split& sp, int row, int rows,
+                                          int64_t& lo, int64_t& hi) {
+  const int share = sp.tpb / rows;
+  lo = ((int64_t)(row / rows) * sp.tpb + (int64_t)(row % rows) * share) * T;
+  hi = min(a.n, lo + (int64_t)share * T);
+  lo = min(lo, a.n);
+}
+
 // Reduce the block ranges and turn them into the Plan (one workgroup).
 __device__ void write_plan(const GArgs& a, int G) {
   __shared__ uint32_t s_red[4][SCT_WAVES];
@@ -171,8 +182,8 @@ __global__ __launch_bounds__(HT) void g_hist0(GArgs a, int vec_ok) {
   for (int b = t; b < nb; b += HT) s_hist[b] = 0;
   block_sync();
 
-  const int64_t lo = (int64_t)g * a.main.tpb * T;
-  const int64_t hi = min(a.n, lo + (int64_t)a.main.tpb * T);
+  int64_t lo, hi;
+  row_range(a, a.main, g, kHistRows, lo, hi);
   Ranges rg;
   int64_t scalar_from = lo;
   if (vec_ok && hi > lo) {
@@ -288,17 +299,17 @@ __global__ __launch_bounds__(SCT) void g_scan(GArgs a, int final) {
   const int b = blockIdx.x;
   if (!final) {
     if (b == (1 << a.d0)) {
-      write_plan(a, a.main.blocks);
+      write_plan(a, a.main.blocks * kHistRows);
       return;
     }
-    column_scan<SCT>(a, 0, b, false, a.main.blocks, scan32, scan64);
+    column_scan<SCT>(a, 0, b, false, a.main.blocks * kHistRows, scan32, scan64);
     return;
   }
   const Plan* pl = a.plan;
   if (!pl->ok) return;
   const int s = (int)pl->nscatter - 1;
   if (b >= (int)pl->nbins[s]) return;
-  column_scan<SCT>(a, s, b, true, a.fin.blocks, scan32, scan64);
+  column_scan<SCT>(a, s, b, true, a.fin.blocks * kHistRows, scan32, scan64);
 }
 
 // ------------------------------------------------------------------------
@@ -353,7 +364,7 @@ __device__ __forceinline__ void rank_tile(const uint32_t (&dg)[K], uint32_t (&rk
 
 // Global digit bases of pass s (exclusive scan of its digit totals) plus this
 // block's offset, for this thread's BPT bins.
-__device__ __forceinline__ void start_offsets(const GArgs& a, int s, int nb, int g,
+__device__ __forceinline__ void start_offsets(const GArgs& a, int s, int nb, int row0,
                                               uint32_t (&carry)[BPT], uint32_t* scan32) {
   uint32_t c[BPT];
   uint32_t sum = 0;
@@ -368,7 +379,7 @@ __device__ __forceinline__ void start_offsets(const GArgs& a, int s, int nb, int
 #pragma unroll
   for (int i = 0; i < BPT; ++i) {
     const int b = threadIdx.x * BPT + i;
-    carry[i] = ex + (b < nb ? a.block_hist[(size_t)g * kMaxBins + b] : 0u);
+    carry[i] = ex + (b < nb ? a.block_hist[(size_t)row0 * kMaxBins + b] : 0u);
     ex += c[i];
   }
 }
@@ -440,7 +451,7 @@ __device__ void scatter_block(const GArgs& a, int s, int g, Split sp, ScatterSha
   };
 
   uint32_t carry[BPT];  // running output offset of each of this thread's digits
-  start_offsets(a, s, nb, g, carry, sh.scan32);
+  start_offsets(a, s, nb, FIRST ? g * kHistRows : g, carry, sh.scan32);
   const int tile0 = g * sp.tpb;
   const int tile1 = min(a.tiles, tile0 + sp.tpb);
   for (int tile = tile0; tile < tile1; ++tile) {
@@ -587,7 +598,7 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
     uint32_t ex = block_excl_scan_u32<NT>(sum, sh.part, tot);
 #pragma unroll
     for (int i = 0; i < OWN; ++i) {
-      carry[i] = ex + (owner ? a.block_hist[(size_t)g * kMaxBins + t * OWN + i] : 0u);
+      carry[i] = ex + (owner ? a.block_hist[(size_t)g * kHistRows * kMaxBins + t * OWN + i] : 0u);
       ex += c[i];
     }
   }
@@ -702,7 +713,7 @@ struct CountShared {
   uint64_t w[kMaxBins];
 };
 
-__device__ void count_block(const GArgs& a, int s, int g, Split sp, bool weights,
+__device__ void count_block(const GArgs& a, int s, int g, Split sp, int rows, bool weights,
                             CountShared& sh, int threads) {
   const Plan* pl = a.plan;
   const int t = threadIdx.x;
@@ -718,8 +729,8 @@ __device__ void count_block(const GArgs& a, int s, int g, Split sp, bool weights
     sh.w[b] = 0;
   }
   block_sync();
-  const int64_t lo = (int64_t)g * sp.tpb * T;
-  const int64_t hi = min(a.n, lo + (int64_t)sp.tpb * T);
+  int64_t lo, hi;
+  row_range(a, sp, g, rows, lo, hi);
   // lo is even (a multiple of the tile), so pairs of elements stay aligned
   const int64_t q0 = lo >> 1, q1 = hi >> 1;
   const ulonglong2* k2 = reinterpret_cast<const ulonglong2*>(keys_in);
@@ -749,11 +760,91 @@ __device__ void count_block(const GArgs& a, int s, int g, Split sp, bool weights
   }
 }
 
+// The big-tile final pass (below) handles final digits of at most 256
+// values with keys in the high word, two passes and lengths below 2^26.
+__device__ __forceinline__ bool use_big_final(const Plan* pl) {
+  return pl->packed && pl->W == 32 && pl->nscatter == 2 && pl->small && pl->nbins[1] <= 256;
+}
+
+// Final-digit histogram of one row when the big final pass runs (keys in the
+// high word, two passes, at most 256 final digits). Every wave counts into
+// bins of its own, so lanes of different waves never meet on an LDS address
+// (with few digits that contention dominated), and a bin's count and length
+// sum share one u64: the count above bit csh, the lengths below, which the
+// caller has checked cannot reach bit csh.
+constexpr int kHistFBins = 256;
+struct HistFShared {
+  uint64_t h[HT / kWave][kHistFBins];
+};
+
+__device__ void histF_fast(const GArgs& a, int row, int64_t lo, int64_t hi, uint32_t csh,
+                           HistFShared& sh) {
+  const Plan* pl = a.plan;
+  const int t = threadIdx.x;
+  const int w = wave_id();
+  const int nb = (int)pl->nbins[1];
+  const uint32_t d0 = (uint32_t)a.d0;
+  const uint32_t psh = pl->wh + d0;
+  const uint32_t H = pl->H;
+  const uint32_t mh = (1u << pl->wh) - 1;
+  const uint32_t lenmask = (1u << psh) - 1;
+  const uint32_t hoff = pl->hmin << d0;
+  const uint64_t one = 1ull << csh;
+  clear_wave_counters<4 * kHistFBins>(reinterpret_cast<uint16_t*>(sh.h[w]));
+  auto add = [&](uint64_t e) {
+    const uint32_t key = (uint32_t)(e >> 32);
+    const uint32_t d = __umul24(key >> psh, H) + ((key >> d0) & mh);
+    atomicAdd((unsigned long long*)&sh.h[w][d], (unsigned long long)(one | ((key & lenmask) + hoff)));
+  };
+  const uint64_t* keys_in = a.keys[0];
+  // lo is even (a multiple of the tile), so pairs of elements stay aligned
+  const int64_t q0 = lo >> 1, q1 = hi >> 1;
+  const ulonglong2* k2 = reinterpret_cast<const ulonglong2*>(keys_in);
+  for (int64_t q = q0 + t; q < q1; q += (int64_t)HT * HU) {
+    ulonglong2 v[HU];
+#pragma unroll
+    for (int u = 0; u < HU; ++u) v[u] = k2[min(q + (int64_t)u * HT, q1 - 1)];
+#pragma unroll
+    for (int u = 0; u < HU; ++u) {
+      if (q + (int64_t)u * HT < q1) {
+        add(v[u].x);
+        add(v[u].y);
+      }
+    }
+  }
+  if ((hi & 1) && t == 0 && hi > lo) add(keys_in[hi - 1]);
+  block_sync();
+  for (int b = t; b < nb; b += HT) {
+    uint64_t sum = 0;
+#pragma unroll
+    for (int v = 0; v < HT / kWave; ++v) sum += sh.h[v][b];
+    a.block_hist[(size_t)row * kMaxBins + b] = (uint32_t)(sum >> csh);
+    a.block_histw[(size_t)row * kMaxBins + b] = sum & (one - 1);
+  }
+}
+
 __global__ __launch_bounds__(HT) void g_histF(GArgs a) {
-  __shared__ CountShared sh;
+  __shared__ union {
+    CountShared generic;
+    HistFShared fast;
+  } sh;
   const Plan* pl = a.plan;
   if (!pl->ok) return;
-  count_block(a, (int)pl->nscatter - 1, blockIdx.x, a.fin, true, sh, HT);
+  const int row = blockIdx.x;
+  if (use_big_final(pl)) {
+    int64_t lo, hi;
+    row_range(a, a.fin, row, kHistRows, lo, hi);
+    // count above csh, lengths below: the row's lengths add up to less than
+    // items * (largest length + 1), which must stay below 2^csh
+    const uint32_t ib = bit_width32((uint32_t)max((int64_t)1, hi - lo));
+    const uint32_t lb = bit_width32(((pl->hmin + pl->H) << a.d0));
+    const uint32_t csh = 64 - ib;
+    if (ib + lb <= csh) {
+      histF_fast(a, row, lo, hi, csh, sh.fast);
+      return;
+    }
+  }
+  count_block(a, (int)pl->nscatter - 1, row, a.fin, kHistRows, true, sh.generic, HT);
 }
 
 // ---- middle passes: one launch of co-resident workgroups, grid barriers ----
@@ -801,7 +892,7 @@ __global__ __launch_bounds__(NT) void g_mid(GArgs a) {
   const int G = a.mid.blocks;
   uint32_t gen = 0;
   for (int s = 1; s < S - 1; ++s) {
-    if ((int)blockIdx.x < G) count_block(a, s, blockIdx.x, a.mid, false, sh.count, NT);
+    if ((int)blockIdx.x < G) count_block(a, s, blockIdx.x, a.mid, 1, false, sh.count, NT);
     if (!grid_barrier(a, ++gen)) return;
     for (int b = blockIdx.x; b < (int)pl->nbins[s]; b += gridDim.x)
       column_scan<NT>(a, s, b, false, G, sh.scan.scan32, sh.scan.scan64);
@@ -844,7 +935,7 @@ __device__ void final_generic(const GArgs& a, int g, FinalShared& sh) {
   for (int b = t; b < 256; b += NT) sh.clo[b] = sh.chi[b] = 0;
   // running position and wait offsets of this thread's digits
   uint32_t carry_c[BPT];
-  start_offsets(a, s, nb, g, carry_c, sh.scan32);
+  start_offsets(a, s, nb, g * kHistRows, carry_c, sh.scan32);
   uint64_t carry_w[BPT];
   {
     uint64_t wv[BPT];
@@ -860,7 +951,7 @@ __device__ void final_generic(const GArgs& a, int g, FinalShared& sh) {
 #pragma unroll
     for (int i = 0; i < BPT; ++i) {
       const int b = t * BPT + i;
-      carry_w[i] = ex + (b < nb ? a.block_histw[(size_t)g * kMaxBins + b] : 0ull);
+      carry_w[i] = ex + (b < nb ? a.block_histw[(size_t)g * kHistRows * kMaxBins + b] : 0ull);
       ex += wv[i];
     }
   }
@@ -1083,7 +1174,7 @@ __device__ void final_fast(const GArgs& a, int g, FinalFastShared& sh) {
   for (int c = t; c < 256; c += NT) sh.clo[c] = sh.chi[c] = 0;
   // running position and wait offsets of the owned digits
   uint32_t carry_c[OWN];
-  start_offsets(a, 1, nb, g, carry_c, sh.part_c);
+  start_offsets(a, 1, nb, g * kHistRows, carry_c, sh.part_c);
   uint64_t carry_w[OWN];
   {
     uint64_t wv[OWN];
@@ -1099,7 +1190,7 @@ __device__ void final_fast(const GArgs& a, int g, FinalFastShared& sh) {
 #pragma unroll
     for (int i = 0; i < OWN; ++i) {
       const int b = t * OWN + i;
-      carry_w[i] = ex + (b < nb ? a.block_histw[(size_t)g * kMaxBins + b] : 0ull);
+      carry_w[i] = ex + (b < nb ? a.block_histw[(size_t)g * kHistRows * kMaxBins + b] : 0ull);
       ex += wv[i];
     }
   }
@@ -1290,9 +1381,6 @@ struct FinalBigShared {
   uint64_t chunk[NWB];
 };
 
-__device__ __forceinline__ bool use_big_final(const Plan* pl) {
-  return pl->packed && pl->W == 32 && pl->nscatter == 2 && pl->small && pl->nbins[1] <= MAXB;
-}
 
 // Elements of one big tile of `cnt` items at item tb, round-major per wave.
 __device__ __forceinline__ void load_final_big(const uint64_t* keys, int64_t tb, int cnt,
@@ -1342,8 +1430,8 @@ __device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
     carry_c = block_excl_scan_u32<NTB>(c, sh.part_c, tc);
     carry_w = block_excl_scan_u64<NTB>(wv, sh.part_w, tw);
     if (owner) {
-      carry_c += a.block_hist[(size_t)g * kMaxBins + t];
-      carry_w += a.block_histw[(size_t)g * kMaxBins + t];
+      carry_c += a.block_hist[(size_t)g * kHistRows * kMaxBins + t];
+      carry_w += a.block_histw[(size_t)g * kHistRows * kMaxBins + t];
     }
   }
   uint32_t cur = ~0u;  // this lane's running wait total and its class - pmin
@@ -1566,8 +1654,9 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   hipLaunchKernelGGL(g_reset, dim3(1), dim3(1024), 0, st, a);
   const int vec_ok = ((uintptr_t)a.priority % 4 == 0) && ((uintptr_t)a.length % 16 == 0);
   const dim3 gm(a.main.blocks);
+  const dim3 gmh(a.main.blocks * kHistRows);
   mark(ev, 0, false, st);
-  hipLaunchKernelGGL(g_hist0, gm, dim3(HT), 0, st, a, vec_ok);
+  hipLaunchKernelGGL(g_hist0, gmh, dim3(HT), 0, st, a, vec_ok);
   mark(ev, 0, true, st);
   hipLaunchKernelGGL(g_scan, dim3((1u << a.d0) + 1), dim3(SCT), 0, st, a, 0);
   mark(ev, 1, false, st);
@@ -1580,7 +1669,7 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   mark(ev, 1, true, st);
   hipLaunchKernelGGL(g_mid, dim3(a.mid.blocks), dim3(NT), 0, st, a);
   const dim3 gf(a.fin.blocks);
-  hipLaunchKernelGGL(g_histF, gf, dim3(HT), 0, st, a);
+  hipLaunchKernelGGL(g_histF, dim3(a.fin.blocks * kHistRows), dim3(HT), 0, st, a);
   hipLaunchKernelGGL(g_scan, dim3(kMaxBins), dim3(SCT), 0, st, a, 1);
   mark(ev, 2, false, st);
   // exactly one of the two does the work; the plan on the device decides

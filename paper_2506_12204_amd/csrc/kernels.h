@@ -44,6 +44,12 @@ constexpr int kGlobalThreads = 512;
 constexpr int kGlobalRounds = 8;
 constexpr int kGlobalTile = kGlobalThreads * kGlobalRounds;
 constexpr int kFirstTiles = 4;   // the first pass works on 4 tiles at a time
+// Histogram rows per block of the first and final passes (a row is counted
+// by a workgroup of its own; a block's offsets are the column scan at its
+// first row). More rows did not speed the histograms up and slowed the column
+// scans, so each block is one row.
+constexpr int kHistRows = 1;
+static_assert(kFirstTiles % kHistRows == 0, "a block splits into whole-tile rows");
 constexpr int kMaxBlocks = 4096; // upper bound on workgroups of a pass
 
 // Decided on the device by the histogram pass once the ranges are known.
