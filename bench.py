@@ -36,7 +36,7 @@ STAGE_BYTES = {
     "final": 20,  # read the element (8 B), write order (4 B) + wait (8 B)
 }
 PATH_BYTES = 17  # the whole schedule's own inputs + outputs per request
-COUNTERS = os.path.join(ROOT, "profiles", "final_pass_c3_counters.json")
+COUNTERS = os.path.join(ROOT, "profiles", "final_pass_c3_counters.md")
 FINAL_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "global_sort.hip")
 
 
@@ -67,24 +67,58 @@ class HipEvents:
         self.rt.hipEventDestroy(ctypes.c_void_p(ev))
 
 
-def file_sha(path: str) -> str:
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def code_sha(path: str) -> str:
+    """SHA-256 of a C++ source with its // comments and blank lines removed:
+    what identifies the kernel a counter measurement belongs to."""
+    lines = []
+    with open(path) as f:
+        for line in f:
+            code = line.split("//", 1)[0].rstrip()
+            if code:
+                lines.append(code)
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()
 
 
 def counter_traffic(n: int):
     """HBM bytes per launch of the final pass from committed rocprofv3 counters.
 
-    Null when the counters were taken on a different version of the kernel
-    source (the file records the source's SHA-256 at collection time).
+    The summary file carries `key: value` lines (n, code_sha256,
+    hbm_bytes_per_launch). Null when the counters were taken on a different
+    version of the kernel source (comments aside) or another request count.
     """
     if not os.path.exists(COUNTERS):
         return None
+    kv = {}
     with open(COUNTERS) as f:
-        c = json.load(f)
-    if c.get("source_sha256") != file_sha(FINAL_SOURCE) or c.get("n") != n:
+        for line in f:
+            if ":" in line and not line.startswith(("|", "#", " ")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip().strip("`")
+    if kv.get("code_sha256") != code_sha(FINAL_SOURCE) or kv.get("n") != str(n):
         return None
-    return c.get("hbm_bytes_per_launch")
+    return float(kv["hbm_bytes_per_launch"])
+
+
+def copy_probe() -> int:
+    """Plain 1 GiB device-to-device copy: the calibration run for the byte
+    counters (FETCH_SIZE / WRITE_SIZE of a copy of known size)."""
+    import torch
+    n = 1 << 28  # int32 elements
+    a = torch.ones(n, dtype=torch.int32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(10):
+        b.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / 10
+    print(json.dumps({"copy_bytes": 4 * n, "ms": ms, "read_plus_write_GBps": 8 * n / ms / 1e6}))
+    return 0
 
 
 def cpu_baseline(p, l, order, wait, totals):
@@ -106,7 +140,11 @@ def main() -> int:
     ap.add_argument("--workload", default="c3", choices=["c3", "c2"])
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle leg (profiling runs)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only time a 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
+    if args.copy_probe:
+        return copy_probe()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the schedule of one queue is not split "
               f"across GPUs in this build (asked for --gpus {args.gpus}).", file=sys.stderr)

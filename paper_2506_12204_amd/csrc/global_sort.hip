@@ -6,32 +6,34 @@
 // waits of Eq. 1 (the exclusive prefix of service times) and exact per-class
 // totals, all fused into the last pass.
 //
-// Every pass splits the queue into the same blocks of consecutive tiles, one
+// Every pass splits the queue into static blocks of consecutive tiles, one
 // block per workgroup. A pass first counts the digits of every block, a
 // column scan turns the counts into per-block offsets, and the scatter then
 // walks its block tile by tile with running per-digit offsets. No workgroup
 // ever waits for another inside a kernel, and consecutive tiles of a digit
 // land next to each other in memory, written by the same workgroup.
 //
-//   g_reset   clear the small per-call state and the totals.
-//   g_hist0   read (priority, length) once: validate, find the ranges and
-//             count the low `d0` bits of every length per block. That digit
-//             does not depend on the ranges, so no separate min/max pass is
-//             needed.
-//   g_scan    per-block digit offsets of one pass (column scans); for the
-//             first pass one more workgroup reduces the block ranges into
-//             the Plan.
-//   g_first   first scatter pass: packs every request into one u64 element
-//               (p - pmin | (len >> d0) - hmin | len & (2^d0 - 1) | id)
-//             and scatters it by the low length digit.
-//   g_mid     middle passes, only for very wide key ranges: count, scan and
-//             scatter by 10-bit digits of u2 = (p - pmin) * H + h, in one
-//             launch of co-resident workgroups with grid barriers between the
-//             phases; it returns at once when two passes suffice.
-//   g_histF   counts and length sums of the final digit per block.
-//   g_final   final scatter by the top digit of u2 with running count and
-//             length offsets: each request's position and wait come out of
-//             the same pass, plus the per-class totals.
+//   g_reset      clear the small per-call state and the totals.
+//   g_hist0      read (priority, length) once: validate, find the ranges and
+//                count the low `d0` bits of every length per block. That
+//                digit does not depend on the ranges, so no separate min/max
+//                pass is needed.
+//   g_scan       per-block digit offsets of one pass (column scans); for the
+//                first pass one more workgroup reduces the block ranges into
+//                the Plan.
+//   g_first      first scatter pass: packs every request into one u64
+//                element (key above id) and scatters it by the low length
+//                digit, on 16K-item tiles.
+//   g_mid        middle passes, only for very wide key ranges: count, scan
+//                and scatter by 10-bit digits of u2 = (p - pmin) * H + h, in
+//                one launch of co-resident workgroups with grid barriers
+//                between the phases; it returns at once when two passes
+//                suffice.
+//   g_histF      counts and length sums of the final digit per block.
+//   g_final_big  final scatter for at most 256 final digits on 16K-item
+//                tiles; g_final does the same for wider digits on 4K-item
+//                tiles, and the general cases. Each request's position and
+//                wait come out of the same pass, plus the per-class totals.
 #include "block_common.h"
 #include "kernels.h"
 
