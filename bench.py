@@ -30,11 +30,20 @@ sys.path.insert(0, ROOT)
 METRIC = "scheduled requests/sec + achieved HBM GB/s, single queue n=2^26, 1 GPU"
 HBM_PEAK_GBPS = 8000.0
 # Algorithmic bytes per request moved by each stage of the long-queue path.
-STAGE_BYTES = {
-    "hist": 5,    # read priority (1 B) + length (4 B)
-    "first": 13,  # read priority + length (5 B), write the packed u64 element (8 B)
-    "final": 20,  # read the element (8 B), write order (4 B) + wait (8 B)
-}
+# The n = 2^26 queue takes the compact layout (u32 elements between the
+# passes); SEMSCHED_NO_COMPACT=1 forces the u64 element layout.
+if os.environ.get("SEMSCHED_NO_COMPACT") == "1":
+    STAGE_BYTES = {
+        "hist": 5,    # read priority (1 B) + length (4 B)
+        "first": 13,  # read priority + length (5 B), write the packed u64 element (8 B)
+        "final": 20,  # read the element (8 B), write order (4 B) + wait (8 B)
+    }
+else:
+    STAGE_BYTES = {
+        "hist": 5,    # read priority (1 B) + length (4 B)
+        "first": 9,   # read priority + length (5 B), write the u32 element (4 B)
+        "final": 16,  # read the element (4 B), write order (4 B) + wait (8 B)
+    }
 PATH_BYTES = 17  # the whole schedule's own inputs + outputs per request
 COUNTERS = os.path.join(ROOT, "profiles", "final_pass_c3_counters.md")
 FINAL_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "global_sort.hip")

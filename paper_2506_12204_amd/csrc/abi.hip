@@ -25,7 +25,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
   size_t flags = 0, barrier = 8, plan = 64;
   size_t hist_cnt = 0, hist_w = 0, block_hist = 0, block_histw = 0, block_ranges = 0;
-  size_t keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0;
+  size_t keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0, chunk_part = 0, sub_start = 0;
   size_t total = kHeaderBytes;
   int64_t tiles = 0;
 };
@@ -54,6 +54,8 @@ Layout layout_for(int64_t n) {
   L.block_hist = take(sizeof(uint32_t) * kMaxBins * blocks);
   L.block_histw = take(sizeof(uint64_t) * kMaxBins * blocks);
   L.block_ranges = take(sizeof(uint32_t) * 4 * blocks);
+  L.chunk_part = take(sizeof(uint32_t) * kMaxChunks * kMaxBins);
+  L.sub_start = take(sizeof(uint32_t) * kMaxChunks * kMaxBins);
   L.keys0 = take(8 * (size_t)n);
   L.keys1 = take(8 * (size_t)n);
   L.ids0 = take(4 * (size_t)n);
@@ -73,6 +75,13 @@ int d0_bits() {
 // need); it lets that layout be exercised on small queues.
 int force_wide() {
   const char* e = std::getenv("SEMSCHED_FORCE_WIDE");
+  return (e && e[0] == '1') ? 1 : 0;
+}
+
+// SEMSCHED_NO_COMPACT=1 keeps the two-pass queues on the u64 element layout
+// (the one queues longer than 2^30 requests use), so that layout stays testable.
+int no_compact() {
+  const char* e = std::getenv("SEMSCHED_NO_COMPACT");
   return (e && e[0] == '1') ? 1 : 0;
 }
 
@@ -195,6 +204,13 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   g.main = global_first_split(n);
   g.fin = global_final_split(n);
   g.mid = global_mid_split(n);
+  g.kchunks = (int32_t)((n + (1ll << kChunkBits) - 1) >> kChunkBits);
+  g.kpb = 0;
+  while ((1 << g.kpb) < g.kchunks) ++g.kpb;
+  // every chunk boundary must fall inside one block of the first pass
+  const int64_t block_items = (int64_t)g.main.tpb * kGlobalTile;
+  g.chunked = (!no_compact() && g.kchunks <= kMaxChunks &&
+               block_items <= (1ll << kChunkBits)) ? 1 : 0;
   g.flags = reinterpret_cast<uint32_t*>(base + L.flags);
   g.barrier = reinterpret_cast<uint32_t*>(base + L.barrier);
   g.block_ranges = reinterpret_cast<uint32_t*>(base + L.block_ranges);
@@ -207,6 +223,8 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   g.keys[1] = reinterpret_cast<uint64_t*>(base + L.keys1);
   g.ids[0] = reinterpret_cast<uint32_t*>(base + L.ids0);
   g.ids[1] = reinterpret_cast<uint32_t*>(base + L.ids1);
+  g.chunk_part = reinterpret_cast<uint32_t*>(base + L.chunk_part);
+  g.sub_start = reinterpret_cast<uint32_t*>(base + L.sub_start);
   StageEvents ev = {};
   bool armed = false;
   {

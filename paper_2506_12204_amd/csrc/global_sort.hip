@@ -170,22 +170,39 @@ __device__ void write_plan(const GArgs& a, int G) {
   pl->nbins[1 + mids] = fb;
   pl->nbits[1 + mids] = bit_width32(fb - 1);
   pl->nscatter = 2 + mids;
+  // compact layout: two passes, at most 256 final digits (the big-tile final
+  // pass), lengths below 2^26, and the sub-bucket starts were counted
+  pl->compact = (a.chunked && !a.force_wide && mids == 0 && fb <= 256 && pl->small) ? 1u : 0u;
   pl->ok = 1;
 }
 
 __global__ __launch_bounds__(HT) void g_hist0(GArgs a, int vec_ok) {
   constexpr int HW = HT / kWave;
   __shared__ uint32_t s_hist[kMaxBins];
+  __shared__ uint32_t s_part[kMaxBins];
   __shared__ uint32_t s_red[4][HW];
   const int t = threadIdx.x;
   const int g = blockIdx.x;
   const int nb = 1 << a.d0;
   const uint32_t mask = (uint32_t)nb - 1;
-  for (int b = t; b < nb; b += HT) s_hist[b] = 0;
-  block_sync();
 
   int64_t lo, hi;
   row_range(a, a.main, g, kHistRows, lo, hi);
+  // The first chunk boundary at or after lo, if it lies in this row: the
+  // row also counts the first digits of its ids below it (none when the
+  // boundary is lo itself). A row is never longer than a chunk, so it holds
+  // at most one boundary.
+  int64_t bnd = -1;
+  if (a.chunked && hi > lo) {
+    const int64_t c = ((lo + (1ll << kChunkBits) - 1) >> kChunkBits) << kChunkBits;
+    if (c > 0 && c < hi) bnd = c;
+  }
+  for (int b = t; b < nb; b += HT) {
+    s_hist[b] = 0;
+    s_part[b] = 0;
+  }
+  block_sync();
+
   Ranges rg;
   int64_t scalar_from = lo;
   if (vec_ok && hi > lo) {
@@ -208,13 +225,23 @@ __global__ __launch_bounds__(HT) void g_hist0(GArgs a, int vec_ok) {
           rg.add((pv[u] >> 8) & 0xff, lv[u].y, a.num_classes, mask, s_hist);
           rg.add((pv[u] >> 16) & 0xff, lv[u].z, a.num_classes, mask, s_hist);
           rg.add(pv[u] >> 24, lv[u].w, a.num_classes, mask, s_hist);
+          // the boundary is a multiple of 4: a quad is below it or not
+          if (4 * (q + (int64_t)u * HT) < bnd) {
+            atomicAdd(&s_part[(uint32_t)lv[u].x & mask], 1u);
+            atomicAdd(&s_part[(uint32_t)lv[u].y & mask], 1u);
+            atomicAdd(&s_part[(uint32_t)lv[u].z & mask], 1u);
+            atomicAdd(&s_part[(uint32_t)lv[u].w & mask], 1u);
+          }
         }
       }
     }
     scalar_from = q1 * 4;
   }
-  for (int64_t i = scalar_from + t; i < hi; i += HT)
-    rg.add(a.priority[i], a.length[i], a.num_classes, mask, s_hist);
+  for (int64_t i = scalar_from + t; i < hi; i += HT) {
+    const int32_t l = a.length[i];
+    rg.add(a.priority[i], l, a.num_classes, mask, s_hist);
+    if (i < bnd) atomicAdd(&s_part[(uint32_t)l & mask], 1u);
+  }
 
   const uint32_t lmin = wave_min_u32(rg.lmin), lmax = wave_max_u32(rg.lmax);
   const uint32_t pmin = wave_min_u32(rg.pmin), pmax = wave_max_u32(rg.pmax);
@@ -244,6 +271,12 @@ __global__ __launch_bounds__(HT) void g_hist0(GArgs a, int vec_ok) {
     r[3] = bh;
   }
   for (int b = t; b < nb; b += HT) a.block_hist[(size_t)g * kMaxBins + b] = s_hist[b];
+  // (a request with a range error makes the whole call fail, so counting it
+  // in s_part does not matter)
+  if (bnd >= 0) {
+    uint32_t* part = a.chunk_part + (size_t)(bnd >> kChunkBits) * kMaxBins;
+    for (int b = t; b < nb; b += HT) part[b] = s_part[b];
+  }
 }
 
 // ------------------------------------------------------------------------
@@ -251,9 +284,14 @@ __global__ __launch_bounds__(HT) void g_hist0(GArgs a, int vec_ok) {
 // before g (block_histw likewise for length sums); the totals go to
 // hist_cnt[s][b] (and hist_w[b]).
 
+// With `chunks` (first digit of the compact layout), column b also yields
+// the starts of its sub-buckets relative to the bucket's start:
+// sub_start[b][k] = number of ids below k * 2^kChunkBits with first digit b =
+// the column prefix at the row holding that boundary + the row's own count
+// below it (chunk_part). Entry 0 is 0; entries K .. Kp-1 hold the bucket size.
 template <int THREADS>
 __device__ void column_scan(const GArgs& a, int s, int b, bool weights, int G,
-                            uint32_t* scan32, uint64_t* scan64) {
+                            uint32_t* scan32, uint64_t* scan64, bool chunks = false) {
   constexpr int SCPER = kMaxBlocks / THREADS;
   const int per = (G + THREADS - 1) / THREADS;
   const int g0 = (int)threadIdx.x * per;
@@ -267,12 +305,31 @@ __device__ void column_scan(const GArgs& a, int s, int b, bool weights, int G,
   }
   uint32_t total;
   uint32_t run = block_excl_scan_u32<THREADS>(local, scan32, total);
+  const int64_t row_items = (int64_t)(a.main.tpb / kHistRows) * T;
+  uint32_t* sub = a.sub_start + ((size_t)b << a.kpb);
 #pragma unroll
   for (int i = 0; i < SCPER; ++i) {
-    if (i < per && g0 + i < G) a.block_hist[(size_t)(g0 + i) * kMaxBins + b] = run;
+    const int g = g0 + i;
+    if (i < per && g < G) {
+      a.block_hist[(size_t)g * kMaxBins + b] = run;
+      if (chunks) {
+        const int64_t lo = (int64_t)g * row_items;
+        const int64_t c = ((lo + (1ll << kChunkBits) - 1) >> kChunkBits) << kChunkBits;
+        if (c > 0 && c < min(a.n, lo + row_items)) {
+          const int k = (int)(c >> kChunkBits);
+          sub[k] = run + a.chunk_part[(size_t)k * kMaxBins + b];
+        }
+      }
+    }
     run += v[i];
   }
-  if (threadIdx.x == 0) a.hist_cnt[s * kMaxBins + b] = total;
+  if (threadIdx.x == 0) {
+    a.hist_cnt[s * kMaxBins + b] = total;
+    if (chunks) {
+      sub[0] = 0;
+      for (int k = a.kchunks; k < (1 << a.kpb); ++k) sub[k] = total;
+    }
+  }
   if (!weights) return;
   uint64_t wv[SCPER];
   uint64_t wl = 0;
@@ -304,7 +361,8 @@ __global__ __launch_bounds__(SCT) void g_scan(GArgs a, int final) {
       write_plan(a, a.main.blocks * kHistRows);
       return;
     }
-    column_scan<SCT>(a, 0, b, false, a.main.blocks * kHistRows, scan32, scan64);
+    column_scan<SCT>(a, 0, b, false, a.main.blocks * kHistRows, scan32, scan64,
+                     a.chunked != 0);
     return;
   }
   const Plan* pl = a.plan;
@@ -566,7 +624,10 @@ __device__ __forceinline__ void clear_wave_counters(uint16_t* cnt) {
   for (int i = 0; i < NBIN / (kWave * 4); ++i) c64[i * kWave + lane_id()] = 0;
 }
 
-template <int D0>
+// COMPACT: the element written is the compact u32 (final digit u2 above the
+// low kChunkBits bits of the id); the key ranked and staged is then
+// u2 << D0 | first digit instead of the packed key.
+template <int D0, bool COMPACT>
 __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
   constexpr int NBIN = 1 << D0;
   constexpr uint32_t M0 = NBIN - 1;
@@ -581,7 +642,9 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
   const uint32_t pmin = pl->pmin;
   const uint32_t psh = pl->wh + D0;
   const uint32_t hoff = pl->hmin << D0;
+  const uint32_t H = pl->H;
   uint64_t* out = a.keys[0];
+  uint32_t* out32 = reinterpret_cast<uint32_t*>(a.keys[0]);
   uint16_t* mycnt = sh.cnt[w];
   clear_wave_counters<NBIN>(mycnt);
 
@@ -612,11 +675,14 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
   load_first(a, lo, (int)min((int64_t)T1, hi - lo), pv, lv);
   for (int64_t tb = lo; tb < hi; tb += T1) {
     const int cv = (int)min((int64_t)T1, hi - tb);
-    // key = (p - pmin) << (wh + d0) | ((l >> d0) - hmin) << d0 | (l & M0); its
-    // low D0 bits are the digit
+    // key = (p - pmin) << (wh + d0) | ((l >> d0) - hmin) << d0 | (l & M0), or
+    // for COMPACT u2 << d0 | (l & M0) with u2 = (p - pmin) * H + (l >> d0) - hmin;
+    // either way its low D0 bits are the digit
     uint32_t key[R1], rk[R1];
 #pragma unroll
-    for (int r = 0; r < R1; ++r) key[r] = ((pv[r] - pmin) << psh) + (lv[r] - hoff);
+    for (int r = 0; r < R1; ++r)
+      key[r] = (COMPACT ? (__umul24(pv[r] - pmin, H) << D0) : ((pv[r] - pmin) << psh)) +
+               (lv[r] - hoff);
     if (cv < T1) {
       // items past the end take the last digit: they rank after every real
       // item of it, i.e. at the tile positions >= cv, which are not written
@@ -681,7 +747,13 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
       if (full || j < cv) {
         const uint64_t e = sh.stage[j];
         const uint32_t pos = sh.base[(uint32_t)(e >> 32) & M0] + (uint32_t)j;
-        if (pos < (uint64_t)a.n) out[pos] = e;  // always true for consistent counts
+        if (pos < (uint64_t)a.n) {  // always true for consistent counts
+          if (COMPACT)  // u2 above the id's low bits
+            out32[pos] = (((uint32_t)(e >> 32) >> D0) << kChunkBits) |
+                         ((uint32_t)e & ((1u << kChunkBits) - 1));
+          else
+            out[pos] = e;
+        }
       }
       // keep the scheduler from hoisting every round's loads at once, which
       // would hold ~5 registers per round live
@@ -703,8 +775,10 @@ __global__ __launch_bounds__(NT, 2) void g_first(GArgs a) {
   } sh;
   const Plan* pl = a.plan;
   if (!pl->ok) return;
-  if (pl->packed && pl->W == 32)
-    first_fast<D0>(a, blockIdx.x, sh.fast);
+  if (pl->compact)
+    first_fast<D0, true>(a, blockIdx.x, sh.fast);
+  else if (pl->packed && pl->W == 32)
+    first_fast<D0, false>(a, blockIdx.x, sh.fast);
   else
     scatter_block<true>(a, 0, blockIdx.x, a.main, sh.generic);
 }
@@ -825,14 +899,150 @@ __device__ void histF_fast(const GArgs& a, int row, int64_t lo, int64_t hi, uint
   }
 }
 
+// ---- compact layout: positions -> (first digit, id chunk) ----------------------
+
+// bstart[d] = position of the first element of first-digit bucket d after the
+// first pass (exclusive scan of that pass's digit totals), for d < 2^d0, and
+// bstart[2^d0] = n. Every thread of the workgroup must call it.
+template <int THREADS>
+__device__ void bucket_starts(const GArgs& a, uint32_t* bstart, uint32_t* scan32) {
+  constexpr int PER = kMaxBins / THREADS;
+  const int nd = 1 << a.d0;
+  uint32_t c[PER];
+  uint32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int d = threadIdx.x * PER + i;
+    c[i] = d < nd ? a.hist_cnt[d] : 0u;
+    sum += c[i];
+  }
+  uint32_t tot;
+  uint32_t ex = block_excl_scan_u32<THREADS>(sum, scan32, tot);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int d = threadIdx.x * PER + i;
+    if (d <= nd) bstart[d] = ex;  // d == nd: the total
+    ex += c[i];
+  }
+  if (threadIdx.x == 0 && nd == kMaxBins) bstart[nd] = tot;
+  block_sync();
+}
+
+// Last bucket d < nd with bstart[d] <= pos. Empty buckets share their start
+// with the next one, so the bucket found is the one that holds pos.
+__device__ __forceinline__ int bucket_of(const uint32_t* bstart, int nd, uint32_t pos) {
+  int lo = 0, hi = nd - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (bstart[mid] <= pos) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Class (relative, p - pmin) of final digit u2 = class * H + h: u2 / H by a
+// multiply with m = ceil(2^22 / H). Exact for u2 < 1024 and H <= 1024: the
+// product exceeds u2 * 2^22 / H by less than u2 / 2^22 < 1/1024 <= 1/H, and
+// u2 * m < 2^32.
+__device__ __forceinline__ uint32_t div_magic(uint32_t H) {
+  return ((1u << 22) + H - 1) / H;
+}
+__device__ __forceinline__ uint32_t class_of(uint32_t u2, uint32_t magic) {
+  return (u2 * magic) >> 22;
+}
+
+// Final-digit histogram of one row for the compact layout: per final digit
+// the count and the sum of first digits (the element holds the final digit;
+// the first digit is the bucket its position lies in, followed by a cursor,
+// since a thread's positions increase). The row's length sum of digit u2 is
+// count * (h + hmin) * 2^d0 + that sum.
+struct HistFCompactShared {
+  uint64_t h[HT / kWave][kHistFBins];
+  uint32_t bstart[kMaxBins + 1];
+  uint32_t scan32[HT / kWave + 1];
+};
+
+__device__ void histF_compact(const GArgs& a, int row, int64_t lo, int64_t hi,
+                              HistFCompactShared& sh) {
+  // count above bit 36: a row holds fewer than 2^23 elements, so its first
+  // digits add up to less than 2^33
+  constexpr uint32_t CSH = 36;
+  const Plan* pl = a.plan;
+  const int t = threadIdx.x;
+  const int w = wave_id();
+  const int nb = (int)pl->nbins[1];
+  const int nd = 1 << a.d0;
+  clear_wave_counters<4 * kHistFBins>(reinterpret_cast<uint16_t*>(sh.h[w]));
+  bucket_starts<HT>(a, sh.bstart, sh.scan32);  // (ends with a barrier)
+
+  const uint32_t* keys_in = reinterpret_cast<const uint32_t*>(a.keys[0]);
+  uint64_t* bins = sh.h[w];
+  // lo is a multiple of 4 (of the tile), so quads of elements stay aligned
+  const int64_t q0 = lo >> 2, q1 = hi >> 2;
+  const uint4* k4 = reinterpret_cast<const uint4*>(keys_in);
+  int d = 0;
+  uint32_t nxt = 0;  // start of bucket d + 1
+  if (q0 + t < q1) {
+    d = bucket_of(sh.bstart, nd, (uint32_t)(4 * (q0 + t)));
+    nxt = sh.bstart[d + 1];
+  }
+  auto add = [&](uint32_t e, uint32_t pos) {
+    while (pos >= nxt) nxt = sh.bstart[++d + 1];
+    atomicAdd((unsigned long long*)&bins[(e >> kChunkBits) & (kHistFBins - 1)],
+              (unsigned long long)((1ull << CSH) | (uint32_t)d));
+  };
+  for (int64_t q = q0 + t; q < q1; q += (int64_t)HT * HU) {
+    uint4 v[HU];
+#pragma unroll
+    for (int u = 0; u < HU; ++u) v[u] = k4[min(q + (int64_t)u * HT, q1 - 1)];
+#pragma unroll
+    for (int u = 0; u < HU; ++u) {
+      const int64_t qq = q + (int64_t)u * HT;
+      if (qq < q1) {
+        const uint32_t p0 = (uint32_t)(4 * qq);
+        add(v[u].x, p0);
+        add(v[u].y, p0 + 1);
+        add(v[u].z, p0 + 2);
+        add(v[u].w, p0 + 3);
+      }
+    }
+  }
+  // the last (n % 4) elements of the queue
+  if (t < (int)(hi - 4 * q1)) {
+    const uint32_t pos = (uint32_t)(4 * q1 + t);
+    d = bucket_of(sh.bstart, nd, pos);
+    nxt = sh.bstart[d + 1];
+    add(keys_in[pos], pos);
+  }
+  block_sync();
+  const uint32_t H = pl->H;
+  const uint32_t magic = div_magic(H);
+  for (int b = t; b < nb; b += HT) {
+    uint64_t sum = 0;
+#pragma unroll
+    for (int v = 0; v < HT / kWave; ++v) sum += sh.h[v][b];
+    const uint64_t cnt = sum >> CSH;
+    const uint32_t hh = (uint32_t)b - class_of((uint32_t)b, magic) * H;
+    a.block_hist[(size_t)row * kMaxBins + b] = (uint32_t)cnt;
+    a.block_histw[(size_t)row * kMaxBins + b] =
+        cnt * ((uint64_t)(hh + pl->hmin) << a.d0) + (sum & ((1ull << CSH) - 1));
+  }
+}
+
 __global__ __launch_bounds__(HT) void g_histF(GArgs a) {
   __shared__ union {
     CountShared generic;
     HistFShared fast;
+    HistFCompactShared compact;
   } sh;
   const Plan* pl = a.plan;
   if (!pl->ok) return;
   const int row = blockIdx.x;
+  if (pl->compact) {
+    int64_t lo, hi;
+    row_range(a, a.fin, row, kHistRows, lo, hi);
+    histF_compact(a, row, lo, hi, sh.compact);
+    return;
+  }
   if (use_big_final(pl)) {
     int64_t lo, hi;
     row_range(a, a.fin, row, kHistRows, lo, hi);
@@ -1573,11 +1783,277 @@ __device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
   }
 }
 
-__global__ __launch_bounds__(NTB) void g_final_big(GArgs a) {
-  __shared__ FinalBigShared sh;
+// ---- compact final pass ------------------------------------------------------
+// The big-tile final pass over compact u32 elements. An element holds its
+// final digit u2 and the low kChunkBits bits of its id; its first digit d and
+// id chunk k come from its position: the first pass left bucket d in id
+// order, so bucket d splits into sub-buckets (d, k) of consecutive positions,
+// and sub-bucket (d, k) starts at bstart[d] + sub_start[d][k]. These starts
+// increase with (d, k); the sub-bucket of a position is the last one whose
+// start is not above it (empty sub-buckets share the next one's start, so
+// the one found always holds the position). A workgroup copies the starts of
+// the buckets its positions span into LDS (`win`) when they fit, narrows them
+// per tile, and binary-searches each element's position among them; when
+// they do not fit it searches the table in global memory instead.
+// Per element: length = ((h + hmin) << d0) + d and id = k << kChunkBits | low
+// bits; the staged value carries (u2, d) and the id, the rest is the
+// big-tile final pass.
+
+constexpr int kWinCap = 512;
+
+struct FinalCompactShared {
+  uint64_t stage[TB];
+  uint16_t cnt[NWB][MAXB];     // wave counters, then the waves' tile offsets
+  uint32_t base_c[MAXB];       // output position of the tile's first item of a digit
+  uint64_t base_w[MAXB];       // wait base of a digit in this tile
+  uint64_t wsum[MAXB];         // length sums of the tile's digits
+  uint64_t clo[256], chi[256]; // class totals, low and high words
+  uint32_t bstart[kMaxBins + 1];
+  uint32_t win[kWinCap];       // absolute sub-bucket starts of this block's buckets
+  uint32_t part_c[NWB + 1];
+  uint64_t part_w[NWB + 1];
+  uint64_t chunk[NWB];
+};
+
+__device__ __forceinline__ void load_final_compact(const uint32_t* keys, int64_t tb, int cnt,
+                                                   uint32_t (&e)[KB]) {
+  const int wb = wave_id() * kWave * KB;
+  const int lim = __builtin_amdgcn_readfirstlane(max(0, min(cnt - wb, kWave * KB)));
+  const __amdgpu_buffer_rsrc_t rk = raw_rsrc(keys + tb + wb, (uint32_t)lim * 4u);
+  const int lane = lane_id();
+#pragma unroll
+  for (int r = 0; r < KB; ++r)
+    e[r] = __builtin_amdgcn_raw_buffer_load_b32(rk, (lane + r * kWave) * 4, 0, 0);
+}
+
+__device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
+  const int t = threadIdx.x;
+  const int lane = lane_id();
+  const int w = wave_id();
+  const int wb = w * kWave * KB;
   const Plan* pl = a.plan;
-  if (!pl->ok || !use_big_final(pl)) return;
-  final_big(a, blockIdx.x, sh);
+  const int nb = (int)pl->nbins[1];
+  const bool owner = t < nb;
+  const uint32_t d0 = (uint32_t)a.d0;
+  const int nd = 1 << a.d0;
+  const uint32_t H = pl->H;
+  const uint32_t hmin = pl->hmin;
+  const uint32_t magic = div_magic(H);
+  const int kpb = a.kpb;
+  const uint32_t* keys_in = reinterpret_cast<const uint32_t*>(a.keys[0]);
+  uint16_t* mycnt = sh.cnt[w];
+  auto len_of = [&](uint32_t u2, uint32_t d) {
+    return ((u2 - class_of(u2, magic) * H + hmin) << d0) + d;
+  };
+
+  clear_wave_counters<MAXB>(mycnt);
+  if (t < MAXB) sh.wsum[t] = 0;
+  if (t < 256) sh.clo[t] = sh.chi[t] = 0;
+  bucket_starts<NTB>(a, sh.bstart, sh.part_c);
+  uint32_t carry_c;
+  uint64_t carry_w;
+  {
+    const uint32_t c = owner ? a.hist_cnt[kMaxBins + t] : 0u;
+    const uint64_t wv = owner ? a.hist_w[t] : 0ull;
+    uint32_t tc;
+    uint64_t tw;
+    carry_c = block_excl_scan_u32<NTB>(c, sh.part_c, tc);
+    carry_w = block_excl_scan_u64<NTB>(wv, sh.part_w, tw);
+    if (owner) {
+      carry_c += a.block_hist[(size_t)g * kHistRows * kMaxBins + t];
+      carry_w += a.block_histw[(size_t)g * kHistRows * kMaxBins + t];
+    }
+  }
+  uint32_t cur = ~0u;  // this lane's running wait total and its class - pmin
+  U128 acc = {0, 0};
+
+  const int64_t lo = (int64_t)g * a.fin.tpb * T;
+  const int64_t hi = min(a.n, lo + (int64_t)a.fin.tpb * T);
+  // sub-bucket starts of the buckets [d_lo, d_hi] that this block's positions span
+  const int d_lo = hi > lo ? bucket_of(sh.bstart, nd, (uint32_t)lo) : 0;
+  const int d_hi = hi > lo ? bucket_of(sh.bstart, nd, (uint32_t)(hi - 1)) : 0;
+  const int win0 = d_lo << kpb;
+  const int wn = (d_hi - d_lo + 1) << kpb;
+  const bool in_lds = wn <= kWinCap;
+  if (in_lds) {
+    for (int j = t; j < wn; j += NTB)
+      sh.win[j] = sh.bstart[(win0 + j) >> kpb] + a.sub_start[win0 + j];
+  }
+  block_sync();
+  auto sb = [&](int j) -> uint32_t {
+    return in_lds ? sh.win[j] : sh.bstart[(win0 + j) >> kpb] + a.sub_start[win0 + j];
+  };
+  // last j in [jl, jh] with sb(j) <= pos, given sb(jl) <= pos: binary
+  // lifting with steps from the largest power of two <= jh - jl down to 1
+  // (jl and jh are uniform, so the trip count is)
+  auto find = [&](uint32_t pos, int jl, int jh) {
+    const int span = jh - jl;
+    for (int step = span > 0 ? 1 << (31 - __clz(span)) : 0; step > 0; step >>= 1) {
+      const int c = min(jl + step, jh);
+      if (sb(c) <= pos) jl = c;
+    }
+    return jl;
+  };
+
+  uint32_t e[KB];
+  load_final_compact(keys_in, lo, (int)min((int64_t)TB, hi - lo), e);
+  for (int64_t tb = lo; tb < hi; tb += TB) {
+    const int cv = (int)min((int64_t)TB, hi - tb);
+    const bool full = cv == TB;
+    // the sub-buckets this tile's positions lie in
+    const int ja = find((uint32_t)tb, 0, wn - 1);
+    const int jb = find((uint32_t)(tb + cv - 1), ja, wn - 1);
+
+    // ---- phase 1: decode, tile length sums per digit, ranks --------------
+    // rw[r] = the item's rank (below 2^14) | its window index << 14 (below 2^18)
+    auto digit_of = [&](int r) {  // past the end: the last digit
+      return (!full && wb + r * kWave + lane >= cv) ? (uint32_t)nb - 1
+                                                    : (e[r] >> kChunkBits) & (MAXB - 1);
+    };
+    uint32_t rw[KB];
+#pragma unroll
+    for (int r = 0; r < KB; ++r) {
+      const int j = wb + r * kWave + lane;
+      const bool past = !full && j >= cv;
+      const uint32_t jj = (uint32_t)find((uint32_t)(tb + j), ja, jb);
+      const uint32_t d = (uint32_t)((win0 + (int)jj) >> kpb);
+      const uint32_t dg = digit_of(r);
+      const uint32_t ls = past ? 0u : len_of(dg, d);
+      atomicAdd((unsigned long long*)&sh.wsum[dg], (unsigned long long)ls);
+      rw[r] = rank_round_c<8>(dg, mycnt) | (jj << 14);
+    }
+    block_sync();  // counters and length sums are complete; phase 2 of the last tile is over
+
+    // ---- offsets (owners) ---------------------------------------------------
+    uint32_t tot = 0;
+    uint64_t ws = 0;
+    if (owner) {
+#pragma unroll
+      for (int v = 0; v < NWB; ++v) tot += sh.cnt[v][t];
+      ws = sh.wsum[t];
+      sh.wsum[t] = 0;
+    }
+    const uint32_t inc_c = wave_incl_scan_u32(tot);
+    const uint64_t inc_w = wave_incl_scan_u40(ws);  // a tile's lengths add up to < 2^40
+    if (lane == kWave - 1) {
+      sh.part_c[w] = inc_c;
+      sh.part_w[w] = inc_w;
+    }
+    block_sync();
+    uint32_t ex_c = inc_c - tot;
+    uint64_t ex_w = inc_w - ws;
+#pragma unroll
+    for (int v = 0; v < NWB; ++v) {
+      ex_c += v < w ? sh.part_c[v] : 0u;
+      ex_w += v < w ? sh.part_w[v] : 0ull;
+    }
+    if (owner) {
+      uint32_t run = ex_c;
+#pragma unroll
+      for (int v = 0; v < NWB; ++v) {
+        const uint32_t c = sh.cnt[v][t];
+        sh.cnt[v][t] = (uint16_t)run;
+        run += c;
+      }
+      sh.base_c[t] = carry_c - ex_c;
+      sh.base_w[t] = carry_w - ex_w;
+      carry_c += tot;
+      carry_w += ws;
+    }
+    block_sync();  // tile offsets and bases are written
+
+    // ---- stage in digit order (digit, first digit, id); load the next tile ---
+    uint32_t rk[KB];
+#pragma unroll
+    for (int r = 0; r < KB; ++r) rk[r] = (rw[r] & 0x3fffu) + mycnt[opaque(digit_of(r))];
+    clear_wave_counters<MAXB>(mycnt);
+#pragma unroll
+    for (int r = 0; r < KB; ++r) {
+      const int idx = win0 + (int)(rw[r] >> 14);
+      const uint32_t d = (uint32_t)(idx >> kpb);
+      const uint32_t id = ((uint32_t)(idx & ((1 << kpb) - 1)) << kChunkBits) |
+                          (e[r] & ((1u << kChunkBits) - 1));
+      sh.stage[rk[r]] = ((uint64_t)((digit_of(r) << 10) | d) << 32) | id;
+    }
+    if (tb + TB < hi) load_final_compact(keys_in, tb + TB, (int)min((int64_t)TB, hi - tb - TB), e);
+    block_sync();  // the tile is staged
+
+    // ---- phase 2: tile length prefix, order, waits, class totals -----------
+    uint32_t exc[KB], rt[KB];  // exclusive length prefix within the round; round total
+    uint64_t chunk = 0;
+#pragma unroll
+    for (int r = 0; r < KB; ++r) {
+      const int j = wb + r * kWave + lane;
+      uint32_t ls = 0;
+      if (full || j < cv) {
+        const uint32_t hw = (uint32_t)(sh.stage[j] >> 32);
+        ls = len_of(hw >> 10, hw & 1023u);
+      }
+      const uint32_t inc = wave_incl_scan_u32(ls);  // below 2^32: 64 lengths < 2^26
+      exc[r] = inc - ls;
+      rt[r] = (uint32_t)__builtin_amdgcn_readlane((int)inc, kWave - 1);
+      chunk += rt[r];
+    }
+    if (lane == 0) sh.chunk[w] = chunk;
+    block_sync();
+    uint64_t run = 0;
+#pragma unroll
+    for (int v = 0; v < NWB; ++v) run += v < w ? sh.chunk[v] : 0ull;
+#pragma unroll
+    for (int r = 0; r < KB; ++r) {
+      const int j = wb + r * kWave + lane;
+      if (full || j < cv) {
+        const uint64_t x = sh.stage[j];
+        const uint32_t u2 = (uint32_t)(x >> 42);
+        const uint32_t c = class_of(u2, magic);  // class - pmin
+        const uint64_t wt = sh.base_w[u2] + run + exc[r];
+        const uint32_t pos = sh.base_c[u2] + (uint32_t)j;
+        if (pos < (uint64_t)a.n) {  // always true for consistent counts
+          a.order[pos] = (int32_t)(uint32_t)x;
+          a.wait[pos] = (int64_t)wt;
+        }
+        if (c != cur) {
+          if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
+          cur = c;
+          acc = {0, 0};
+        }
+        add128(acc, wt);
+      }
+      run += rt[r];
+    }
+  }
+  if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
+
+  block_sync();  // every lane's total is in
+  const int P = (int)pl->P;
+  for (int c = t; c < P; c += NTB) {
+    U128 v = {sh.clo[c], sh.chi[c]};
+    const int cls = c + (int)pl->pmin;
+    if (v.lo | v.hi) atomic_add128(a.totals + 2 * (1 + cls), a.totals + 2 * (1 + cls) + 1, v);
+  }
+  if (t == 0) {
+    U128 gsum = {0, 0};
+    for (int c = 0; c < P; ++c) {
+      U128 v = {sh.clo[c], sh.chi[c]};
+      add128(gsum, v);
+    }
+    if (gsum.lo | gsum.hi) atomic_add128(a.totals, a.totals + 1, gsum);
+  }
+}
+
+__global__ __launch_bounds__(NTB) void g_final_big(GArgs a) {
+  __shared__ union {
+    FinalBigShared big;
+    FinalCompactShared compact;
+  } sh;
+  const Plan* pl = a.plan;
+  if (!pl->ok) return;
+  if (pl->compact) {
+    final_compact(a, blockIdx.x, sh.compact);
+    return;
+  }
+  if (!use_big_final(pl)) return;
+  final_big(a, blockIdx.x, sh.big);
 }
 
 template <typename unused = void>
@@ -1587,7 +2063,7 @@ __global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
     FinalFastShared fast;
   } sh;
   const Plan* pl = a.plan;
-  if (!pl->ok || use_big_final(pl)) return;
+  if (!pl->ok || pl->compact || use_big_final(pl)) return;
   if (pl->packed && pl->W == 32 && pl->nscatter == 2 && pl->small) {
     if (pl->nbits[1] <= 8)
       final_fast<8>(a, blockIdx.x, sh.fast);

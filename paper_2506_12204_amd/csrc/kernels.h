@@ -52,6 +52,15 @@ constexpr int kHistRows = 1;
 static_assert(kFirstTiles % kHistRows == 0, "a block splits into whole-tile rows");
 constexpr int kMaxBlocks = 4096; // upper bound on workgroups of a pass
 
+// Compact two-pass layout. Between the passes an element is one u32: the
+// final digit above the low kChunkBits bits of the request id. The id's high
+// bits (its chunk, id >> kChunkBits) and the first digit are not stored: the
+// first pass leaves every first-digit bucket in id order, so an element's
+// bucket and chunk follow from its position and the sub-bucket starts
+// (bucket, chunk) counted by the histogram pass.
+constexpr int kChunkBits = 22;
+constexpr int kMaxChunks = 256;  // ids below 2^30
+
 // Decided on the device by the histogram pass once the ranges are known.
 struct Plan {
   uint32_t ok;        // 0 if a range error was found
@@ -66,6 +75,7 @@ struct Plan {
   uint32_t packed;    // 1: element = key << W | id in one u64
   uint32_t small;     // 1: every length < 2^26 (64-lane length sums fit 32 bits)
   uint32_t nscatter;  // number of scatter passes (>= 2)
+  uint32_t compact;   // 1: the compact two-pass layout (u32 elements) is used
   uint32_t shift[kMaxScatter];  // digit = (u2 >> shift) & (bins - 1), passes >= 1
   uint32_t nbits[kMaxScatter];
   uint32_t nbins[kMaxScatter];
@@ -88,6 +98,11 @@ struct GArgs {
   int32_t d0;           // width of the first (low-length) digit
   int32_t tiles;
   int32_t force_wide;   // 1: never pack the id into the key word
+  int32_t chunked;      // 1: the histogram pass counts the chunk sub-buckets, so the
+                        // compact layout may be chosen (host: kchunks <= kMaxChunks,
+                        // blocks of the first pass no longer than a chunk)
+  int32_t kchunks;      // K = ceil(n / 2^kChunkBits) id chunks
+  int32_t kpb;          // log2 of Kp, the power of two >= K that strides sub_start
   Split main;           // first histogram and first pass (tpb a multiple of kFirstTiles)
   Split fin;            // final histogram and final pass
   Split mid;            // the cooperative middle-pass kernel
@@ -101,6 +116,10 @@ struct GArgs {
   uint64_t* block_histw;// [blocks][kMaxBins] final-digit length sums, then offsets
   uint64_t* keys[2];
   uint32_t* ids[2];
+  uint32_t* chunk_part; // [kMaxChunks][kMaxBins] first-digit counts of the ids of
+                        // chunk boundary k's block that lie below the boundary
+  uint32_t* sub_start;  // [kMaxBins][Kp] start of sub-bucket (digit d, chunk k)
+                        // relative to bucket d's start; k >= K hold the bucket size
 };
 
 // Optional events recorded around one stage's kernel (null: not armed).

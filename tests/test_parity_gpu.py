@@ -80,10 +80,43 @@ def test_fuzz_sizes(n):
 
 
 @pytest.mark.parametrize("d0", ["8", "9", "10"])
-def test_first_digit_widths(d0, monkeypatch):
+@pytest.mark.parametrize("max_len", [2000, 32768])
+def test_first_digit_widths(d0, max_len, monkeypatch):
+    # max_len 2000 keeps the final digit under 256 values for every width
+    # (compact layout); 32768 with 8 or 9 bits gives 640 or 320 (u64 layout)
     monkeypatch.setenv("SEMSCHED_D0", d0)
-    p, l = fuzz_queue(200_000, seed=7, classes=5, max_len=32768, tie_frac=0.2)
-    check_queue(p, l, f"d0={d0}")
+    p, l = fuzz_queue(200_000, seed=7, classes=5, max_len=max_len, tie_frac=0.2)
+    check_queue(p, l, f"d0={d0},max_len={max_len}")
+
+
+# ---- compact two-pass layout: id chunks and the sub-bucket search -------------
+
+def test_compact_chunk_boundaries_inside_blocks():
+    # 10M requests: 3 id chunks of 2^22 ids; the first pass's blocks hold
+    # 49,152 ids, so both chunk boundaries fall inside a block
+    p, l = fuzz_queue(10_000_000, seed=31, classes=5, max_len=32768, tie_frac=0.2)
+    check_queue(p, l, "chunks-unaligned")
+
+
+def test_compact_window_in_global_memory():
+    # 99 % of the lengths are multiples of 1024 (first digit 0); the rest
+    # spread over the other 1023 first digits, so the last blocks span
+    # hundreds of buckets x 4 chunk slots: more sub-bucket starts than the
+    # LDS window holds, and the search reads them from global memory
+    rng = np.random.default_rng(32)
+    n = 12_000_000
+    p = rng.integers(0, 4, n).astype(np.uint8)
+    l = (rng.integers(1, 8, n) * 1024).astype(np.int32)
+    sprinkle = rng.random(n) < 0.01
+    l[sprinkle] = rng.integers(1, 8192, int(sprinkle.sum()))
+    check_queue(p, l, "window-global")
+
+
+@pytest.mark.parametrize("n", [100_003, 5_000_000])
+def test_u64_layout_when_compact_is_off(n, monkeypatch):
+    monkeypatch.setenv("SEMSCHED_NO_COMPACT", "1")
+    p, l = fuzz_queue(n, seed=33, classes=5, max_len=32768, tie_frac=0.2)
+    check_queue(p, l, "no-compact")
 
 
 # ---- degenerate and adversarial queues ----------------------------------------
