@@ -1900,9 +1900,16 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   for (int64_t tb = lo; tb < hi; tb += TB) {
     const int cv = (int)min((int64_t)TB, hi - tb);
     const bool full = cv == TB;
-    // the sub-buckets this tile's positions lie in
-    const int ja = find((uint32_t)tb, 0, wn - 1);
-    const int jb = find((uint32_t)(tb + cv - 1), ja, wn - 1);
+    // the sub-buckets this tile's positions lie in, then those of this wave's
+    // share (usually one: a wave covers 1024 positions); the bounds are
+    // uniform, so the searches below have uniform trip counts
+    const int ja = __builtin_amdgcn_readfirstlane(find((uint32_t)tb, 0, wn - 1));
+    const int jb = __builtin_amdgcn_readfirstlane(find((uint32_t)(tb + cv - 1), ja, wn - 1));
+    const uint32_t wlast = (uint32_t)(tb + cv - 1);
+    const int wja = __builtin_amdgcn_readfirstlane(
+        find(min((uint32_t)(tb + wb), wlast), ja, jb));
+    const int wjb = __builtin_amdgcn_readfirstlane(
+        find(min((uint32_t)(tb + wb + kWave * KB - 1), wlast), wja, jb));
 
     // ---- phase 1: decode, tile length sums per digit, ranks --------------
     // rw[r] = the item's rank (below 2^14) | its window index << 14 (below 2^18)
@@ -1915,7 +1922,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     for (int r = 0; r < KB; ++r) {
       const int j = wb + r * kWave + lane;
       const bool past = !full && j >= cv;
-      const uint32_t jj = (uint32_t)find((uint32_t)(tb + j), ja, jb);
+      const uint32_t jj = (uint32_t)find((uint32_t)(tb + j), wja, wjb);
       const uint32_t d = (uint32_t)((win0 + (int)jj) >> kpb);
       const uint32_t dg = digit_of(r);
       const uint32_t ls = past ? 0u : len_of(dg, d);
