@@ -23,7 +23,7 @@ constexpr size_t kHeaderBytes = 256;  // flags, counters, ranges, plan
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  size_t flags = 0, barrier = 8, plan = 64;
+  size_t flags = 0, barrier = 8, sink = 16, plan = 64;
   size_t hist_cnt = 0, hist_w = 0, block_hist = 0, block_histw = 0, block_ranges = 0;
   size_t keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0, chunk_part = 0, sub_start = 0;
   size_t total = kHeaderBytes;
@@ -213,6 +213,7 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
                block_items <= (1ll << kChunkBits)) ? 1 : 0;
   g.flags = reinterpret_cast<uint32_t*>(base + L.flags);
   g.barrier = reinterpret_cast<uint32_t*>(base + L.barrier);
+  g.sink = reinterpret_cast<uint64_t*>(base + L.sink);
   g.block_ranges = reinterpret_cast<uint32_t*>(base + L.block_ranges);
   g.plan = reinterpret_cast<Plan*>(base + L.plan);
   g.hist_cnt = reinterpret_cast<uint32_t*>(base + L.hist_cnt);

@@ -1826,6 +1826,9 @@ __device__ __forceinline__ void load_final_compact(const uint32_t* keys, int64_t
     e[r] = __builtin_amdgcn_raw_buffer_load_b32(rk, (lane + r * kWave) * 4, 0, 0);
 }
 
+// WIN_LDS: the block's sub-bucket starts fit the LDS window; else they are
+// read from global memory (separate kernels, see g_final_cglb).
+template <bool WIN_LDS>
 __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   const int t = threadIdx.x;
   const int lane = lane_id();
@@ -1874,14 +1877,14 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   const int d_hi = hi > lo ? bucket_of(sh.bstart, nd, (uint32_t)(hi - 1)) : 0;
   const int win0 = d_lo << kpb;
   const int wn = (d_hi - d_lo + 1) << kpb;
-  const bool in_lds = wn <= kWinCap;
-  if (in_lds) {
+  if (WIN_LDS != (wn <= kWinCap)) return;  // the other kernel's block
+  if (WIN_LDS) {
     for (int j = t; j < wn; j += NTB)
       sh.win[j] = sh.bstart[(win0 + j) >> kpb] + a.sub_start[win0 + j];
   }
   block_sync();
   auto sb = [&](int j) -> uint32_t {
-    return in_lds ? sh.win[j] : sh.bstart[(win0 + j) >> kpb] + a.sub_start[win0 + j];
+    return WIN_LDS ? sh.win[j] : sh.bstart[(win0 + j) >> kpb] + a.sub_start[win0 + j];
   };
   // last j in [jl, jh] with sb(j) <= pos, given sb(jl) <= pos: binary
   // lifting with steps from the largest power of two <= jh - jl down to 1
@@ -1895,11 +1898,21 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     return jl;
   };
 
-  uint32_t e[KB];
-  load_final_compact(keys_in, lo, (int)min((int64_t)TB, hi - lo), e);
-  for (int64_t tb = lo; tb < hi; tb += TB) {
-    const int cv = (int)min((int64_t)TB, hi - tb);
-    const bool full = cv == TB;
+  // The loop is rotated: the first phase of tile t + 1 runs at the end of
+  // iteration t, after the prefetch of its elements and the stores of tile
+  // t. The compiler then sees, in straight-line order, the loads, the (exactly
+  // counted, unconditional) stores and the first use of the loads, and waits
+  // only for the loads: the stores drain while the next tile is ranked.
+  uint32_t e[KB];   // elements of the tile being ranked
+  uint32_t rw[KB];  // per item: rank (below 2^14) | window index << 14 (below 2^18)
+  auto tile_items = [&](int64_t tb) { return (int)min((int64_t)TB, hi - tb); };
+  auto digit_of = [&](int r, int cv) {  // past the end: the last digit
+    return (cv < TB && wb + r * kWave + lane >= cv) ? (uint32_t)nb - 1
+                                                   : (e[r] >> kChunkBits) & (MAXB - 1);
+  };
+  // ---- phase 1: decode, tile length sums per digit, ranks --------------
+  auto phase1 = [&](int64_t tb) {
+    const int cv = tile_items(tb);
     // the sub-buckets this tile's positions lie in, then those of this wave's
     // share (usually one: a wave covers 1024 positions); the bounds are
     // uniform, so the searches below have uniform trip counts
@@ -1910,25 +1923,24 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
         find(min((uint32_t)(tb + wb), wlast), ja, jb));
     const int wjb = __builtin_amdgcn_readfirstlane(
         find(min((uint32_t)(tb + wb + kWave * KB - 1), wlast), wja, jb));
-
-    // ---- phase 1: decode, tile length sums per digit, ranks --------------
-    // rw[r] = the item's rank (below 2^14) | its window index << 14 (below 2^18)
-    auto digit_of = [&](int r) {  // past the end: the last digit
-      return (!full && wb + r * kWave + lane >= cv) ? (uint32_t)nb - 1
-                                                    : (e[r] >> kChunkBits) & (MAXB - 1);
-    };
-    uint32_t rw[KB];
 #pragma unroll
     for (int r = 0; r < KB; ++r) {
       const int j = wb + r * kWave + lane;
-      const bool past = !full && j >= cv;
+      const bool past = j >= cv;
       const uint32_t jj = (uint32_t)find((uint32_t)(tb + j), wja, wjb);
       const uint32_t d = (uint32_t)((win0 + (int)jj) >> kpb);
-      const uint32_t dg = digit_of(r);
+      const uint32_t dg = digit_of(r, cv);
       const uint32_t ls = past ? 0u : len_of(dg, d);
       atomicAdd((unsigned long long*)&sh.wsum[dg], (unsigned long long)ls);
       rw[r] = rank_round_c<8>(dg, mycnt) | (jj << 14);
     }
+  };
+
+  load_final_compact(keys_in, lo, tile_items(lo), e);
+  phase1(lo);
+  for (int64_t tb = lo; tb < hi; tb += TB) {
+    const int cv = tile_items(tb);
+    const bool full = cv == TB;
     block_sync();  // counters and length sums are complete; phase 2 of the last tile is over
 
     // ---- offsets (owners) ---------------------------------------------------
@@ -1949,10 +1961,9 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     block_sync();
     uint32_t ex_c = inc_c - tot;
     uint64_t ex_w = inc_w - ws;
-#pragma unroll
-    for (int v = 0; v < NWB; ++v) {
-      ex_c += v < w ? sh.part_c[v] : 0u;
-      ex_w += v < w ? sh.part_w[v] : 0ull;
+    for (int v = 0; v < w; ++v) {  // (w is uniform)
+      ex_c += sh.part_c[v];
+      ex_w += sh.part_w[v];
     }
     if (owner) {
       uint32_t run = ex_c;
@@ -1969,10 +1980,10 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     }
     block_sync();  // tile offsets and bases are written
 
-    // ---- stage in digit order (digit, first digit, id); load the next tile ---
+    // ---- stage (digit, first digit, id) in digit order; load the next tile ---
     uint32_t rk[KB];
 #pragma unroll
-    for (int r = 0; r < KB; ++r) rk[r] = (rw[r] & 0x3fffu) + mycnt[opaque(digit_of(r))];
+    for (int r = 0; r < KB; ++r) rk[r] = (rw[r] & 0x3fffu) + mycnt[opaque(digit_of(r, cv))];
     clear_wave_counters<MAXB>(mycnt);
 #pragma unroll
     for (int r = 0; r < KB; ++r) {
@@ -1980,9 +1991,10 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
       const uint32_t d = (uint32_t)(idx >> kpb);
       const uint32_t id = ((uint32_t)(idx & ((1 << kpb) - 1)) << kChunkBits) |
                           (e[r] & ((1u << kChunkBits) - 1));
-      sh.stage[rk[r]] = ((uint64_t)((digit_of(r) << 10) | d) << 32) | id;
+      sh.stage[rk[r]] = ((uint64_t)((digit_of(r, cv) << 10) | d) << 32) | id;
     }
-    if (tb + TB < hi) load_final_compact(keys_in, tb + TB, (int)min((int64_t)TB, hi - tb - TB), e);
+    const bool more = tb + TB < hi;
+    if (more) load_final_compact(keys_in, tb + TB, tile_items(tb + TB), e);
     block_sync();  // the tile is staged
 
     // ---- phase 2: tile length prefix, order, waits, class totals -----------
@@ -2004,21 +2016,22 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     if (lane == 0) sh.chunk[w] = chunk;
     block_sync();
     uint64_t run = 0;
-#pragma unroll
-    for (int v = 0; v < NWB; ++v) run += v < w ? sh.chunk[v] : 0ull;
+    for (int v = 0; v < w; ++v) run += sh.chunk[v];  // (w is uniform)
+    // Stores are unconditional: lanes without an item write to the sink.
 #pragma unroll
     for (int r = 0; r < KB; ++r) {
       const int j = wb + r * kWave + lane;
+      const uint64_t x = sh.stage[j];
+      const uint32_t u2 = (uint32_t)(x >> 42);
+      const uint64_t wt = sh.base_w[u2] + run + exc[r];
+      const uint32_t pos = sh.base_c[u2] + (uint32_t)j;
+      const bool item = (full || j < cv) && pos < (uint64_t)a.n;  // (pos < n for consistent counts)
+      int32_t* po = item ? a.order + pos : reinterpret_cast<int32_t*>(a.sink);
+      int64_t* pw = item ? a.wait + pos : reinterpret_cast<int64_t*>(a.sink + 1);
+      *po = (int32_t)(uint32_t)x;
+      *pw = (int64_t)wt;
       if (full || j < cv) {
-        const uint64_t x = sh.stage[j];
-        const uint32_t u2 = (uint32_t)(x >> 42);
         const uint32_t c = class_of(u2, magic);  // class - pmin
-        const uint64_t wt = sh.base_w[u2] + run + exc[r];
-        const uint32_t pos = sh.base_c[u2] + (uint32_t)j;
-        if (pos < (uint64_t)a.n) {  // always true for consistent counts
-          a.order[pos] = (int32_t)(uint32_t)x;
-          a.wait[pos] = (int64_t)wt;
-        }
         if (c != cur) {
           if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
           cur = c;
@@ -2028,6 +2041,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
       }
       run += rt[r];
     }
+    if (more) phase1(tb + TB);
   }
   if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
 
@@ -2056,11 +2070,23 @@ __global__ __launch_bounds__(NTB) void g_final_big(GArgs a) {
   const Plan* pl = a.plan;
   if (!pl->ok) return;
   if (pl->compact) {
-    final_compact(a, blockIdx.x, sh.compact);
+    final_compact<true>(a, blockIdx.x, sh.compact);
     return;
   }
   if (!use_big_final(pl)) return;
   final_big(a, blockIdx.x, sh.big);
+}
+
+// The compact final pass for the blocks whose sub-bucket starts do not fit
+// the LDS window (rare: a block must span hundreds of first-digit buckets);
+// they are searched in global memory. A kernel of its own, so that the common
+// kind's loop holds no global loads besides the element prefetch and the
+// compiler's wait counts stay exact there. Returns at once for other blocks.
+__global__ __launch_bounds__(NTB) void g_final_cglb(GArgs a) {
+  __shared__ FinalCompactShared sh;
+  const Plan* pl = a.plan;
+  if (!pl->ok || !pl->compact) return;
+  final_compact<false>(a, blockIdx.x, sh);
 }
 
 template <typename unused = void>
@@ -2159,6 +2185,7 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   mark(ev, 2, false, st);
   // exactly one of the two does the work; the plan on the device decides
   hipLaunchKernelGGL(g_final_big, gf, dim3(NTB), 0, st, a);
+  if (a.chunked) hipLaunchKernelGGL(g_final_cglb, gf, dim3(NTB), 0, st, a);
   hipLaunchKernelGGL(g_final<>, gf, dim3(NT), 0, st, a);
   mark(ev, 2, true, st);
   return hipGetLastError();

@@ -108,6 +108,8 @@ struct GArgs {
   Split mid;            // the cooperative middle-pass kernel
   uint32_t* flags;
   uint32_t* barrier;    // arrivals at the middle-pass grid barriers
+  uint64_t* sink;       // 16 bytes that absorb the stores of lanes without an item
+                        // (so that a pass's stores are unconditional)
   uint32_t* block_ranges;  // [blocks][4] pmin, pmax, lmin, lmax of every block
   Plan* plan;
   uint32_t* hist_cnt;   // [kMaxScatter][kMaxBins] digit totals of every pass
