@@ -671,14 +671,17 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
   // this block's items: tiles [g * tpb, (g + 1) * tpb), tpb a multiple of kFirstTiles
   const int64_t lo = (int64_t)g * a.main.tpb * T;
   const int64_t hi = min(a.n, lo + (int64_t)a.main.tpb * T);
+  // The loop is rotated: the ranking of tile t + 1 runs at the end of
+  // iteration t, after the prefetch of its inputs and the (unconditional,
+  // exactly counted) stores of tile t, so that the compiler's waits before
+  // the ranking cover the loads only and the stores drain meanwhile.
   uint32_t pv[R1], lv[R1];
-  load_first(a, lo, (int)min((int64_t)T1, hi - lo), pv, lv);
-  for (int64_t tb = lo; tb < hi; tb += T1) {
-    const int cv = (int)min((int64_t)T1, hi - tb);
-    // key = (p - pmin) << (wh + d0) | ((l >> d0) - hmin) << d0 | (l & M0), or
-    // for COMPACT u2 << d0 | (l & M0) with u2 = (p - pmin) * H + (l >> d0) - hmin;
-    // either way its low D0 bits are the digit
-    uint32_t key[R1], rk[R1];
+  uint32_t key[R1], rk[R1];
+  auto tile_items = [&](int64_t tb) { return (int)min((int64_t)T1, hi - tb); };
+  // key = (p - pmin) << (wh + d0) | ((l >> d0) - hmin) << d0 | (l & M0), or
+  // for COMPACT u2 << d0 | (l & M0) with u2 = (p - pmin) * H + (l >> d0) - hmin;
+  // either way its low D0 bits are the digit
+  auto rank_tile = [&](int cv) {
 #pragma unroll
     for (int r = 0; r < R1; ++r)
       key[r] = (COMPACT ? (__umul24(pv[r] - pmin, H) << D0) : ((pv[r] - pmin) << psh)) +
@@ -690,11 +693,17 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
       for (int r = 0; r < R1; ++r)
         if (wb + r * kWave + lane >= cv) key[r] |= M0;
     }
-
 #pragma unroll
     for (int r = 0; r < R1; ++r) rk[r] = rank_round_c<D0>(key[r] & M0, mycnt);
+  };
+
+  load_first(a, lo, tile_items(lo), pv, lv);
+  rank_tile(tile_items(lo));
+  for (int64_t tb = lo; tb < hi; tb += T1) {
+    const int cv = tile_items(tb);
+    const bool more = tb + T1 < hi;
     // the next tile's inputs load while this one is offset, staged and written
-    if (tb + T1 < hi) load_first(a, tb + T1, (int)min((int64_t)T1, hi - tb - T1), pv, lv);
+    if (more) load_first(a, tb + T1, tile_items(tb + T1), pv, lv);
     block_sync();  // every wave's counters are complete
 
     uint32_t cw[OWN][NW], tot[OWN];
@@ -713,8 +722,7 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
     if (lane == kWave - 1) sh.part[w] = incl;
     block_sync();
     uint32_t ex = incl - local;
-#pragma unroll
-    for (int v = 0; v < NW; ++v) ex += v < w ? sh.part[v] : 0u;
+    for (int v = 0; v < w; ++v) ex += sh.part[v];  // (w is uniform)
     if (owner) {
 #pragma unroll
       for (int i = 0; i < OWN; ++i) {
@@ -740,25 +748,26 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
       sh.stage[rk[r]] = ((uint64_t)key[r] << 32) | (uint32_t)(tb + wb + r * kWave + lane);
     block_sync();  // the tile is staged in digit order
 
+    // stores are unconditional: lanes without an item write to the sink
     const bool full = cv == T1;
 #pragma unroll
     for (int r = 0; r < R1; ++r) {
       const int j = wb + r * kWave + lane;
-      if (full || j < cv) {
-        const uint64_t e = sh.stage[j];
-        const uint32_t pos = sh.base[(uint32_t)(e >> 32) & M0] + (uint32_t)j;
-        if (pos < (uint64_t)a.n) {  // always true for consistent counts
-          if (COMPACT)  // u2 above the id's low bits
-            out32[pos] = (((uint32_t)(e >> 32) >> D0) << kChunkBits) |
-                         ((uint32_t)e & ((1u << kChunkBits) - 1));
-          else
-            out[pos] = e;
-        }
+      const uint64_t e = sh.stage[j];
+      const uint32_t pos = sh.base[(uint32_t)(e >> 32) & M0] + (uint32_t)j;
+      const bool item = (full || j < cv) && pos < (uint64_t)a.n;  // (pos < n for consistent counts)
+      if (COMPACT) {  // u2 above the id's low bits
+        uint32_t* po = item ? out32 + pos : reinterpret_cast<uint32_t*>(a.sink);
+        *po = (((uint32_t)(e >> 32) >> D0) << kChunkBits) | ((uint32_t)e & ((1u << kChunkBits) - 1));
+      } else {
+        uint64_t* po = item ? out + pos : a.sink;
+        *po = e;
       }
       // keep the scheduler from hoisting every round's loads at once, which
       // would hold ~5 registers per round live
       if (r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
     }
+    if (more) rank_tile(tile_items(tb + T1));
   }
 }
 
