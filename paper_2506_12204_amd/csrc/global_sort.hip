@@ -956,7 +956,7 @@ __device__ __forceinline__ uint32_t div_magic(uint32_t H) {
   return ((1u << 22) + H - 1) / H;
 }
 __device__ __forceinline__ uint32_t class_of(uint32_t u2, uint32_t magic) {
-  return (u2 * magic) >> 22;
+  return __umul24(u2, magic) >> 22;  // both factors below 2^24
 }
 
 // Final-digit histogram of one row for the compact layout: per final digit
@@ -1855,7 +1855,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   const uint32_t* keys_in = reinterpret_cast<const uint32_t*>(a.keys[0]);
   uint16_t* mycnt = sh.cnt[w];
   auto len_of = [&](uint32_t u2, uint32_t d) {
-    return ((u2 - class_of(u2, magic) * H + hmin) << d0) + d;
+    return ((u2 - __umul24(class_of(u2, magic), H) + hmin) << d0) + d;
   };
 
   clear_wave_counters<MAXB>(mycnt);
@@ -1876,8 +1876,18 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
       carry_w += a.block_histw[(size_t)g * kHistRows * kMaxBins + t];
     }
   }
-  uint32_t cur = ~0u;  // this lane's running wait total and its class - pmin
-  U128 acc = {0, 0};
+  // This lane's running wait total of its current class within the tile
+  // (class - pmin = cur; that class's digits end below cur_end). The sorted
+  // tile is class-major, so within a tile the classes a lane meets never
+  // decrease; the sum goes to the class's LDS total at every class change
+  // and at the end of the tile. A lane's 16 waits of a tile stay below 2^61,
+  // so the sum fits 64 bits.
+  uint32_t cur = ~0u, cur_end = 0;
+  uint64_t acc64 = 0;
+  auto flush_class = [&]() {
+    if (acc64) atomic_add128(sh.clo + cur, sh.chi + cur, U128{acc64, 0});
+    acc64 = 0;
+  };
 
   const int64_t lo = (int64_t)g * a.fin.tpb * T;
   const int64_t hi = min(a.n, lo + (int64_t)a.fin.tpb * T);
@@ -2026,7 +2036,9 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     block_sync();
     uint64_t run = 0;
     for (int v = 0; v < w; ++v) run += sh.chunk[v];  // (w is uniform)
-    // Stores are unconditional: lanes without an item write to the sink.
+    // Stores are unconditional, so that the compiler counts them exactly:
+    // lanes without an item (past the end of the last, partial tile) write to
+    // the sink.
 #pragma unroll
     for (int r = 0; r < KB; ++r) {
       const int j = wb + r * kWave + lane;
@@ -2034,26 +2046,27 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
       const uint32_t u2 = (uint32_t)(x >> 42);
       const uint64_t wt = sh.base_w[u2] + run + exc[r];
       const uint32_t pos = sh.base_c[u2] + (uint32_t)j;
-      const bool item = (full || j < cv) && pos < (uint64_t)a.n;  // (pos < n for consistent counts)
+      const bool in_tile = full || j < cv;
+      const bool item = in_tile && pos < (uint64_t)a.n;  // (pos < n for consistent counts)
       int32_t* po = item ? a.order + pos : reinterpret_cast<int32_t*>(a.sink);
       int64_t* pw = item ? a.wait + pos : reinterpret_cast<int64_t*>(a.sink + 1);
       *po = (int32_t)(uint32_t)x;
       *pw = (int64_t)wt;
-      if (full || j < cv) {
-        const uint32_t c = class_of(u2, magic);  // class - pmin
-        if (c != cur) {
-          if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
-          cur = c;
-          acc = {0, 0};
+      if (in_tile) {
+        if (u2 >= cur_end) {  // a new class for this lane
+          if (cur != ~0u) flush_class();
+          cur = class_of(u2, magic);  // class - pmin
+          cur_end = __umul24(cur + 1, H);
         }
-        add128(acc, wt);
+        acc64 += wt;
       }
       run += rt[r];
     }
+    if (cur != ~0u) flush_class();  // the next tile starts again at the first class
+    cur = ~0u;
+    cur_end = 0;
     if (more) phase1(tb + TB);
   }
-  if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
-
   block_sync();  // every lane's total is in
   const int P = (int)pl->P;
   for (int c = t; c < P; c += NTB) {
