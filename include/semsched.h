@@ -136,6 +136,45 @@ int sem_schedule_batched_async(const uint8_t *priority, const int32_t *length,
                                int64_t *wait_out, sem_i128 *totals_out,
                                void *workspace, size_t ws_bytes, void *stream);
 
+/*
+ * Insert m newly arrived requests into an existing schedule (blocking): the
+ * data-parallel form of Algorithm 1's HeapInsert under the asynchronous queue
+ * management of Section 3.3 (arrivals join the heap that already holds the
+ * earlier requests; draining it gives the schedule of all of them).
+ *   priority, length [n_old + m] DEVICE: requests 0 .. n_old-1 are the earlier
+ *             ones, n_old .. n_old+m-1 the arrivals (ids continue the arrival
+ *             index, so an exact (priority, length) tie goes to the earlier
+ *             request).
+ *   order_old, wait_old [n_old] DEVICE: the schedule of requests 0 .. n_old-1
+ *             as sem_schedule returned it (read only).
+ *   order_out, wait_out [n_old + m], totals_out [1 + 256] DEVICE: the schedule
+ *             of all n_old + m requests, identical to what sem_schedule returns
+ *             for them. The outputs must not overlap order_old / wait_old.
+ * Only the arrivals are sorted; every earlier entry is read and written once.
+ * Errors: SEM_EINVAL (n_old or m < 0, n_old + m > INT32_MAX, null pointers,
+ * overlapping outputs), SEM_ERANGE (an arrival's length < 0). If order_old /
+ * wait_old are not the schedule of the earlier requests the result is
+ * unspecified, but no memory outside the arguments is accessed.
+ */
+int sem_insert(const uint8_t *priority, const int32_t *length, int64_t n_old,
+               int64_t m, const int32_t *order_old, const int64_t *wait_old,
+               int32_t *order_out, int64_t *wait_out, sem_i128 *totals_out);
+
+/* Workspace size in bytes needed by sem_insert_async. */
+size_t sem_insert_workspace_bytes(int64_t n_old, int64_t m);
+
+/*
+ * Asynchronous sem_insert: same arguments plus a caller-owned DEVICE
+ * workspace of at least sem_insert_workspace_bytes(n_old, m) bytes (256-byte
+ * aligned) and the stream; allocates nothing, does not synchronise; an
+ * arrival's range error is returned by sem_check(workspace, stream).
+ */
+int sem_insert_async(const uint8_t *priority, const int32_t *length,
+                     int64_t n_old, int64_t m, const int32_t *order_old,
+                     const int64_t *wait_old, int32_t *order_out,
+                     int64_t *wait_out, sem_i128 *totals_out, void *workspace,
+                     size_t ws_bytes, void *stream);
+
 /* Stream used by the blocking calls (NULL = null stream). */
 int sem_set_stream(void *stream);
 

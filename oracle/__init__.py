@@ -20,6 +20,7 @@ import numpy as np
 from .semsched_oracle import (  # noqa: F401
     MAX_CLASSES,
     OracleRangeError,
+    insert_queue,
     schedule_batched,
     schedule_queue,
 )
@@ -108,3 +109,13 @@ def c_oracle_batched(p: np.ndarray, l: np.ndarray, offsets: np.ndarray,
         raise ValueError(f"oracle_schedule_batched failed: {rc}")
     return order, wait, _join128(lo[: s * (1 + num_classes)],
                                  hi[: s * (1 + num_classes)])
+
+
+def c_oracle_insert(p: np.ndarray, l: np.ndarray, n_old: int,
+                    order_old: np.ndarray, wait_old: np.ndarray):
+    """Large-size ``insert_queue`` through oracle.c: checks that the earlier
+    schedule is that of the first ``n_old`` requests, then schedules all."""
+    o, w, _ = c_oracle_queue(p[:n_old], l[:n_old])
+    if not (np.array_equal(o, order_old) and np.array_equal(w, wait_old)):
+        raise ValueError("order_old / wait_old are not the schedule of the first n_old requests")
+    return c_oracle_queue(p, l)

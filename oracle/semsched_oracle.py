@@ -33,6 +33,12 @@ Pins (see tests/test_oracle_*): brute force over every rank-respecting
 permutation for n <= 8, the adjacent-exchange invariant, closed forms,
 special cases that reduce to textbook policies, ``numpy.lexsort``, a
 hand-worked example and a 128-bit width case.
+
+``insert_queue`` is the incremental form (Section 3.3, asynchronous queue
+management; Algorithm 1's HeapInsert): new arrivals are inserted into the
+heap that already holds the earlier requests, and draining it gives the
+schedule of all of them. It is pinned to a literal binary min-heap
+(``heapq``) that receives the arrivals one by one (tests/test_oracle_insert).
 """
 
 from __future__ import annotations
@@ -82,6 +88,30 @@ def schedule_queue(p: Sequence[int], l: Sequence[int],
         totals[0] += wait[k]
         totals[1 + p[order[k]]] += wait[k]
     return order, wait, totals
+
+
+def insert_queue(p: Sequence[int], l: Sequence[int], n_old: int,
+                 order_old: Sequence[int], wait_old: Sequence[int],
+                 num_classes: int = MAX_CLASSES
+                 ) -> Tuple[List[int], List[int], List[int]]:
+    """Insert requests ``n_old .. len(p)-1`` into the schedule of the first
+    ``n_old`` requests; returns the schedule (order, wait, totals) of all.
+
+    ``order_old`` / ``wait_old`` must be the schedule of requests
+    ``0 .. n_old-1`` (checked: ValueError otherwise). The arrivals carry the
+    next arrival indices as ids, so an exact (rank, length) tie between an
+    earlier request and a new one goes to the earlier request. Inserting them
+    into the heap and draining it yields the ids ascending by the priority
+    tuple over all requests: the plain definition of ``schedule_queue``.
+    """
+    p = [int(x) for x in p]
+    l = [int(x) for x in l]
+    if not 0 <= n_old <= len(p):
+        raise ValueError("n_old must be in [0, n]")
+    want_o, want_w, _ = schedule_queue(p[:n_old], l[:n_old], num_classes)
+    if [int(x) for x in order_old] != want_o or [int(x) for x in wait_old] != want_w:
+        raise ValueError("order_old / wait_old are not the schedule of the first n_old requests")
+    return schedule_queue(p, l, num_classes)
 
 
 def schedule_batched(p: Sequence[int], l: Sequence[int],

@@ -43,6 +43,9 @@ SYMBOLS = (
     "sem_check",
     "sem_strerror",
     "sem_trace_stage",
+    "sem_insert",
+    "sem_insert_workspace_bytes",
+    "sem_insert_async",
 )
 STAGE_HIST, STAGE_FIRST, STAGE_FINAL = 0, 1, 2
 
@@ -76,10 +79,15 @@ def _load() -> ctypes.CDLL:
     lib.sem_check.argtypes = [vp, vp]
     lib.sem_trace_stage.argtypes = [ctypes.c_int, vp, vp]
     lib.sem_trace_stage.restype = ctypes.c_int
+    lib.sem_insert.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp]
+    lib.sem_insert_workspace_bytes.argtypes = [i64, i64]
+    lib.sem_insert_workspace_bytes.restype = sz
+    lib.sem_insert_async.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.sem_strerror.argtypes = [ctypes.c_int]
     lib.sem_strerror.restype = ctypes.c_char_p
     for name in ("sem_schedule", "sem_schedule_batched", "sem_schedule_async",
-                 "sem_schedule_batched_async", "sem_set_stream", "sem_check"):
+                 "sem_schedule_batched_async", "sem_set_stream", "sem_check", "sem_insert",
+                 "sem_insert_async"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -212,3 +220,52 @@ def schedule_batched(priority: torch.Tensor, length: torch.Tensor, offsets: torc
                                       num_classes, _ptr(order), _ptr(wait), _ptr(totals))
         _raise(rc, "sem_schedule_batched")
     return order, wait, totals_to_ints(totals[:s]) if s else []
+
+
+class Inserter:
+    """Reusable insertion of m arrivals into a schedule of n_old requests.
+
+    ``run`` enqueues sem_insert_async on the current stream into this
+    object's outputs (order, wait, totals of all n_old + m requests); ``check``
+    waits and raises on a device-detected error.
+    """
+
+    def __init__(self, n_old: int, m: int, device="cuda"):
+        self.n_old, self.m = int(n_old), int(m)
+        self.device = torch.device(device)
+        n = self.n_old + self.m
+        self.order = torch.empty(n, dtype=torch.int32, device=self.device)
+        self.wait = torch.empty(n, dtype=torch.int64, device=self.device)
+        self.totals = torch.empty((1 + MAX_CLASSES, 2), dtype=torch.int64, device=self.device)
+        self.ws_bytes = int(lib.sem_insert_workspace_bytes(self.n_old, self.m))
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+
+    def run(self, priority: torch.Tensor, length: torch.Tensor, order_old: torch.Tensor,
+            wait_old: torch.Tensor) -> None:
+        _check_inputs(priority, length)
+        if priority.numel() != self.n_old + self.m:
+            raise ValueError("priority/length must hold n_old + m requests")
+        if (order_old.dtype != torch.int32 or wait_old.dtype != torch.int64
+                or order_old.numel() != self.n_old or wait_old.numel() != self.n_old
+                or order_old.device != priority.device or wait_old.device != priority.device
+                or not (order_old.is_contiguous() and wait_old.is_contiguous())):
+            raise TypeError("order_old (int32) and wait_old (int64) must hold n_old entries "
+                            "on the inputs' GPU")
+        rc = lib.sem_insert_async(_ptr(priority), _ptr(length), self.n_old, self.m,
+                                  _ptr(order_old), _ptr(wait_old), _ptr(self.order),
+                                  _ptr(self.wait), _ptr(self.totals), _ptr(self.workspace),
+                                  self.ws_bytes, _stream_handle(self.device))
+        _raise(rc, "sem_insert_async")
+
+    def check(self) -> None:
+        _raise(lib.sem_check(_ptr(self.workspace), _stream_handle(self.device)), "sem_check")
+
+
+def insert(priority: torch.Tensor, length: torch.Tensor, n_old: int, order_old: torch.Tensor,
+           wait_old: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor, List[int]]:
+    """Insert requests n_old.. into the schedule (order_old, wait_old) of the
+    first n_old; returns the schedule of all (order, wait, totals[257] ints)."""
+    s = Inserter(n_old, priority.numel() - int(n_old), priority.device)
+    s.run(priority, length, order_old, wait_old)
+    s.check()
+    return s.order, s.wait, totals_to_ints(s.totals)

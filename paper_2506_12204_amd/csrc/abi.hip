@@ -241,6 +241,82 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
                                                                            : SEM_EDEVICE;
 }
 
+// Workspace of an insertion: the arrivals' own schedule (its workspace first,
+// so that the error flags sit at offset 0), then their order and waits, the
+// insertion points, class starts, length totals and scratch totals.
+struct InsLayout {
+  size_t order_m = 0, wait_m = 0, ins = 0, cs = 0, lsum = 0, totals_m = 0, total = 0;
+};
+
+InsLayout insert_layout(int64_t m) {
+  InsLayout L;
+  size_t off = align_up(layout_for(m).total);
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  L.order_m = take(4 * (size_t)m);
+  L.wait_m = take(8 * (size_t)m);
+  L.ins = take(4 * (size_t)m);
+  L.cs = take(4 * 2 * 257);
+  L.lsum = take(16);
+  L.totals_m = take(sizeof(sem_i128) * (1 + SEM_MAX_CLASSES));
+  L.total = off;
+  return L;
+}
+
+bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return abytes > 0 && bbytes > 0 && x < y + bbytes && y < x + abytes;
+}
+
+int check_insert_args(const uint8_t* p, const int32_t* l, int64_t n_old, int64_t m,
+                      const int32_t* order_old, const int64_t* wait_old, int32_t* order,
+                      int64_t* wait, sem_i128* totals) {
+  if (n_old < 0 || m < 0 || n_old + m > INT32_MAX || !totals) return SEM_EINVAL;
+  const int64_t n = n_old + m;
+  if (n > 0 && (!p || !l || !order || !wait)) return SEM_EINVAL;
+  if (n_old > 0 && (!order_old || !wait_old)) return SEM_EINVAL;
+  if (overlaps(order, 4 * (size_t)n, order_old, 4 * (size_t)n_old) ||
+      overlaps(wait, 8 * (size_t)n, wait_old, 8 * (size_t)n_old) ||
+      overlaps(order, 4 * (size_t)n, wait_old, 8 * (size_t)n_old) ||
+      overlaps(wait, 8 * (size_t)n, order_old, 4 * (size_t)n_old))
+    return SEM_EINVAL;
+  return SEM_OK;
+}
+
+int enqueue_insert(const uint8_t* p, const int32_t* l, int64_t n_old, int64_t m,
+                   const int32_t* order_old, const int64_t* wait_old, int32_t* order,
+                   int64_t* wait, sem_i128* totals, void* ws, hipStream_t st) {
+  char* base = static_cast<char*>(ws);
+  const InsLayout L = insert_layout(m);
+  InsArgs a = {};
+  a.priority = p;
+  a.length = l;
+  a.n_old = n_old;
+  a.m = m;
+  a.order_old = order_old;
+  a.wait_old = wait_old;
+  a.order_m = reinterpret_cast<int32_t*>(base + L.order_m);
+  a.wait_m = reinterpret_cast<int64_t*>(base + L.wait_m);
+  a.ins = reinterpret_cast<uint32_t*>(base + L.ins);
+  a.cs = reinterpret_cast<uint32_t*>(base + L.cs);
+  a.lsum = reinterpret_cast<uint64_t*>(base + L.lsum);
+  a.order = order;
+  a.wait = wait;
+  a.totals = reinterpret_cast<uint64_t*>(totals);
+  // the arrivals' own schedule (validates them; resets the error flags)
+  int rc = enqueue_queue(p + n_old, l + n_old, m, SEM_MAX_CLASSES,
+                         const_cast<int32_t*>(a.order_m), const_cast<int64_t*>(a.wait_m),
+                         reinterpret_cast<sem_i128*>(base + L.totals_m), ws, st);
+  if (rc != SEM_OK) return rc;
+  if (launch_fill_zero(reinterpret_cast<uint32_t*>(totals), 4 * (size_t)(1 + SEM_MAX_CLASSES),
+                       st) != hipSuccess)
+    return SEM_EDEVICE;
+  return launch_insert(a, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
+}
+
 int check_queue_args(const uint8_t* p, const int32_t* l, int64_t n, int32_t* order,
                      int64_t* wait, sem_i128* totals) {
   if (n < 0 || n > INT32_MAX) return SEM_EINVAL;
@@ -325,6 +401,42 @@ int sem_schedule_async(const uint8_t* priority, const int32_t* length, int64_t n
     return SEM_EINVAL;
   return enqueue_queue(priority, length, n, SEM_MAX_CLASSES, order_out, wait_out, totals_out,
                        workspace, static_cast<hipStream_t>(stream));
+}
+
+size_t sem_insert_workspace_bytes(int64_t n_old, int64_t m) {
+  if (n_old < 0 || m < 0) return 0;
+  return insert_layout(m).total;
+}
+
+int sem_insert_async(const uint8_t* priority, const int32_t* length, int64_t n_old, int64_t m,
+                     const int32_t* order_old, const int64_t* wait_old, int32_t* order_out,
+                     int64_t* wait_out, sem_i128* totals_out, void* workspace, size_t ws_bytes,
+                     void* stream) {
+  const int rc = check_insert_args(priority, length, n_old, m, order_old, wait_old, order_out,
+                                   wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  if (!workspace || ws_bytes < sem_insert_workspace_bytes(n_old, m) ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return SEM_EINVAL;
+  return enqueue_insert(priority, length, n_old, m, order_old, wait_old, order_out, wait_out,
+                        totals_out, workspace, static_cast<hipStream_t>(stream));
+}
+
+int sem_insert(const uint8_t* priority, const int32_t* length, int64_t n_old, int64_t m,
+               const int32_t* order_old, const int64_t* wait_old, int32_t* order_out,
+               int64_t* wait_out, sem_i128* totals_out) {
+  int rc = check_insert_args(priority, length, n_old, m, order_old, wait_old, order_out,
+                             wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  std::lock_guard<std::mutex> g(state().mu);
+  void* ws = nullptr;
+  rc = cached_workspace(sem_insert_workspace_bytes(n_old, m), &ws);
+  if (rc != SEM_OK) return rc;
+  const hipStream_t st = state().stream;
+  rc = enqueue_insert(priority, length, n_old, m, order_old, wait_old, order_out, wait_out,
+                      totals_out, ws, st);
+  if (rc != SEM_OK) return rc;
+  return finish(ws, st);
 }
 
 int sem_schedule(const uint8_t* priority, const int32_t* length, int64_t n, int32_t* order_out,

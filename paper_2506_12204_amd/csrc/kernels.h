@@ -139,4 +139,24 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
 // Zeroes `count` 32-bit words (graph-safe replacement for a memset).
 hipError_t launch_fill_zero(uint32_t* p, size_t count, hipStream_t st);
 
+// ---------------------------------------------------------------------------
+// Insertion of arrivals into an existing schedule (insert.hip).
+struct InsArgs {
+  const uint8_t* priority;  // [n_old + m], earlier requests first
+  const int32_t* length;
+  int64_t n_old, m;
+  const int32_t* order_old; // [n_old] the earlier schedule
+  const int64_t* wait_old;
+  const int32_t* order_m;   // [m] the arrivals' own schedule (ids local to them)
+  const int64_t* wait_m;
+  uint32_t* ins;            // [m] earlier entries not above each arrival
+  uint32_t* cs;             // [2][257] class starts of the earlier sequence, of the arrivals
+  uint64_t* lsum;           // [2] total lengths of the two sequences
+  int32_t* order;           // [n_old + m] the merged schedule
+  int64_t* wait;
+  uint64_t* totals;         // (lo, hi) pairs, 1 + 256, zeroed by the caller
+};
+
+hipError_t launch_insert(const InsArgs& a, hipStream_t st);
+
 }  // namespace semsched

@@ -91,3 +91,24 @@ def test_binding_type_checks(ss):
         ss.schedule(p, l)  # CPU tensors are refused: there is no CPU path
     with pytest.raises(TypeError):
         ss.schedule(p.to(torch.int32), l)
+
+
+def test_insert_argument_errors(ss):
+    L = ss.lib
+    fake = ctypes.c_void_p(1 << 40)  # never dereferenced: the call fails first
+    base = 1 << 40
+    o_old = ctypes.c_void_p(base)
+    w_old = ctypes.c_void_p(base + (1 << 20))
+    assert L.sem_insert(fake, fake, -1, 5, o_old, w_old, fake, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_insert(fake, fake, 5, -1, o_old, w_old, fake, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_insert(fake, fake, 1 << 30, 1 << 30, o_old, w_old, fake, fake,
+                        fake) == ss.SEM_EINVAL
+    assert L.sem_insert(fake, fake, 5, 5, ctypes.c_void_p(0), w_old, fake, fake,
+                        fake) == ss.SEM_EINVAL
+    # outputs overlapping the earlier schedule
+    assert L.sem_insert(fake, fake, 100, 5, o_old, w_old, ctypes.c_void_p(base + 8),
+                        ctypes.c_void_p(base + (1 << 30)), fake) == ss.SEM_EINVAL
+    assert L.sem_insert(fake, fake, 100, 5, o_old, w_old, ctypes.c_void_p(base + (1 << 30)),
+                        ctypes.c_void_p(base + (1 << 20) + 16), fake) == ss.SEM_EINVAL
+    assert ss.lib.sem_insert_workspace_bytes(-1, 3) == 0
+    assert ss.lib.sem_insert_workspace_bytes(1000, 100) >= 256 + 16 * 100
