@@ -6,7 +6,7 @@ One step = one complete schedule of a single queue of n = 2^26 requests
 order, every request's wait, and exact total and per-class waits, with the
 inputs already resident in HBM. Prints ONE JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+  python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--op insert]
 
 Besides whole-step throughput it reports, for the dominant kernel, the
 achieved bandwidth from its algorithmic bytes and its average duration
@@ -141,12 +141,119 @@ def cpu_baseline(p, l, order, wait, totals):
     return dt, same
 
 
+INSERT_ARRIVALS = 1 << 16
+# Algorithmic bytes of the insertion's merge pass: an earlier entry reads and
+# writes its order (4 B) and wait (8 B); an arrival reads its order, wait and
+# insertion point (4 + 8 + 4 B) and the earlier wait at that point (8 B), and
+# writes 12 B.
+MERGE_OLD_BYTES = 24
+MERGE_NEW_BYTES = 36
+
+
+def bench_insert(args) -> int:
+    """Insert the last 2^16 requests of the n = 2^26 workload into the
+    schedule of the others (sem_insert); one step = one insertion."""
+    import numpy as np
+    import torch
+    import paper_2506_12204_amd as ss
+    from workloads import generate
+
+    w = generate("c3")
+    n = w.n
+    m = INSERT_ARRIVALS
+    n_old = n - m
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    p = torch.from_numpy(w.priority).to(dev)
+    l = torch.from_numpy(w.length).to(dev)
+    old = ss.Scheduler(n_old, dev)
+    old.run(p[:n_old], l[:n_old])
+    old.check()
+    ins = ss.Inserter(n_old, m, dev)
+    print(f"[bench] insert {m} arrivals into a schedule of {n_old}; warmup {args.warmup}",
+          file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        ins.run(p, l, old.order, old.wait)
+    ins.check()
+    hip = HipEvents()
+    pairs = [(hip.create(), hip.create()) for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for k in range(args.steps):
+        ss.trace_stage(ss.STAGE_MERGE, *pairs[k])
+        ins.run(p, l, old.order, old.wait)
+    t1.record()
+    torch.cuda.synchronize()
+    ins.check()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    merge_ms = sum(hip.elapsed_ms(a, b) for a, b in pairs) / args.steps
+    for a, b in pairs:
+        hip.destroy(a)
+        hip.destroy(b)
+    print(f"[bench] {args.steps} inserts: {ms_step:.4f} ms each; merge pass {merge_ms:.4f} ms",
+          file=sys.stderr, flush=True)
+    merge_bytes = MERGE_OLD_BYTES * n_old + MERGE_NEW_BYTES * m
+    achieved = merge_bytes / (merge_ms * 1e-3) / 1e9
+    out = {
+        "metric": "merged schedule requests/s, 2^16 arrivals into a queue of 2^26 - 2^16, 1 GPU",
+        "value": n / (ms_step * 1e-3),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {
+            "workload": ("insert the last 2^16 requests of the single queue n=2^26 "
+                         "(5 urgency classes uniform, lengths uniform int32 in [1,32768], "
+                         "seed 2) into the schedule of the others"),
+            "n_old": n_old, "arrivals": m, "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "insertion merge pass", "achieved": achieved,
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": None, "bytes_per_launch": merge_bytes, "avg_launch_ms": merge_ms,
+        },
+    }
+    if not args.no_cpu_baseline:
+        from oracle import c_oracle_insert
+        o_old = old.order.cpu().numpy()
+        w_old = old.wait.cpu().numpy()
+        t = time.perf_counter()
+        want = c_oracle_insert(w.priority, w.length, n_old, o_old, w_old)
+        dt = time.perf_counter() - t
+        same = (want[0].tobytes() == ins.order.cpu().numpy().tobytes()
+                and want[1].tobytes() == ins.wait.cpu().numpy().tobytes()
+                and list(want[2]) == ss.totals_to_ints(ins.totals))
+        out["cpu_baseline"] = {
+            "value": n / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": (f"the full workload (n={n}): the plain C oracle checks the earlier "
+                       f"schedule and schedules all requests (merge sort + running sum), "
+                       f"single thread"),
+        }
+        out["parity"] = "bit-exact vs oracle" if same else "MISMATCH vs oracle"
+        if not same:
+            print(json.dumps(out))
+            return 1
+    print(json.dumps(out))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c3", choices=["c3", "c2"])
+    ap.add_argument("--op", default="schedule", choices=["schedule", "insert"],
+                    help="schedule (default): the whole queue; insert: 2^16 arrivals "
+                         "merged into the schedule of the rest")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle leg (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -158,6 +265,8 @@ def main() -> int:
         print(f"bench.py measures one GPU only: the schedule of one queue is not split "
               f"across GPUs in this build (asked for --gpus {args.gpus}).", file=sys.stderr)
         return 2
+    if args.op == "insert":
+        return bench_insert(args)
 
     import numpy as np
     import torch

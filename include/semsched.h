@@ -188,20 +188,23 @@ int sem_check(const void *workspace, void *stream);
 const char *sem_strerror(int code);
 
 /*
- * Measurement hook. Arms a one-shot pair of events for one stage of the
- * multi-pass single-queue path (n > SEM_SEGMENT_CAP): the next asynchronous
- * or blocking single-queue call on that path records `before` and `after`
- * (hipEvent_t passed as void *, created by the caller) on its stream right
- * before and right after that stage's kernel, then disarms the stage.
- *   stage: SEM_STAGE_HIST  (range check + first-digit histogram),
- *          SEM_STAGE_FIRST (first scatter pass),
- *          SEM_STAGE_FINAL (final scatter pass: order, waits, totals).
+ * Measurement hook. Arms a one-shot pair of events for one stage: the next
+ * call that runs that stage records `before` and `after` (hipEvent_t passed
+ * as void *, created by the caller) on its stream right before and right
+ * after the stage's kernels, then disarms the stage.
+ *   stage: SEM_STAGE_HIST  (multi-pass single-queue path, n > SEM_SEGMENT_CAP:
+ *                           range check + first-digit histogram),
+ *          SEM_STAGE_FIRST (same path: first scatter pass),
+ *          SEM_STAGE_FINAL (same path: final scatter pass: order, waits, totals),
+ *          SEM_STAGE_MERGE (sem_insert / sem_insert_async: the merge pass that
+ *                           moves the earlier entries and places the arrivals).
  * Passing NULL events disarms the stage. Returns SEM_EINVAL for an unknown
  * stage. The events are owned by the caller and must outlive the call.
  */
 #define SEM_STAGE_HIST 0
 #define SEM_STAGE_FIRST 1
 #define SEM_STAGE_FINAL 2
+#define SEM_STAGE_MERGE 3
 int sem_trace_stage(int stage, void *before, void *after);
 
 #ifdef __cplusplus

@@ -47,7 +47,7 @@ SYMBOLS = (
     "sem_insert_workspace_bytes",
     "sem_insert_async",
 )
-STAGE_HIST, STAGE_FIRST, STAGE_FINAL = 0, 1, 2
+STAGE_HIST, STAGE_FIRST, STAGE_FINAL, STAGE_MERGE = 0, 1, 2, 3
 
 
 class SemschedError(RuntimeError):

@@ -230,7 +230,7 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   bool armed = false;
   {
     std::lock_guard<std::mutex> guard(trace_mu());
-    for (int k = 0; k < 3; ++k) {
+    for (int k = SEM_STAGE_HIST; k <= SEM_STAGE_FINAL; ++k) {
       ev.before[k] = trace_slots().before[k];
       ev.after[k] = trace_slots().after[k];
       armed = armed || ev.before[k] || ev.after[k];
@@ -314,7 +314,14 @@ int enqueue_insert(const uint8_t* p, const int32_t* l, int64_t n_old, int64_t m,
   if (launch_fill_zero(reinterpret_cast<uint32_t*>(totals), 4 * (size_t)(1 + SEM_MAX_CLASSES),
                        st) != hipSuccess)
     return SEM_EDEVICE;
-  return launch_insert(a, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
+  hipEvent_t before = nullptr, after = nullptr;
+  {
+    std::lock_guard<std::mutex> guard(trace_mu());
+    before = trace_slots().before[SEM_STAGE_MERGE];
+    after = trace_slots().after[SEM_STAGE_MERGE];
+    trace_slots().before[SEM_STAGE_MERGE] = trace_slots().after[SEM_STAGE_MERGE] = nullptr;
+  }
+  return launch_insert(a, st, before, after) == hipSuccess ? SEM_OK : SEM_EDEVICE;
 }
 
 int check_queue_args(const uint8_t* p, const int32_t* l, int64_t n, int32_t* order,
@@ -367,7 +374,7 @@ const char* sem_strerror(int code) {
 }
 
 int sem_trace_stage(int stage, void* before, void* after) {
-  if (stage < SEM_STAGE_HIST || stage > SEM_STAGE_FINAL) return SEM_EINVAL;
+  if (stage < SEM_STAGE_HIST || stage > SEM_STAGE_MERGE) return SEM_EINVAL;
   std::lock_guard<std::mutex> guard(trace_mu());
   trace_slots().before[stage] = static_cast<hipEvent_t>(before);
   trace_slots().after[stage] = static_cast<hipEvent_t>(after);

@@ -22,6 +22,8 @@
 //
 // Only the arrivals are sorted; every earlier entry is read and written
 // once (4 + 8 bytes each way).
+#include <algorithm>
+
 #include "block_common.h"
 #include "kernels.h"
 
@@ -33,6 +35,7 @@ constexpr int IT = 256;          // threads of the insertion kernels
 constexpr int IK = 16;           // rounds: a block merges IT * IK entries
 constexpr int ITILE = IT * IK;
 constexpr int kClassSlots = 257;  // class starts per sequence (classes 0..255 and the end)
+constexpr int64_t kMergeBlocks = 2048;  // workgroups of the merge pass (tiles are walked)
 
 // key of an earlier entry / of an arrival, both as (priority, length)
 struct KeyPL {
@@ -103,77 +106,146 @@ __device__ __forceinline__ int last_le(const uint32_t* table, int lo, int hi, ui
   return lo;
 }
 
+constexpr int kSliceCap = 256;  // arrivals inside one tile held in LDS (more: searched in global)
+constexpr int kCountCap = 32;   // up to this many, every lane counts them all (no search)
+
 struct MergeShared {
   uint32_t cs[kClassSlots];   // class starts of this block's sequence
   uint64_t clo[256], chi[256];
-  int64_t cbase[2];           // c(k) at the first and last entry of the tile
+  int64_t cbase[2];           // c(k) at the first and at the last entry of the tile
+  int32_t ncb, cls0;          // class starts inside the tile; the class at its first entry
+  uint32_t cb[kClassSlots];   // those class starts
+  uint32_t slice[kSliceCap];  // insertion points of the arrivals landing inside the tile
+  uint64_t pnew[kSliceCap + 1];  // length prefix of the arrivals at c(k0) .. c(k1 - 1)
 };
 
-// Blocks 0 .. old_blocks-1 move earlier entries; the rest place arrivals.
-__global__ __launch_bounds__(IT) void i_merge(InsArgs a, int64_t old_blocks) {
+// Number of the first `count` entries of a non-decreasing LDS table that are
+// <= x: with few entries every lane counts them all (broadcast reads, a
+// uniform trip count), else a binary search.
+__device__ __forceinline__ int count_le(const uint32_t* table, int count, uint32_t x) {
+  if (count <= kCountCap) {
+    int c = 0;
+    for (int i = 0; i < count; ++i) c += table[i] <= x ? 1 : 0;
+    return c;
+  }
+  int lo = 0, hi = count;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (table[mid] <= x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+// Tiles 0 .. old_tiles-1 move earlier entries; the rest place arrivals. A
+// block walks tiles blockIdx.x, blockIdx.x + gridDim.x, ... and adds its
+// class totals to the global ones once, at the end (a grid of a few
+// thousand blocks keeps those 128-bit atomics on a dozen words rare).
+// Within a tile a lane handles entries k0 + r * IT + lane (r = 0 .. IK-1):
+// consecutive lanes read and write consecutive entries, and a lane's
+// entries increase, so its class only moves forward.
+__global__ __launch_bounds__(IT) void i_merge(InsArgs a, int64_t old_tiles, int64_t tiles) {
   __shared__ MergeShared sh;
   const int t = threadIdx.x;
-  const bool arrivals = (int64_t)blockIdx.x >= old_blocks;
-  const int64_t blk = arrivals ? (int64_t)blockIdx.x - old_blocks : (int64_t)blockIdx.x;
-  const int64_t cnt = arrivals ? a.m : a.n_old;  // entries of this block's sequence
-  const int64_t k0 = blk * ITILE;
-  const int64_t k1 = min(cnt, k0 + ITILE);
-  for (int c = t; c < kClassSlots; c += IT) sh.cs[c] = a.cs[(arrivals ? kClassSlots : 0) + c];
   for (int c = t; c < 256; c += IT) sh.clo[c] = sh.chi[c] = 0;
-  if (!arrivals && t < 2 && k1 > k0) {
-    // c(k) = number of arrivals with ins[j] <= k, at k0 and at k1 - 1
-    const uint32_t x = (uint32_t)(t == 0 ? k0 : k1 - 1);
-    int64_t lo = 0, hi = a.m;
-    while (lo < hi) {
-      const int64_t mid = (lo + hi) >> 1;
-      if (a.ins[mid] <= x) lo = mid + 1; else hi = mid;
-    }
-    sh.cbase[t] = lo;
-  }
-  block_sync();
-
   const uint64_t lnew = a.lsum[1], lold = a.lsum[0];
-  int cur = -1;          // this lane's current class and its 128-bit wait sum
-  U128 acc = {0, 0};
-  const int64_t clo_k = arrivals ? 0 : sh.cbase[0];
-  const int64_t chi_k = arrivals ? 0 : sh.cbase[1];
-  int cls = 0;
-  for (int r = 0; r < IK; ++r) {
-    const int64_t k = k0 + (int64_t)r * IT + t;
-    if (k >= k1) break;
-    int64_t q;
-    int32_t id;
-    uint64_t wt;
-    if (!arrivals) {
-      // arrivals ahead of earlier entry k: c(k) in [clo_k, chi_k]
-      int64_t lo = clo_k, hi = chi_k;
+  for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const bool arrivals = tile >= old_tiles;
+    const int64_t cnt = arrivals ? a.m : a.n_old;  // entries of this tile's sequence
+    const int64_t k0 = (arrivals ? tile - old_tiles : tile) * ITILE;
+    const int64_t k1 = min(cnt, k0 + ITILE);       // (k0 < k1 for every tile)
+    block_sync();  // the previous tile's tables are no longer read
+    for (int c = t; c < kClassSlots; c += IT) sh.cs[c] = a.cs[(arrivals ? kClassSlots : 0) + c];
+    if (!arrivals && t < 2) {
+      // c(k) = number of arrivals with ins[j] <= k, at k0 and at k1 - 1
+      const uint32_t x = (uint32_t)(t == 0 ? k0 : k1 - 1);
+      int64_t lo = 0, hi = a.m;
       while (lo < hi) {
         const int64_t mid = (lo + hi) >> 1;
-        if (a.ins[mid] <= (uint32_t)k) lo = mid + 1; else hi = mid;
+        if (a.ins[mid] <= x) lo = mid + 1; else hi = mid;
       }
-      const int64_t c = lo;
-      q = k + c;
-      id = a.order_old[k];
-      wt = (uint64_t)a.wait_old[k] + (c < a.m ? (uint64_t)a.wait_m[c] : lnew);
-    } else {
-      const int64_t at = min((int64_t)a.ins[k], a.n_old);
-      q = at + k;
-      id = (int32_t)(a.n_old + a.order_m[k]);
-      wt = (uint64_t)a.wait_m[k] + (at < a.n_old ? (uint64_t)a.wait_old[at] : lold);
+      sh.cbase[t] = lo;
     }
-    if (q < a.n_old + a.m) {  // always true for a consistent earlier schedule
-      a.order[q] = id;
-      a.wait[q] = (int64_t)wt;
+    block_sync();
+    if (t == 0) {
+      // the class of the tile's first entry and the class starts inside the tile
+      const int c0 = last_le(sh.cs, 0, 256, (uint32_t)k0);
+      int nc = 0;
+      for (int c = c0 + 1; c < 256 && sh.cs[c] < (uint32_t)k1; ++c) sh.cb[nc++] = sh.cs[c];
+      sh.cls0 = c0;
+      sh.ncb = nc;
     }
-    cls = last_le(sh.cs, cls, 256, (uint32_t)k);  // classes never decrease along a lane
-    if (cls != cur) {
-      if (cur >= 0 && (acc.lo | acc.hi)) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
-      cur = cls;
-      acc = {0, 0};
+    const int64_t c0 = arrivals ? 0 : sh.cbase[0];
+    const int64_t ns = arrivals ? 0 : sh.cbase[1] - c0;  // arrivals landing inside the tile
+    const bool in_lds = ns <= kSliceCap;
+    if (!arrivals && in_lds) {
+      for (int64_t i = t; i < ns; i += IT) sh.slice[i] = a.ins[c0 + i];
+      for (int64_t i = t; i <= ns; i += IT)
+        sh.pnew[i] = c0 + i < a.m ? (uint64_t)a.wait_m[c0 + i] : lnew;
     }
-    add128(acc, wt);
+    block_sync();
+    const int ncb = sh.ncb, cls0 = sh.cls0;
+
+    // every round's inputs first, so that their loads overlap
+    int32_t id[IK];
+    uint64_t w0[IK];
+    uint32_t at[IK];
+#pragma unroll
+    for (int r = 0; r < IK; ++r) {
+      const int64_t k = min(k0 + (int64_t)r * IT + t, k1 - 1);
+      if (!arrivals) {
+        id[r] = a.order_old[k];
+        w0[r] = (uint64_t)a.wait_old[k];
+      } else {
+        id[r] = (int32_t)(a.n_old + a.order_m[k]);
+        w0[r] = (uint64_t)a.wait_m[k];
+        at[r] = (uint32_t)min((int64_t)a.ins[k], a.n_old);
+      }
+    }
+    int cur = -1;  // this lane's current class and its 128-bit wait sum
+    U128 acc = {0, 0};
+#pragma unroll
+    for (int r = 0; r < IK; ++r) {
+      const int64_t k = k0 + (int64_t)r * IT + t;
+      int64_t q;
+      uint64_t wt;
+      if (!arrivals) {
+        // arrivals ahead of earlier entry k: c0 + those of the tile's slice at or before k
+        int64_t c;
+        uint64_t pn;
+        if (in_lds) {
+          c = count_le(sh.slice, (int)ns, (uint32_t)k);
+          pn = sh.pnew[c];
+        } else {
+          int64_t lo = 0, hi = ns;
+          while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (a.ins[c0 + mid] <= (uint32_t)k) lo = mid + 1; else hi = mid;
+          }
+          c = lo;
+          pn = c0 + c < a.m ? (uint64_t)a.wait_m[c0 + c] : lnew;
+        }
+        q = k + c0 + c;
+        wt = w0[r] + pn;
+      } else {
+        q = (int64_t)at[r] + k;
+        wt = w0[r] + (at[r] < a.n_old ? (uint64_t)a.wait_old[at[r]] : lold);
+      }
+      if (k < k1 && q < a.n_old + a.m) {  // (q < n always, for a consistent earlier schedule)
+        a.order[q] = id[r];
+        a.wait[q] = (int64_t)wt;
+      }
+      if (k < k1) {
+        const int cls = cls0 + count_le(sh.cb, ncb, (uint32_t)k);
+        if (cls != cur) {
+          if (cur >= 0 && (acc.lo | acc.hi)) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
+          cur = cls;
+          acc = {0, 0};
+        }
+        add128(acc, wt);
+      }
+    }
+    if (cur >= 0 && (acc.lo | acc.hi)) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
   }
-  if (cur >= 0 && (acc.lo | acc.hi)) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
   block_sync();
   for (int c = t; c < 256; c += IT) {
     U128 v = {sh.clo[c], sh.chi[c]};
@@ -188,14 +260,16 @@ __global__ __launch_bounds__(IT) void i_merge(InsArgs a, int64_t old_blocks) {
 
 }  // namespace
 
-hipError_t launch_insert(const InsArgs& a, hipStream_t st) {
+hipError_t launch_insert(const InsArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after) {
   const int64_t searches = a.m + 2 * kClassSlots + 1;
   hipLaunchKernelGGL(i_search, dim3((unsigned)((searches + IT - 1) / IT)), dim3(IT), 0, st, a);
-  const int64_t old_blocks = (a.n_old + ITILE - 1) / ITILE;
-  const int64_t new_blocks = (a.m + ITILE - 1) / ITILE;
-  if (old_blocks + new_blocks > 0)
-    hipLaunchKernelGGL(i_merge, dim3((unsigned)(old_blocks + new_blocks)), dim3(IT), 0, st, a,
-                       old_blocks);
+  const int64_t old_tiles = (a.n_old + ITILE - 1) / ITILE;
+  const int64_t tiles = old_tiles + (a.m + ITILE - 1) / ITILE;
+  const int64_t grid = std::min<int64_t>(tiles, kMergeBlocks);
+  if (before) (void)hipEventRecord(before, st);
+  if (grid > 0)
+    hipLaunchKernelGGL(i_merge, dim3((unsigned)grid), dim3(IT), 0, st, a, old_tiles, tiles);
+  if (after) (void)hipEventRecord(after, st);
   return hipGetLastError();
 }
 

@@ -125,9 +125,10 @@ struct GArgs {
 };
 
 // Optional events recorded around one stage's kernel (null: not armed).
+constexpr int kStages = 4;  // hist, first, final (long queues); merge (insertion)
 struct StageEvents {
-  hipEvent_t before[3];
-  hipEvent_t after[3];
+  hipEvent_t before[kStages];
+  hipEvent_t after[kStages];
 };
 
 // Work splits of the passes for n requests (device-dependent occupancy).
@@ -157,6 +158,7 @@ struct InsArgs {
   uint64_t* totals;         // (lo, hi) pairs, 1 + 256, zeroed by the caller
 };
 
-hipError_t launch_insert(const InsArgs& a, hipStream_t st);
+// `before` / `after` (may be null) are recorded around the merge kernel.
+hipError_t launch_insert(const InsArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after);
 
 }  // namespace semsched
