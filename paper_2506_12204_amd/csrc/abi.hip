@@ -245,10 +245,11 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
 // so that the error flags sit at offset 0), then their order and waits, the
 // insertion points, class starts, length totals and scratch totals.
 struct InsLayout {
-  size_t order_m = 0, wait_m = 0, ins = 0, cs = 0, lsum = 0, totals_m = 0, total = 0;
+  size_t order_m = 0, wait_m = 0, ins = 0, desc = 0, cs = 0, lsum = 0, sink = 0, totals_m = 0,
+         total = 0;
 };
 
-InsLayout insert_layout(int64_t m) {
+InsLayout insert_layout(int64_t n_old, int64_t m) {
   InsLayout L;
   size_t off = align_up(layout_for(m).total);
   auto take = [&](size_t bytes) {
@@ -256,11 +257,14 @@ InsLayout insert_layout(int64_t m) {
     off = align_up(off + bytes);
     return at;
   };
-  L.order_m = take(4 * (size_t)m);
-  L.wait_m = take(8 * (size_t)m);
-  L.ins = take(4 * (size_t)m);
-  L.cs = take(4 * 2 * 257);
+  const size_t m1 = (size_t)std::max<int64_t>(m, 1);  // the merge pass reads entry 0 even if m = 0
+  L.order_m = take(4 * m1);
+  L.wait_m = take(8 * m1);
+  L.ins = take(4 * m1);
+  L.desc = take(8 * (size_t)(insert_units(n_old) + 1));
+  L.cs = take(4 * 257);
   L.lsum = take(16);
+  L.sink = take(16);
   L.totals_m = take(sizeof(sem_i128) * (1 + SEM_MAX_CLASSES));
   L.total = off;
   return L;
@@ -290,7 +294,7 @@ int enqueue_insert(const uint8_t* p, const int32_t* l, int64_t n_old, int64_t m,
                    const int32_t* order_old, const int64_t* wait_old, int32_t* order,
                    int64_t* wait, sem_i128* totals, void* ws, hipStream_t st) {
   char* base = static_cast<char*>(ws);
-  const InsLayout L = insert_layout(m);
+  const InsLayout L = insert_layout(n_old, m);
   InsArgs a = {};
   a.priority = p;
   a.length = l;
@@ -301,8 +305,10 @@ int enqueue_insert(const uint8_t* p, const int32_t* l, int64_t n_old, int64_t m,
   a.order_m = reinterpret_cast<int32_t*>(base + L.order_m);
   a.wait_m = reinterpret_cast<int64_t*>(base + L.wait_m);
   a.ins = reinterpret_cast<uint32_t*>(base + L.ins);
+  a.desc = reinterpret_cast<uint64_t*>(base + L.desc);
   a.cs = reinterpret_cast<uint32_t*>(base + L.cs);
   a.lsum = reinterpret_cast<uint64_t*>(base + L.lsum);
+  a.sink = reinterpret_cast<uint64_t*>(base + L.sink);
   a.order = order;
   a.wait = wait;
   a.totals = reinterpret_cast<uint64_t*>(totals);
@@ -412,7 +418,7 @@ int sem_schedule_async(const uint8_t* priority, const int32_t* length, int64_t n
 
 size_t sem_insert_workspace_bytes(int64_t n_old, int64_t m) {
   if (n_old < 0 || m < 0) return 0;
-  return insert_layout(m).total;
+  return insert_layout(n_old, m).total;
 }
 
 int sem_insert_async(const uint8_t* priority, const int32_t* length, int64_t n_old, int64_t m,

@@ -142,6 +142,8 @@ hipError_t launch_fill_zero(uint32_t* p, size_t count, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // Insertion of arrivals into an existing schedule (insert.hip).
+constexpr int kInsUnit = 1024;  // earlier entries per unit of the merge pass (one wave)
+
 struct InsArgs {
   const uint8_t* priority;  // [n_old + m], earlier requests first
   const int32_t* length;
@@ -150,14 +152,20 @@ struct InsArgs {
   const int64_t* wait_old;
   const int32_t* order_m;   // [m] the arrivals' own schedule (ids local to them)
   const int64_t* wait_m;
-  uint32_t* ins;            // [m] earlier entries not above each arrival
-  uint32_t* cs;             // [2][257] class starts of the earlier sequence, of the arrivals
+  uint32_t* ins;            // [max(m, 1)] earlier entries not above each arrival
+  uint64_t* desc;           // [units + 1] per unit of kInsUnit earlier entries: arrivals
+                            // placed before its first entry (bits 0..31), the class of
+                            // its first (32..39) and of its last entry (40..47)
+  uint32_t* cs;             // [257] class starts of the earlier sequence
   uint64_t* lsum;           // [2] total lengths of the two sequences
+  uint64_t* sink;           // 16 bytes that absorb the stores of lanes without an entry
   int32_t* order;           // [n_old + m] the merged schedule
   int64_t* wait;
   uint64_t* totals;         // (lo, hi) pairs, 1 + 256, zeroed by the caller
 };
 
+// Units of kInsUnit earlier entries (desc holds one more entry).
+int64_t insert_units(int64_t n_old);
 // `before` / `after` (may be null) are recorded around the merge kernel.
 hipError_t launch_insert(const InsArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after);
 
