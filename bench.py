@@ -47,6 +47,8 @@ else:
 PATH_BYTES = 17  # the whole schedule's own inputs + outputs per request
 COUNTERS = os.path.join(ROOT, "profiles", "final_pass_c3_counters.md")
 FINAL_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "global_sort.hip")
+MERGE_COUNTERS = os.path.join(ROOT, "profiles", "insert_merge_c3_counters.md")
+MERGE_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "insert.hip")
 
 
 class HipEvents:
@@ -88,22 +90,22 @@ def code_sha(path: str) -> str:
     return hashlib.sha256("\n".join(lines).encode()).hexdigest()
 
 
-def counter_traffic(n: int):
-    """HBM bytes per launch of the final pass from committed rocprofv3 counters.
+def counter_traffic(n: int, counters: str = COUNTERS, source: str = FINAL_SOURCE):
+    """HBM bytes per launch of a kernel from committed rocprofv3 counters.
 
     The summary file carries `key: value` lines (n, code_sha256,
     hbm_bytes_per_launch). Null when the counters were taken on a different
     version of the kernel source (comments aside) or another request count.
     """
-    if not os.path.exists(COUNTERS):
+    if not os.path.exists(counters):
         return None
     kv = {}
-    with open(COUNTERS) as f:
+    with open(counters) as f:
         for line in f:
             if ":" in line and not line.startswith(("|", "#", " ")):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip().strip("`")
-    if kv.get("code_sha256") != code_sha(FINAL_SOURCE) or kv.get("n") != str(n):
+    if kv.get("code_sha256") != code_sha(source) or kv.get("n") != str(n):
         return None
     return float(kv["hbm_bytes_per_launch"])
 
@@ -218,7 +220,8 @@ def bench_insert(args) -> int:
         "roofline": {
             "bound": "hbm", "kernel": "insertion merge pass", "achieved": achieved,
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": None, "bytes_per_launch": merge_bytes, "avg_launch_ms": merge_ms,
+            "traffic": counter_traffic(n, MERGE_COUNTERS, MERGE_SOURCE),
+            "bytes_per_launch": merge_bytes, "avg_launch_ms": merge_ms,
         },
     }
     if not args.no_cpu_baseline:
