@@ -19,9 +19,15 @@ import numpy as np
 
 from .semsched_oracle import (  # noqa: F401
     MAX_CLASSES,
+    POLICIES,
+    POLICY_FCFS,
+    POLICY_HPJF,
+    POLICY_SEMANTIC,
+    POLICY_SJF,
     OracleRangeError,
     insert_queue,
     schedule_batched,
+    schedule_policy,
     schedule_queue,
 )
 
@@ -58,6 +64,8 @@ def _load():
     lib.oracle_schedule_batched.argtypes = [vp, vp, vp, i64, ctypes.c_int32,
                                             vp, vp, vp, vp]
     lib.oracle_schedule_batched.restype = ctypes.c_int
+    lib.oracle_schedule_policy.argtypes = [ctypes.c_int, vp, vp, i64, vp, vp, vp, vp]
+    lib.oracle_schedule_policy.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -85,6 +93,24 @@ def c_oracle_queue(p: np.ndarray, l: np.ndarray):
         raise OracleRangeError("length < 0 or priority out of range")
     if rc != ORACLE_OK:
         raise ValueError(f"oracle_schedule failed: {rc}")
+    return order, wait, _join128(lo, hi)
+
+
+def c_oracle_policy(p: np.ndarray, l: np.ndarray, policy: int):
+    """Single queue under a comparison policy through oracle.c."""
+    p = np.ascontiguousarray(p, dtype=np.uint8)
+    l = np.ascontiguousarray(l, dtype=np.int32)
+    n = p.shape[0]
+    order = np.empty(n, np.int32)
+    wait = np.empty(n, np.int64)
+    lo = np.zeros(257, np.uint64)
+    hi = np.zeros(257, np.uint64)
+    rc = _load().oracle_schedule_policy(int(policy), _ptr(p), _ptr(l), n, _ptr(order),
+                                        _ptr(wait), _ptr(lo), _ptr(hi))
+    if rc == ORACLE_ERANGE:
+        raise OracleRangeError("length < 0 or priority out of range")
+    if rc != ORACLE_OK:
+        raise ValueError(f"oracle_schedule_policy failed: {rc}")
     return order, wait, _join128(lo, hi)
 
 

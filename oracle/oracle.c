@@ -20,6 +20,10 @@
  * The sort is a top-down merge sort on (p, l, id) records. Because the
  * comparison covers the id, the order is total and any correct sort gives
  * the same permutation.
+ *
+ * oracle_schedule_policy orders by the comparison policies of Section 4
+ * instead (arrival order; length then id; rank then id); waits and
+ * per-class totals are defined the same way for every policy.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -36,20 +40,30 @@ typedef struct {
   uint8_t pri;
 } rec_t;
 
-static int rec_less(const rec_t *a, const rec_t *b) {
-  if (a->pri != b->pri) return a->pri < b->pri;
-  if (a->len != b->len) return a->len < b->len;
+/* Comparison policies of the experiments (Section 4): which fields key the
+ * order before the id. 0 = (rank, length), 1 = none (arrival order),
+ * 2 = (length), 3 = (rank). */
+#define ORACLE_POLICY_SEMANTIC 0
+#define ORACLE_POLICY_FCFS 1
+#define ORACLE_POLICY_SJF 2
+#define ORACLE_POLICY_HPJF 3
+
+static int rec_less(const rec_t *a, const rec_t *b, int policy) {
+  const int use_pri = policy == ORACLE_POLICY_SEMANTIC || policy == ORACLE_POLICY_HPJF;
+  const int use_len = policy == ORACLE_POLICY_SEMANTIC || policy == ORACLE_POLICY_SJF;
+  if (use_pri && a->pri != b->pri) return a->pri < b->pri;
+  if (use_len && a->len != b->len) return a->len < b->len;
   return a->id < b->id;
 }
 
-static void merge_sort(rec_t *a, rec_t *tmp, int64_t n) {
+static void merge_sort(rec_t *a, rec_t *tmp, int64_t n, int policy) {
   if (n < 2) return;
   int64_t h = n / 2;
-  merge_sort(a, tmp, h);
-  merge_sort(a + h, tmp, n - h);
+  merge_sort(a, tmp, h, policy);
+  merge_sort(a + h, tmp, n - h, policy);
   int64_t i = 0, j = h, k = 0;
   while (i < h && j < n) {
-    if (rec_less(&a[j], &a[i]))
+    if (rec_less(&a[j], &a[i], policy))
       tmp[k++] = a[j++];
     else
       tmp[k++] = a[i++];
@@ -61,8 +75,8 @@ static void merge_sort(rec_t *a, rec_t *tmp, int64_t n) {
 
 /* One queue. totals_lo/hi have 1 + num_classes entries. */
 static int schedule_one(const uint8_t *pri, const int32_t *len, int64_t n,
-                        int32_t num_classes, int32_t *order, int64_t *wait,
-                        uint64_t *totals_lo, uint64_t *totals_hi,
+                        int32_t num_classes, int policy, int32_t *order,
+                        int64_t *wait, uint64_t *totals_lo, uint64_t *totals_hi,
                         rec_t *recs, rec_t *tmp) {
   for (int64_t i = 0; i < n; ++i) {
     if (len[i] < 0 || (int32_t)pri[i] >= num_classes) return ORACLE_ERANGE;
@@ -70,7 +84,7 @@ static int schedule_one(const uint8_t *pri, const int32_t *len, int64_t n,
     recs[i].len = len[i];
     recs[i].id = (int32_t)i;
   }
-  merge_sort(recs, tmp, n);
+  merge_sort(recs, tmp, n, policy);
 
   unsigned __int128 tot[257];
   for (int c = 0; c <= num_classes; ++c) tot[c] = 0;
@@ -89,10 +103,11 @@ static int schedule_one(const uint8_t *pri, const int32_t *len, int64_t n,
   return ORACLE_OK;
 }
 
-int oracle_schedule(const uint8_t *pri, const int32_t *len, int64_t n,
-                    int32_t *order, int64_t *wait, uint64_t *totals_lo,
-                    uint64_t *totals_hi) {
+int oracle_schedule_policy(int policy, const uint8_t *pri, const int32_t *len,
+                           int64_t n, int32_t *order, int64_t *wait,
+                           uint64_t *totals_lo, uint64_t *totals_hi) {
   if (n < 0 || n > INT32_MAX) return ORACLE_EINVAL;
+  if (policy < ORACLE_POLICY_SEMANTIC || policy > ORACLE_POLICY_HPJF) return ORACLE_EINVAL;
   rec_t *recs = (rec_t *)malloc((size_t)(n ? n : 1) * sizeof(rec_t));
   rec_t *tmp = (rec_t *)malloc((size_t)(n ? n : 1) * sizeof(rec_t));
   if (!recs || !tmp) {
@@ -100,11 +115,18 @@ int oracle_schedule(const uint8_t *pri, const int32_t *len, int64_t n,
     free(tmp);
     return ORACLE_ENOMEM;
   }
-  int rc = schedule_one(pri, len, n, 256, order, wait, totals_lo, totals_hi,
-                        recs, tmp);
+  int rc = schedule_one(pri, len, n, 256, policy, order, wait, totals_lo,
+                        totals_hi, recs, tmp);
   free(recs);
   free(tmp);
   return rc;
+}
+
+int oracle_schedule(const uint8_t *pri, const int32_t *len, int64_t n,
+                    int32_t *order, int64_t *wait, uint64_t *totals_lo,
+                    uint64_t *totals_hi) {
+  return oracle_schedule_policy(ORACLE_POLICY_SEMANTIC, pri, len, n, order,
+                                wait, totals_lo, totals_hi);
 }
 
 int oracle_schedule_batched(const uint8_t *pri, const int32_t *len,
@@ -131,7 +153,8 @@ int oracle_schedule_batched(const uint8_t *pri, const int32_t *len,
   const int64_t stride = 1 + num_classes;
   for (int64_t s = 0; s < num_segments && rc == ORACLE_OK; ++s) {
     int64_t a = offsets[s], m = offsets[s + 1] - offsets[s];
-    rc = schedule_one(pri + a, len + a, m, num_classes, order + a, wait + a,
+    rc = schedule_one(pri + a, len + a, m, num_classes, ORACLE_POLICY_SEMANTIC,
+                      order + a, wait + a,
                       totals_lo + s * stride, totals_hi + s * stride, recs, tmp);
   }
   free(recs);

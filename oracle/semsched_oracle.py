@@ -34,6 +34,11 @@ permutation for n <= 8, the adjacent-exchange invariant, closed forms,
 special cases that reduce to textbook policies, ``numpy.lexsort``, a
 hand-worked example and a 128-bit width case.
 
+``schedule_policy`` orders the same queue by the comparison policies of the
+paper's experiments (Section 4, request spikes: first-come-first-served,
+shortest job first, highest-priority job first) as well as by the semantic
+tuple; waits and per-class totals are defined as above for every policy.
+
 ``insert_queue`` is the incremental form (Section 3.3, asynchronous queue
 management; Algorithm 1's HeapInsert): new arrivals are inserted into the
 heap that already holds the earlier requests, and draining it gives the
@@ -83,6 +88,53 @@ def schedule_queue(p: Sequence[int], l: Sequence[int],
     for k in range(1, n):
         wait[k] = wait[k - 1] + l[order[k - 1]]
     # Step 3: Eq. 1's numerator, overall and per urgency class.
+    totals = [0] * (1 + num_classes)
+    for k in range(n):
+        totals[0] += wait[k]
+        totals[1 + p[order[k]]] += wait[k]
+    return order, wait, totals
+
+
+POLICY_SEMANTIC = 0  # (rank, length, id): the priority tuple of Algorithm 1
+POLICY_FCFS = 1      # (id): arrival order
+POLICY_SJF = 2       # (length, id): shortest predicted job first, rank ignored
+POLICY_HPJF = 3      # (rank, id): most urgent first, length ignored
+POLICIES = (POLICY_SEMANTIC, POLICY_FCFS, POLICY_SJF, POLICY_HPJF)
+
+
+def policy_key(policy: int, p: Sequence[int], l: Sequence[int]):
+    """Sort key of request i under ``policy``; the id closes every key, so
+    the order is total (ties go to the earlier arrival)."""
+    if policy == POLICY_SEMANTIC:
+        return lambda i: (p[i], l[i], i)
+    if policy == POLICY_FCFS:
+        return lambda i: (i,)
+    if policy == POLICY_SJF:
+        return lambda i: (l[i], i)
+    if policy == POLICY_HPJF:
+        return lambda i: (p[i], i)
+    raise ValueError(f"unknown policy {policy}")
+
+
+def schedule_policy(p: Sequence[int], l: Sequence[int], policy: int,
+                    num_classes: int = MAX_CLASSES
+                    ) -> Tuple[List[int], List[int], List[int]]:
+    """Schedule one queue under ``policy``; returns (order, wait, totals).
+
+    The comparison policies of Section 4: FCFS serves in arrival order, SJF
+    by predicted length alone, HPJF by urgency rank alone (each with the
+    arrival id as the last key). Waits are the exclusive prefix of the
+    lengths in the chosen order and ``totals[1 + c]`` adds the waits of the
+    requests whose rank is c, whatever the policy.
+    """
+    p = [int(x) for x in p]
+    l = [int(x) for x in l]
+    _check(p, l, num_classes)
+    n = len(p)
+    order = sorted(range(n), key=policy_key(policy, p, l))
+    wait = [0] * n
+    for k in range(1, n):
+        wait[k] = wait[k - 1] + l[order[k - 1]]
     totals = [0] * (1 + num_classes)
     for k in range(n):
         totals[0] += wait[k]
