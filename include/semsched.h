@@ -175,6 +175,46 @@ int sem_insert_async(const uint8_t *priority, const int32_t *length,
                      int64_t *wait_out, sem_i128 *totals_out, void *workspace,
                      size_t ws_bytes, void *stream);
 
+/*
+ * Comparison policies: the baselines of the request-spike experiments of
+ * Section 4 (first-come-first-served, shortest job first, highest-priority
+ * job first), plus the semantic order itself. Each keys the order by some
+ * fields of the request and closes the key with the id:
+ *   SEM_POLICY_SEMANTIC  (priority, length, id): the same as sem_schedule
+ *   SEM_POLICY_FCFS      (id): arrival order
+ *   SEM_POLICY_SJF       (length, id): the rank is ignored
+ *   SEM_POLICY_HPJF      (priority, id): the length is ignored
+ */
+#define SEM_POLICY_SEMANTIC 0
+#define SEM_POLICY_FCFS 1
+#define SEM_POLICY_SJF 2
+#define SEM_POLICY_HPJF 3
+
+/*
+ * Schedule one queue under `policy` (blocking). Arguments, layouts and
+ * outputs as for sem_schedule: wait_out[k] is the exclusive prefix of the
+ * lengths in the policy's order, totals_out[1 + c] the sum of the waits of
+ * the requests whose priority is c (whatever the policy orders by).
+ * Errors: SEM_EINVAL for an unknown policy, else as sem_schedule (a negative
+ * length is SEM_ERANGE under every policy, FCFS included).
+ */
+int sem_schedule_policy(int policy, const uint8_t *priority, const int32_t *length,
+                        int64_t n, int32_t *order_out, int64_t *wait_out,
+                        sem_i128 *totals_out);
+
+/* Workspace size in bytes of sem_schedule_policy_async (0 for an unknown
+ * policy or n < 0). */
+size_t sem_policy_workspace_bytes(int policy, int64_t n);
+
+/* Asynchronous sem_schedule_policy: a caller-owned DEVICE workspace of at
+ * least sem_policy_workspace_bytes(policy, n) bytes (256-byte aligned) and
+ * the stream; allocates nothing, does not synchronise; range errors are
+ * returned by sem_check(workspace, stream). */
+int sem_schedule_policy_async(int policy, const uint8_t *priority, const int32_t *length,
+                              int64_t n, int32_t *order_out, int64_t *wait_out,
+                              sem_i128 *totals_out, void *workspace, size_t ws_bytes,
+                              void *stream);
+
 /* Stream used by the blocking calls (NULL = null stream). */
 int sem_set_stream(void *stream);
 
@@ -197,7 +237,10 @@ const char *sem_strerror(int code);
  *          SEM_STAGE_FIRST (same path: first scatter pass),
  *          SEM_STAGE_FINAL (same path: final scatter pass: order, waits, totals),
  *          SEM_STAGE_MERGE (sem_insert / sem_insert_async: the merge pass that
- *                           moves the earlier entries and places the arrivals).
+ *                           moves the earlier entries and places the arrivals),
+ *          SEM_STAGE_POLICY (sem_schedule_policy*: for FCFS and HPJF the pass
+ *                           that writes order and waits, for SJF the pass
+ *                           that sums the waits per class).
  * Passing NULL events disarms the stage. Returns SEM_EINVAL for an unknown
  * stage. The events are owned by the caller and must outlive the call.
  */
@@ -205,6 +248,7 @@ const char *sem_strerror(int code);
 #define SEM_STAGE_FIRST 1
 #define SEM_STAGE_FINAL 2
 #define SEM_STAGE_MERGE 3
+#define SEM_STAGE_POLICY 4
 int sem_trace_stage(int stage, void *before, void *after);
 
 #ifdef __cplusplus

@@ -46,8 +46,13 @@ SYMBOLS = (
     "sem_insert",
     "sem_insert_workspace_bytes",
     "sem_insert_async",
+    "sem_schedule_policy",
+    "sem_policy_workspace_bytes",
+    "sem_schedule_policy_async",
 )
-STAGE_HIST, STAGE_FIRST, STAGE_FINAL, STAGE_MERGE = 0, 1, 2, 3
+STAGE_HIST, STAGE_FIRST, STAGE_FINAL, STAGE_MERGE, STAGE_POLICY = 0, 1, 2, 3, 4
+# comparison policies (Section 4): the key fields before the id
+POLICY_SEMANTIC, POLICY_FCFS, POLICY_SJF, POLICY_HPJF = 0, 1, 2, 3
 
 
 class SemschedError(RuntimeError):
@@ -83,11 +88,15 @@ def _load() -> ctypes.CDLL:
     lib.sem_insert_workspace_bytes.argtypes = [i64, i64]
     lib.sem_insert_workspace_bytes.restype = sz
     lib.sem_insert_async.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.sem_schedule_policy.argtypes = [ctypes.c_int, vp, vp, i64, vp, vp, vp]
+    lib.sem_policy_workspace_bytes.argtypes = [ctypes.c_int, i64]
+    lib.sem_policy_workspace_bytes.restype = sz
+    lib.sem_schedule_policy_async.argtypes = [ctypes.c_int, vp, vp, i64, vp, vp, vp, vp, sz, vp]
     lib.sem_strerror.argtypes = [ctypes.c_int]
     lib.sem_strerror.restype = ctypes.c_char_p
     for name in ("sem_schedule", "sem_schedule_batched", "sem_schedule_async",
                  "sem_schedule_batched_async", "sem_set_stream", "sem_check", "sem_insert",
-                 "sem_insert_async"):
+                 "sem_insert_async", "sem_schedule_policy", "sem_schedule_policy_async"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -267,5 +276,46 @@ def insert(priority: torch.Tensor, length: torch.Tensor, n_old: int, order_old: 
     first n_old; returns the schedule of all (order, wait, totals[257] ints)."""
     s = Inserter(n_old, priority.numel() - int(n_old), priority.device)
     s.run(priority, length, order_old, wait_old)
+    s.check()
+    return s.order, s.wait, totals_to_ints(s.totals)
+
+
+class PolicyScheduler:
+    """Reusable single-queue schedule of size n under a comparison policy
+    (POLICY_FCFS, POLICY_SJF, POLICY_HPJF or POLICY_SEMANTIC); ``run`` enqueues
+    sem_schedule_policy_async on the current stream, ``check`` waits and raises
+    on a device-detected error."""
+
+    def __init__(self, n: int, policy: int, device="cuda"):
+        self.n, self.policy = int(n), int(policy)
+        self.device = torch.device(device)
+        self.order = torch.empty(self.n, dtype=torch.int32, device=self.device)
+        self.wait = torch.empty(self.n, dtype=torch.int64, device=self.device)
+        self.totals = torch.empty((1 + MAX_CLASSES, 2), dtype=torch.int64, device=self.device)
+        self.ws_bytes = int(lib.sem_policy_workspace_bytes(self.policy, self.n))
+        if self.ws_bytes == 0:
+            raise SemschedError(SEM_EINVAL, "sem_policy_workspace_bytes")
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+
+    def run(self, priority: torch.Tensor, length: torch.Tensor) -> None:
+        _check_inputs(priority, length)
+        if priority.numel() != self.n:
+            raise ValueError("size differs from the PolicyScheduler's n")
+        rc = lib.sem_schedule_policy_async(self.policy, _ptr(priority), _ptr(length), self.n,
+                                           _ptr(self.order), _ptr(self.wait), _ptr(self.totals),
+                                           _ptr(self.workspace), self.ws_bytes,
+                                           _stream_handle(self.device))
+        _raise(rc, "sem_schedule_policy_async")
+
+    def check(self) -> None:
+        _raise(lib.sem_check(_ptr(self.workspace), _stream_handle(self.device)), "sem_check")
+
+
+def schedule_policy(priority: torch.Tensor, length: torch.Tensor, policy: int
+                    ) -> Tuple[torch.Tensor, torch.Tensor, List[int]]:
+    """Schedule one queue under ``policy``; returns (order, wait, totals[257] ints)."""
+    _check_inputs(priority, length)
+    s = PolicyScheduler(priority.numel(), policy, priority.device)
+    s.run(priority, length)
     s.check()
     return s.order, s.wait, totals_to_ints(s.totals)

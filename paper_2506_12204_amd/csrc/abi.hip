@@ -330,6 +330,105 @@ int enqueue_insert(const uint8_t* p, const int32_t* l, int64_t n_old, int64_t m,
   return launch_insert(a, st, before, after) == hipSuccess ? SEM_OK : SEM_EDEVICE;
 }
 
+// Workspace of a comparison-policy schedule. SJF runs the queue kernels on a
+// zeroed rank array first, so its layout starts with the queue workspace
+// (error flags at offset 0) and that array; FCFS and HPJF use the header's
+// flag word. Then the policy kernels' tables.
+struct PolLayout {
+  size_t zeros = 0, pmax = 0, rsum = 0, tab_cnt = 0, tab_len = 0, ctot_cnt = 0, ctot_len = 0,
+         part = 0, sink = 0, total = 0;
+};
+
+PolLayout policy_layout(int policy, int64_t n) {
+  PolLayout L;
+  size_t off = policy == SEM_POLICY_SJF ? align_up(layout_for(n).total) : kHeaderBytes;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  const size_t ranges = (size_t)std::max<int64_t>(policy_ranges(n), 1);
+  const size_t blocks = (size_t)std::max<int64_t>(policy_blocks(n), 1);
+  if (policy == SEM_POLICY_SJF) L.zeros = take(((size_t)n + 3) / 4 * 4);
+  L.pmax = take(4);
+  if (policy == SEM_POLICY_FCFS) L.rsum = take(8 * ranges);
+  if (policy == SEM_POLICY_HPJF) {
+    L.tab_cnt = take(4 * ranges * SEM_MAX_CLASSES);
+    L.tab_len = take(8 * ranges * SEM_MAX_CLASSES);
+    L.ctot_cnt = take(4 * SEM_MAX_CLASSES);
+    L.ctot_len = take(8 * SEM_MAX_CLASSES);
+  }
+  L.part = take(16 * blocks * SEM_MAX_CLASSES);
+  L.sink = take(16);
+  L.total = off;
+  return L;
+}
+
+bool known_policy(int policy) {
+  return policy == SEM_POLICY_SEMANTIC || policy == SEM_POLICY_FCFS ||
+         policy == SEM_POLICY_SJF || policy == SEM_POLICY_HPJF;
+}
+
+int check_queue_args(const uint8_t* p, const int32_t* l, int64_t n, int32_t* order,
+                     int64_t* wait, sem_i128* totals);
+
+int enqueue_policy(int policy, const uint8_t* p, const int32_t* l, int64_t n, int32_t* order,
+                   int64_t* wait, sem_i128* totals, void* ws, hipStream_t st) {
+  if (policy == SEM_POLICY_SEMANTIC)
+    return enqueue_queue(p, l, n, SEM_MAX_CLASSES, order, wait, totals, ws, st);
+  char* base = static_cast<char*>(ws);
+  uint32_t* flags = reinterpret_cast<uint32_t*>(base);
+  uint32_t* tot32 = reinterpret_cast<uint32_t*>(totals);
+  const size_t tot_words = 4 * (size_t)(1 + SEM_MAX_CLASSES);
+  if (n == 0) {
+    if (launch_fill_zero(flags, 1, st) != hipSuccess ||
+        launch_fill_zero(tot32, tot_words, st) != hipSuccess)
+      return SEM_EDEVICE;
+    return SEM_OK;
+  }
+  const PolLayout L = policy_layout(policy, n);
+  PolArgs a = {};
+  a.priority = p;
+  a.length = l;
+  a.n = n;
+  a.order = order;
+  a.wait = wait;
+  a.totals = reinterpret_cast<uint64_t*>(totals);
+  a.flags = flags;
+  a.pmax = reinterpret_cast<uint32_t*>(base + L.pmax);
+  a.rsum = reinterpret_cast<uint64_t*>(base + L.rsum);
+  a.tab_cnt = reinterpret_cast<uint32_t*>(base + L.tab_cnt);
+  a.tab_len = reinterpret_cast<uint64_t*>(base + L.tab_len);
+  a.ctot_cnt = reinterpret_cast<uint32_t*>(base + L.ctot_cnt);
+  a.ctot_len = reinterpret_cast<uint64_t*>(base + L.ctot_len);
+  a.part = reinterpret_cast<uint64_t*>(base + L.part);
+  a.sink = reinterpret_cast<uint64_t*>(base + L.sink);
+  if (policy == SEM_POLICY_SJF) {
+    // the order by (length, id): the queue kernels with every rank read as 0
+    uint32_t* zeros = reinterpret_cast<uint32_t*>(base + L.zeros);
+    if (launch_fill_zero(zeros, ((size_t)n + 3) / 4, st) != hipSuccess) return SEM_EDEVICE;
+    const int rc = enqueue_queue(reinterpret_cast<const uint8_t*>(zeros), l, n, SEM_MAX_CLASSES,
+                                 order, wait, totals, ws, st);
+    if (rc != SEM_OK) return rc;
+  } else if (launch_fill_zero(flags, 1, st) != hipSuccess) {
+    return SEM_EDEVICE;
+  }
+  if (launch_fill_zero(a.pmax, 1, st) != hipSuccess ||
+      launch_fill_zero(tot32, tot_words, st) != hipSuccess)
+    return SEM_EDEVICE;
+  hipEvent_t before = nullptr, after = nullptr;
+  {
+    std::lock_guard<std::mutex> guard(trace_mu());
+    before = trace_slots().before[SEM_STAGE_POLICY];
+    after = trace_slots().after[SEM_STAGE_POLICY];
+    trace_slots().before[SEM_STAGE_POLICY] = trace_slots().after[SEM_STAGE_POLICY] = nullptr;
+  }
+  hipError_t e = policy == SEM_POLICY_FCFS   ? launch_fcfs(a, st, before, after)
+                 : policy == SEM_POLICY_HPJF ? launch_hpjf(a, st, before, after)
+                                             : launch_class_totals(a, st, before, after);
+  return e == hipSuccess ? SEM_OK : SEM_EDEVICE;
+}
+
 int check_queue_args(const uint8_t* p, const int32_t* l, int64_t n, int32_t* order,
                      int64_t* wait, sem_i128* totals) {
   if (n < 0 || n > INT32_MAX) return SEM_EINVAL;
@@ -380,7 +479,7 @@ const char* sem_strerror(int code) {
 }
 
 int sem_trace_stage(int stage, void* before, void* after) {
-  if (stage < SEM_STAGE_HIST || stage > SEM_STAGE_MERGE) return SEM_EINVAL;
+  if (stage < SEM_STAGE_HIST || stage > SEM_STAGE_POLICY) return SEM_EINVAL;
   std::lock_guard<std::mutex> guard(trace_mu());
   trace_slots().before[stage] = static_cast<hipEvent_t>(before);
   trace_slots().after[stage] = static_cast<hipEvent_t>(after);
@@ -448,6 +547,41 @@ int sem_insert(const uint8_t* priority, const int32_t* length, int64_t n_old, in
   const hipStream_t st = state().stream;
   rc = enqueue_insert(priority, length, n_old, m, order_old, wait_old, order_out, wait_out,
                       totals_out, ws, st);
+  if (rc != SEM_OK) return rc;
+  return finish(ws, st);
+}
+
+size_t sem_policy_workspace_bytes(int policy, int64_t n) {
+  if (n < 0 || !known_policy(policy)) return 0;
+  if (policy == SEM_POLICY_SEMANTIC) return sem_workspace_bytes(n, 1);
+  return policy_layout(policy, n).total;
+}
+
+int sem_schedule_policy_async(int policy, const uint8_t* priority, const int32_t* length,
+                              int64_t n, int32_t* order_out, int64_t* wait_out,
+                              sem_i128* totals_out, void* workspace, size_t ws_bytes,
+                              void* stream) {
+  if (!known_policy(policy)) return SEM_EINVAL;
+  const int rc = check_queue_args(priority, length, n, order_out, wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  if (!workspace || ws_bytes < sem_policy_workspace_bytes(policy, n) ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return SEM_EINVAL;
+  return enqueue_policy(policy, priority, length, n, order_out, wait_out, totals_out, workspace,
+                        static_cast<hipStream_t>(stream));
+}
+
+int sem_schedule_policy(int policy, const uint8_t* priority, const int32_t* length, int64_t n,
+                        int32_t* order_out, int64_t* wait_out, sem_i128* totals_out) {
+  if (!known_policy(policy)) return SEM_EINVAL;
+  int rc = check_queue_args(priority, length, n, order_out, wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  std::lock_guard<std::mutex> g(state().mu);
+  void* ws = nullptr;
+  rc = cached_workspace(sem_policy_workspace_bytes(policy, n), &ws);
+  if (rc != SEM_OK) return rc;
+  const hipStream_t st = state().stream;
+  rc = enqueue_policy(policy, priority, length, n, order_out, wait_out, totals_out, ws, st);
   if (rc != SEM_OK) return rc;
   return finish(ws, st);
 }

@@ -125,7 +125,7 @@ struct GArgs {
 };
 
 // Optional events recorded around one stage's kernel (null: not armed).
-constexpr int kStages = 4;  // hist, first, final (long queues); merge (insertion)
+constexpr int kStages = 5;  // hist, first, final (long queues); merge (insertion); policy pass
 struct StageEvents {
   hipEvent_t before[kStages];
   hipEvent_t after[kStages];
@@ -168,5 +168,36 @@ struct InsArgs {
 int64_t insert_units(int64_t n_old);
 // `before` / `after` (may be null) are recorded around the merge kernel.
 hipError_t launch_insert(const InsArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after);
+
+// ---------------------------------------------------------------------------
+// Comparison policies (policy.hip): FCFS, SJF's class totals, HPJF.
+constexpr int kPolRange = 4096;  // positions per wave of the policy kernels
+
+struct PolArgs {
+  const uint8_t* priority;  // [n]
+  const int32_t* length;    // [n]
+  int64_t n;
+  int32_t* order;           // [n] (SJF: the schedule already computed)
+  int64_t* wait;            // [n]
+  uint64_t* totals;         // (lo, hi) pairs, 1 + 256, zeroed by the caller
+  uint32_t* flags;          // device error bits
+  uint32_t* pmax;           // largest rank, zeroed by the caller
+  uint64_t* rsum;           // [ranges] FCFS: length sum per range, then range offsets
+  uint32_t* tab_cnt;        // [ranges * P] HPJF: per range and class, count, then offset
+  uint64_t* tab_len;        // [ranges * P] HPJF: per range and class, length sum, then offset
+  uint32_t* ctot_cnt;       // [256] HPJF: class sizes
+  uint64_t* ctot_len;       // [256] HPJF: class length totals
+  uint64_t* part;           // [blocks * P] (lo, hi) per-block class sums
+  uint64_t* sink;           // 16 bytes for the stores of lanes without an element
+};
+
+int64_t policy_ranges(int64_t n);
+int64_t policy_blocks(int64_t n);
+// `before` / `after` (may be null) are recorded around the pass that writes
+// the schedule (FCFS, HPJF) or sums the classes (SJF).
+hipError_t launch_fcfs(const PolArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after);
+hipError_t launch_hpjf(const PolArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after);
+hipError_t launch_class_totals(const PolArgs& a, hipStream_t st, hipEvent_t before,
+                               hipEvent_t after);
 
 }  // namespace semsched

@@ -1,0 +1,578 @@
+// Comparison policies of the request-spike experiments (Section 4): first
+// come first served (arrival order), shortest job first (predicted length,
+// then id) and highest-priority job first (urgency rank, then id). Waits are
+// the exclusive prefix of the lengths in the policy's order and the totals
+// are split by each request's own rank, as for the semantic order.
+//
+// Every kernel gives each wave one range of kPolRange consecutive positions
+// (64 rounds of 64 lanes); a block's four waves are independent. Per-class
+// sums are formed once per round for each rank present among the round's
+// lanes (a uniform loop: pick a lane's rank, ballot its peers, reduce them)
+// and kept in lanes: class c in lane c % 64 of register set c / 64.
+//
+//   p_range    largest rank (the class count P = largest + 1)
+//   FCFS       f_sums: length sum of every range, length check;
+//              f_scan: exclusive scan of the range sums;
+//              f_write: order[k] = k, wait = range offset + in-range prefix
+//   HPJF       h_count: per range and class, count and length sum;
+//              h_scan: per class, exclusive scans of both over the ranges;
+//              h_scatter: a stable counting sort by rank, each element at
+//              (class start + range offset + rank among its class in the
+//              range) with wait = the same prefix of lengths
+//   SJF        the semantic kernels with every rank read as 0 (the order by
+//              (length, id)), then s_classes: per-class sums of the waits
+//              with each position's rank gathered through its id
+//   p_total    adds the per-block class sums of the last pass: totals
+#include <algorithm>
+
+#include "block_common.h"
+#include "kernels.h"
+
+namespace semsched {
+
+namespace {
+
+constexpr int PT = 256;                // threads of the range kernels (4 waves)
+constexpr int kWaves = PT / kWave;
+constexpr int kRounds = kPolRange / kWave;  // 64 rounds per range
+constexpr int kBatch = 16;             // rounds loaded together
+constexpr int kBatches = kRounds / kBatch;
+constexpr int ST = 1024;               // threads of the scan kernels
+static_assert(kRounds % kBatch == 0, "whole batches per range");
+
+typedef const __attribute__((address_space(4))) uint64_t ConstU64;
+typedef const __attribute__((address_space(4))) uint32_t ConstU32;
+
+__device__ __forceinline__ int64_t wave_index() {
+  return (int64_t)blockIdx.x * kWaves + __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+}
+
+__device__ __forceinline__ uint32_t class_count(const PolArgs& a) {
+  return *((ConstU32*)a.pmax) + 1u;  // (written by p_range, a kernel before)
+}
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+  return (uint64_t)hi << 32 | lo;
+}
+
+// Uniform 64 x 32 -> 128-bit product plus a 64-bit addend.
+__device__ __forceinline__ U128 mul_add(uint64_t x, uint32_t k, uint64_t add) {
+  U128 r = {x * k, __umul64hi(x, (uint64_t)k)};
+  add128(r, add);
+  return r;
+}
+
+// 256 per-class values held in lanes: class c in lane c % 64 of set c / 64.
+// SETS = 1 when every rank is below 64. The class index and the value added
+// are uniform across the wave.
+template <int SETS, typename T>
+struct LaneTab {
+  T v[SETS];
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int i = 0; i < SETS; ++i) v[i] = 0;
+  }
+  __device__ __forceinline__ T pick(int s) const {
+    T x = v[0];
+#pragma unroll
+    for (int i = 1; i < SETS; ++i) x = s == i ? v[i] : x;
+    return x;
+  }
+  __device__ __forceinline__ T get(uint32_t c) const {
+    const T x = pick((int)(c >> 6));
+    if constexpr (sizeof(T) == 8) return readlane_u64(x, (int)(c & 63));
+    else return (T)__builtin_amdgcn_readlane((int)x, (int)(c & 63));
+  }
+  __device__ __forceinline__ void add(uint32_t c, T d) {
+    const bool me = lane_id() == (int)(c & 63);
+#pragma unroll
+    for (int i = 0; i < SETS; ++i) v[i] += (me && (int)(c >> 6) == i) ? d : (T)0;
+  }
+};
+
+// Exact 128-bit per-class sums in lanes.
+template <int SETS>
+struct LaneAcc {
+  LaneTab<SETS, uint64_t> lo, hi;
+  __device__ __forceinline__ void zero() {
+    lo.zero();
+    hi.zero();
+  }
+  __device__ __forceinline__ void add(uint32_t c, const U128& d) {
+    const bool me = lane_id() == (int)(c & 63);
+#pragma unroll
+    for (int i = 0; i < SETS; ++i) {
+      const bool on = me && (int)(c >> 6) == i;
+      const uint64_t dl = on ? d.lo : 0, dh = on ? d.hi : 0;
+      lo.v[i] += dl;
+      hi.v[i] += dh + (lo.v[i] < dl ? 1u : 0u);
+    }
+  }
+};
+
+// Calls f(c, peers) once for every distinct rank c among the lanes of `live`
+// (`peers` = the live lanes holding c). All 64 lanes must be active.
+template <typename F>
+__device__ __forceinline__ void for_each_class(uint32_t cls, uint64_t live, F&& f) {
+  uint64_t rem = live;
+  while (rem) {
+    const int l0 = __builtin_ctzll(rem);
+    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)cls, l0);
+    const uint64_t peers = __ballot(cls == c) & live;
+    f(c, peers);
+    rem &= ~peers;
+  }
+}
+
+__device__ __forceinline__ bool in_mask(uint64_t m) { return (m >> lane_id()) & 1ull; }
+
+// Sum over the wave of values below 2^40 (per-lane prefixes of a round).
+__device__ __forceinline__ uint64_t wave_sum_u40(uint64_t v) {
+  return readlane_u64(wave_incl_scan_u40(v), 63);
+}
+
+// The block's class sums: every wave adds its lanes into LDS, then the first
+// P threads store them as the block's row of the partial table.
+struct PartShared {
+  uint64_t lo[256], hi[256];
+};
+
+template <int SETS>
+__device__ __forceinline__ void store_partials(const PolArgs& a, const LaneAcc<SETS>& acc,
+                                               PartShared& sh, uint32_t P) {
+#pragma unroll
+  for (int s = 0; s < SETS; ++s) {
+    const U128 v = {acc.lo.v[s], acc.hi.v[s]};
+    const int c = s * kWave + lane_id();
+    if (v.lo | v.hi) atomic_add128(sh.lo + c, sh.hi + c, v);
+  }
+  block_sync();
+  const int t = threadIdx.x;
+  if (t < (int)P) {
+    uint64_t* row = a.part + 2 * ((uint64_t)blockIdx.x * P + t);
+    row[0] = sh.lo[t];
+    row[1] = sh.hi[t];
+  }
+}
+
+__device__ __forceinline__ void zero_partials(PartShared& sh) {
+  sh.lo[threadIdx.x] = sh.hi[threadIdx.x] = 0;
+  block_sync();
+}
+
+// ---------------------------------------------------------------------------
+
+// Largest rank over all requests.
+__global__ __launch_bounds__(PT) void p_range(PolArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * PT;
+  uint32_t m = 0;
+  for (int64_t i = (int64_t)blockIdx.x * PT + threadIdx.x; i < a.n; i += stride)
+    m = max(m, (uint32_t)a.priority[i]);
+  m = wave_max_u32(m);
+  if (lane_id() == 0 && m) atomicMax(a.pmax, m);
+}
+
+// FCFS: length sum of every range; negative lengths are flagged.
+__global__ __launch_bounds__(PT) void f_sums(PolArgs a, int64_t ranges) {
+  const int64_t w = wave_index();
+  if (w >= ranges) return;
+  const int64_t k0 = w * kPolRange;
+  uint64_t s = 0;
+  bool bad = false;
+  for (int r = 0; r < kRounds; ++r) {
+    const int64_t k = k0 + r * kWave + lane_id();
+    const int32_t l = k < a.n ? a.length[k] : 0;
+    bad |= l < 0;
+    s += (uint32_t)l;
+  }
+  if (__ballot(bad)) {
+    if (lane_id() == 0) atomicOr(a.flags, kFlagRange);
+  }
+  s = readlane_u64(wave_incl_scan_u64(s), 63);
+  if (lane_id() == 0) a.rsum[w] = s;
+}
+
+// Exclusive scan of `count` u64 values in place (one block; each thread
+// scans a contiguous chunk). Writes the grand total to *total if non-null.
+__device__ __forceinline__ void chunk_scan_u64(uint64_t* v, int64_t count, int64_t stride,
+                                               uint64_t* total, uint64_t* scratch) {
+  const int t = threadIdx.x;
+  const int64_t per = (count + ST - 1) / ST;
+  const int64_t lo = min(count, t * per), hi = min(count, lo + per);
+  uint64_t s = 0;
+  for (int64_t i = lo; i < hi; ++i) s += v[i * stride];
+  uint64_t tot;
+  uint64_t run = block_excl_scan_u64<ST>(s, scratch, tot);
+  for (int64_t i = lo; i < hi; ++i) {
+    const uint64_t x = v[i * stride];
+    v[i * stride] = run;
+    run += x;
+  }
+  if (total && t == 0) *total = tot;
+}
+
+__global__ __launch_bounds__(ST) void f_scan(PolArgs a, int64_t ranges) {
+  __shared__ uint64_t scratch[ST / kWave + 1];
+  chunk_scan_u64(a.rsum, ranges, 1, nullptr, scratch);
+}
+
+// FCFS: order[k] = k, wait[k] = offset of the range + prefix inside it.
+template <int SETS>
+__device__ __forceinline__ void fcfs_range(const PolArgs& a, int64_t w, LaneAcc<SETS>& acc) {
+  const int64_t k0 = w * kPolRange;
+  uint64_t base = *((ConstU64*)(a.rsum + w));
+  int32_t len[2][kBatch];
+  uint8_t pri[2][kBatch];
+  auto load = [&](int b, int32_t* l, uint8_t* p) {
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) {
+      const int64_t k = min(k0 + (b * kBatch + r) * kWave + lane_id(), a.n - 1);
+      l[r] = a.length[k];
+      p[r] = a.priority[k];
+    }
+  };
+  load(0, len[0], pri[0]);
+#pragma unroll
+  for (int b = 0; b < kBatches; ++b) {
+    const int cur = b & 1;
+    if (b + 1 < kBatches) load(b + 1, len[cur ^ 1], pri[cur ^ 1]);
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) {
+      const int64_t kr = k0 + (b * kBatch + r) * kWave;
+      const int64_t k = kr + lane_id();
+      const bool live = k < a.n;
+      const uint32_t lv = live ? (uint32_t)len[cur][r] : 0u;
+      const uint64_t incl = wave_incl_scan_len(lv);
+      const uint64_t excl = incl - lv;
+      int32_t* po = live ? a.order + k : reinterpret_cast<int32_t*>(a.sink);
+      int64_t* pw = live ? a.wait + k : reinterpret_cast<int64_t*>(a.sink + 1);
+      *po = (int32_t)k;
+      *pw = (int64_t)(base + excl);
+      const uint64_t lmask = __ballot(live);
+      for_each_class((uint32_t)pri[cur][r], lmask, [&](uint32_t c, uint64_t peers) {
+        const uint64_t s = wave_sum_u40(in_mask(peers) ? excl : 0);
+        acc.add(c, mul_add(base, (uint32_t)__popcll(peers), s));
+      });
+      base += readlane_u64(incl, 63);
+    }
+  }
+}
+
+template <int SETS>
+__device__ __forceinline__ void fcfs_write(const PolArgs& a, int64_t ranges, PartShared& sh,
+                                           uint32_t P) {
+  LaneAcc<SETS> acc;
+  acc.zero();
+  const int64_t w = wave_index();
+  if (w < ranges) fcfs_range<SETS>(a, w, acc);
+  store_partials<SETS>(a, acc, sh, P);
+}
+
+__global__ __launch_bounds__(PT) void f_write(PolArgs a, int64_t ranges) {
+  __shared__ PartShared sh;
+  zero_partials(sh);
+  const uint32_t P = class_count(a);
+  if (P <= 64) fcfs_write<1>(a, ranges, sh, P);
+  else fcfs_write<4>(a, ranges, sh, P);
+}
+
+// ---------------------------------------------------------------------------
+// HPJF
+
+template <int SETS>
+__device__ __forceinline__ void hpjf_count(const PolArgs& a, int64_t w, uint32_t P) {
+  LaneTab<SETS, uint32_t> cnt;
+  LaneTab<SETS, uint64_t> lsum;
+  cnt.zero();
+  lsum.zero();
+  const int64_t k0 = w * kPolRange;
+  bool bad = false;
+  for (int r = 0; r < kRounds; ++r) {
+    const int64_t k = k0 + r * kWave + lane_id();
+    const bool live = k < a.n;
+    const int64_t kc = min(k, a.n - 1);
+    const int32_t l = a.length[kc];
+    const uint32_t p = a.priority[kc];
+    bad |= live && l < 0;
+    const uint32_t lv = live ? (uint32_t)l : 0u;
+    for_each_class(p, __ballot(live), [&](uint32_t c, uint64_t peers) {
+      cnt.add(c, (uint32_t)__popcll(peers));
+      lsum.add(c, readlane_u64(wave_incl_scan_len(in_mask(peers) ? lv : 0u), 63));
+    });
+  }
+  if (__ballot(bad)) {
+    if (lane_id() == 0) atomicOr(a.flags, kFlagRange);
+  }
+#pragma unroll
+  for (int s = 0; s < SETS; ++s) {
+    const uint32_t c = s * kWave + lane_id();
+    if (c < P) {
+      a.tab_cnt[w * P + c] = cnt.v[s];
+      a.tab_len[w * P + c] = lsum.v[s];
+    }
+  }
+}
+
+__global__ __launch_bounds__(PT) void h_count(PolArgs a, int64_t ranges) {
+  const int64_t w = wave_index();
+  if (w >= ranges) return;
+  const uint32_t P = class_count(a);
+  if (P <= 64) hpjf_count<1>(a, w, P);
+  else hpjf_count<4>(a, w, P);
+}
+
+// Block c: exclusive scans over the ranges of class c's counts and length
+// sums (in place); the class's size and length total.
+__global__ __launch_bounds__(ST) void h_scan(PolArgs a, int64_t ranges) {
+  __shared__ uint32_t s32[ST / kWave + 1];
+  __shared__ uint64_t s64[ST / kWave + 1];
+  const uint32_t P = class_count(a);
+  const uint32_t c = blockIdx.x;
+  if (c >= P) return;
+  const int t = threadIdx.x;
+  const int64_t per = (ranges + ST - 1) / ST;
+  const int64_t lo = min(ranges, t * per), hi = min(ranges, lo + per);
+  uint32_t sc = 0;
+  uint64_t sl = 0;
+  for (int64_t i = lo; i < hi; ++i) {
+    sc += a.tab_cnt[i * P + c];
+    sl += a.tab_len[i * P + c];
+  }
+  uint32_t tc;
+  uint64_t tl;
+  uint32_t rc = block_excl_scan_u32<ST>(sc, s32, tc);
+  uint64_t rl = block_excl_scan_u64<ST>(sl, s64, tl);
+  for (int64_t i = lo; i < hi; ++i) {
+    const uint32_t x = a.tab_cnt[i * P + c];
+    const uint64_t y = a.tab_len[i * P + c];
+    a.tab_cnt[i * P + c] = rc;
+    a.tab_len[i * P + c] = rl;
+    rc += x;
+    rl += y;
+  }
+  if (t == 0) {
+    a.ctot_cnt[c] = tc;
+    a.ctot_len[c] = tl;
+  }
+}
+
+template <int SETS>
+__device__ __forceinline__ void hpjf_range(const PolArgs& a, int64_t w, uint32_t P,
+                                           LaneAcc<SETS>& acc) {
+  // running output position and wait of every class in this range: class
+  // start (exclusive scan of the class sizes / length totals) + the range's
+  // offset inside the class
+  LaneTab<SETS, uint32_t> pos;
+  LaneTab<SETS, uint64_t> wb;
+  uint32_t carry_c = 0;
+  uint64_t carry_l = 0;
+#pragma unroll
+  for (int s = 0; s < SETS; ++s) {
+    const uint32_t c = s * kWave + lane_id();
+    const uint32_t cc = c < P ? a.ctot_cnt[c] : 0u;
+    const uint64_t cl = c < P ? a.ctot_len[c] : 0u;
+    const uint32_t ic = wave_incl_scan_u32(cc);
+    const uint64_t il = wave_incl_scan_u64(cl);
+    pos.v[s] = carry_c + ic - cc + (c < P ? a.tab_cnt[w * P + c] : 0u);
+    wb.v[s] = carry_l + il - cl + (c < P ? a.tab_len[w * P + c] : 0u);
+    carry_c += (uint32_t)__builtin_amdgcn_readlane((int)ic, 63);
+    carry_l += readlane_u64(il, 63);
+  }
+  const int64_t k0 = w * kPolRange;
+  int32_t len[2][kBatch];
+  uint8_t pri[2][kBatch];
+  auto load = [&](int b, int32_t* l, uint8_t* p) {
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) {
+      const int64_t k = min(k0 + (b * kBatch + r) * kWave + lane_id(), a.n - 1);
+      l[r] = a.length[k];
+      p[r] = a.priority[k];
+    }
+  };
+  load(0, len[0], pri[0]);
+#pragma unroll
+  for (int b = 0; b < kBatches; ++b) {
+    const int cur = b & 1;
+    if (b + 1 < kBatches) load(b + 1, len[cur ^ 1], pri[cur ^ 1]);
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) {
+      const int64_t k = k0 + (b * kBatch + r) * kWave + lane_id();
+      const bool live = k < a.n;
+      const uint32_t lv = live ? (uint32_t)len[cur][r] : 0u;
+      uint32_t q = 0;
+      uint64_t wt = 0;
+      for_each_class((uint32_t)pri[cur][r], __ballot(live), [&](uint32_t c, uint64_t peers) {
+        const bool mine = in_mask(peers);
+        const uint32_t mv = mine ? lv : 0u;
+        const uint64_t incl = wave_incl_scan_len(mv);
+        const uint64_t excl = incl - mv;
+        const uint32_t pc = pos.get(c);
+        const uint64_t wc = wb.get(c);
+        const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
+            (uint32_t)(peers >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
+        q = mine ? pc + rank : q;
+        wt = mine ? wc + excl : wt;
+        const uint32_t cnt = (uint32_t)__popcll(peers);
+        acc.add(c, mul_add(wc, cnt, wave_sum_u40(mine ? excl : 0)));
+        pos.add(c, cnt);
+        wb.add(c, readlane_u64(incl, 63));
+      });
+      const bool ok = live && (int64_t)q < a.n;  // (always, for consistent counts)
+      int32_t* po = ok ? a.order + q : reinterpret_cast<int32_t*>(a.sink);
+      int64_t* pw = ok ? a.wait + q : reinterpret_cast<int64_t*>(a.sink + 1);
+      *po = (int32_t)k;
+      *pw = (int64_t)wt;
+    }
+  }
+}
+
+template <int SETS>
+__device__ __forceinline__ void hpjf_scatter(const PolArgs& a, int64_t ranges, PartShared& sh,
+                                             uint32_t P) {
+  LaneAcc<SETS> acc;
+  acc.zero();
+  const int64_t w = wave_index();
+  if (w < ranges) hpjf_range<SETS>(a, w, P, acc);
+  store_partials<SETS>(a, acc, sh, P);
+}
+
+__global__ __launch_bounds__(PT) void h_scatter(PolArgs a, int64_t ranges) {
+  __shared__ PartShared sh;
+  zero_partials(sh);
+  const uint32_t P = class_count(a);
+  if (P <= 64) hpjf_scatter<1>(a, ranges, sh, P);
+  else hpjf_scatter<4>(a, ranges, sh, P);
+}
+
+// ---------------------------------------------------------------------------
+// SJF: per-class sums of an existing schedule's waits, the rank of each
+// position gathered through its id. Waits grow along the schedule, so each
+// round's waits are lane 0's plus a difference below 2^37.
+
+template <int SETS>
+__device__ __forceinline__ void class_range(const PolArgs& a, int64_t w, LaneAcc<SETS>& acc) {
+  const int64_t k0 = w * kPolRange;
+  for (int b = 0; b < kBatches; ++b) {
+    int32_t id[kBatch];
+    uint64_t wt[kBatch];
+    uint32_t p[kBatch];
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) {
+      const int64_t k = min(k0 + (b * kBatch + r) * kWave + lane_id(), a.n - 1);
+      id[r] = a.order[k];
+      wt[r] = (uint64_t)a.wait[k];
+    }
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r)
+      p[r] = a.priority[min(max((int64_t)id[r], (int64_t)0), a.n - 1)];
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) {
+      const int64_t k = k0 + (b * kBatch + r) * kWave + lane_id();
+      const bool live = k < a.n;
+      const uint64_t w0 = readlane_u64(wt[r], 0);
+      const uint64_t d = wt[r] - w0;
+      for_each_class(p[r], __ballot(live), [&](uint32_t c, uint64_t peers) {
+        acc.add(c, mul_add(w0, (uint32_t)__popcll(peers), wave_sum_u40(in_mask(peers) ? d : 0)));
+      });
+    }
+  }
+}
+
+template <int SETS>
+__device__ __forceinline__ void class_sums(const PolArgs& a, int64_t ranges, PartShared& sh,
+                                           uint32_t P) {
+  LaneAcc<SETS> acc;
+  acc.zero();
+  const int64_t w = wave_index();
+  if (w < ranges) class_range<SETS>(a, w, acc);
+  store_partials<SETS>(a, acc, sh, P);
+}
+
+__global__ __launch_bounds__(PT) void s_classes(PolArgs a, int64_t ranges) {
+  __shared__ PartShared sh;
+  zero_partials(sh);
+  const uint32_t P = class_count(a);
+  if (P <= 64) class_sums<1>(a, ranges, sh, P);
+  else class_sums<4>(a, ranges, sh, P);
+}
+
+// Block c: class c's total from the blocks' partial sums; added to the grand
+// total as well. totals were zeroed before.
+__global__ __launch_bounds__(PT) void p_total(PolArgs a, int64_t blocks) {
+  __shared__ U128 ws[kWaves];
+  const uint32_t P = class_count(a);
+  const uint32_t c = blockIdx.x;
+  if (c >= P) return;
+  U128 s = {0, 0};
+  for (int64_t b = threadIdx.x; b < blocks; b += PT) {
+    const uint64_t* row = a.part + 2 * ((uint64_t)b * P + c);
+    add128(s, U128{row[0], row[1]});
+  }
+  s = wave_sum128(s);
+  if (lane_id() == 0) ws[threadIdx.x / kWave] = s;
+  block_sync();
+  if (threadIdx.x == 0) {
+    U128 g = {0, 0};
+    for (int i = 0; i < kWaves; ++i) add128(g, ws[i]);
+    a.totals[2 * (1 + c)] = g.lo;
+    a.totals[2 * (1 + c) + 1] = g.hi;
+    if (g.lo | g.hi) atomic_add128(a.totals, a.totals + 1, g);
+  }
+}
+
+int64_t ranges_of(int64_t n) { return (n + kPolRange - 1) / kPolRange; }
+int64_t blocks_of(int64_t n) { return (ranges_of(n) + kWaves - 1) / kWaves; }
+
+hipError_t launch_p_range(const PolArgs& a, hipStream_t st) {
+  const int64_t g = std::min<int64_t>((a.n + PT * 16 - 1) / (PT * 16), 2048);
+  hipLaunchKernelGGL(p_range, dim3((unsigned)std::max<int64_t>(g, 1)), dim3(PT), 0, st, a);
+  return hipGetLastError();
+}
+
+void mark(hipEvent_t e, hipStream_t st) {
+  if (e) (void)hipEventRecord(e, st);
+}
+
+}  // namespace
+
+int64_t policy_ranges(int64_t n) { return ranges_of(n); }
+int64_t policy_blocks(int64_t n) { return blocks_of(n); }
+
+hipError_t launch_fcfs(const PolArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after) {
+  const int64_t ranges = ranges_of(a.n), blocks = blocks_of(a.n);
+  if (launch_p_range(a, st) != hipSuccess) return hipGetLastError();
+  hipLaunchKernelGGL(f_sums, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(f_scan, dim3(1), dim3(ST), 0, st, a, ranges);
+  mark(before, st);
+  hipLaunchKernelGGL(f_write, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  mark(after, st);
+  hipLaunchKernelGGL(p_total, dim3(256), dim3(PT), 0, st, a, blocks);
+  return hipGetLastError();
+}
+
+hipError_t launch_hpjf(const PolArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after) {
+  const int64_t ranges = ranges_of(a.n), blocks = blocks_of(a.n);
+  if (launch_p_range(a, st) != hipSuccess) return hipGetLastError();
+  hipLaunchKernelGGL(h_count, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(h_scan, dim3(256), dim3(ST), 0, st, a, ranges);
+  mark(before, st);
+  hipLaunchKernelGGL(h_scatter, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  mark(after, st);
+  hipLaunchKernelGGL(p_total, dim3(256), dim3(PT), 0, st, a, blocks);
+  return hipGetLastError();
+}
+
+hipError_t launch_class_totals(const PolArgs& a, hipStream_t st, hipEvent_t before,
+                               hipEvent_t after) {
+  const int64_t ranges = ranges_of(a.n), blocks = blocks_of(a.n);
+  if (launch_p_range(a, st) != hipSuccess) return hipGetLastError();
+  mark(before, st);
+  hipLaunchKernelGGL(s_classes, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  mark(after, st);
+  hipLaunchKernelGGL(p_total, dim3(256), dim3(PT), 0, st, a, blocks);
+  return hipGetLastError();
+}
+
+}  // namespace semsched

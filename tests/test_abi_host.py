@@ -112,3 +112,21 @@ def test_insert_argument_errors(ss):
                         ctypes.c_void_p(base + (1 << 20) + 16), fake) == ss.SEM_EINVAL
     assert ss.lib.sem_insert_workspace_bytes(-1, 3) == 0
     assert ss.lib.sem_insert_workspace_bytes(1000, 100) >= 256 + 16 * 100
+
+
+def test_policy_argument_errors(ss):
+    L = ss.lib
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 40)  # never dereferenced: the call fails first
+    for policy in (ss.POLICY_SEMANTIC, ss.POLICY_FCFS, ss.POLICY_SJF, ss.POLICY_HPJF):
+        assert L.sem_schedule_policy(policy, fake, fake, -1, fake, fake, fake) == ss.SEM_EINVAL
+        assert L.sem_schedule_policy(policy, nul, fake, 5, fake, fake, fake) == ss.SEM_EINVAL
+        assert L.sem_schedule_policy(policy, fake, fake, 5, fake, fake, nul) == ss.SEM_EINVAL
+        assert L.sem_policy_workspace_bytes(policy, 1 << 20) >= 256
+        assert L.sem_schedule_policy_async(policy, fake, fake, 1 << 20, fake, fake, fake, fake,
+                                           256, nul) == ss.SEM_EINVAL
+    for bad in (-1, 4, 99):
+        assert L.sem_schedule_policy(bad, fake, fake, 5, fake, fake, fake) == ss.SEM_EINVAL
+        assert L.sem_policy_workspace_bytes(bad, 5) == 0
+    assert L.sem_policy_workspace_bytes(ss.POLICY_SEMANTIC, 1 << 20) == ss.workspace_bytes(1 << 20)
+    assert L.sem_policy_workspace_bytes(ss.POLICY_FCFS, -1) == 0
