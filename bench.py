@@ -49,6 +49,21 @@ COUNTERS = os.path.join(ROOT, "profiles", "final_pass_c3_counters.md")
 FINAL_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "global_sort.hip")
 MERGE_COUNTERS = os.path.join(ROOT, "profiles", "insert_merge_c3_counters.md")
 MERGE_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "insert.hip")
+WORKLOAD_TEXT = {
+    "c3": "single queue n=2^26, 5 urgency classes uniform, lengths uniform int32 in [1,32768], "
+          "seed 2",
+    "c2": "single queue n=2^20, 10 Zipf(1.2) classes, lognormal lengths, seed 1",
+}
+POLICY_COUNTERS = os.path.join(ROOT, "profiles", "policy_c3_counters.md")
+POLICY_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "policy.hip")
+# algorithmic bytes per request of the pass each policy's roofline is taken on
+# (FCFS and HPJF: rank and length read, order and wait written; SJF's class
+# pass: order and wait read, the rank gathered through the id)
+POLICY_PASS = {
+    "fcfs": ("f_write: identity order and waits", 17),
+    "hpjf": ("h_scatter: stable scatter by rank", 17),
+    "sjf": ("s_classes: per-class sums of the waits", 13),
+}
 
 
 class HipEvents:
@@ -90,7 +105,8 @@ def code_sha(path: str) -> str:
     return hashlib.sha256("\n".join(lines).encode()).hexdigest()
 
 
-def counter_traffic(n: int, counters: str = COUNTERS, source: str = FINAL_SOURCE):
+def counter_traffic(n: int, counters: str = COUNTERS, source: str = FINAL_SOURCE,
+                    prefix: str = ""):
     """HBM bytes per launch of a kernel from committed rocprofv3 counters.
 
     The summary file carries `key: value` lines (n, code_sha256,
@@ -107,7 +123,8 @@ def counter_traffic(n: int, counters: str = COUNTERS, source: str = FINAL_SOURCE
                 kv[k.strip()] = v.strip().strip("`")
     if kv.get("code_sha256") != code_sha(source) or kv.get("n") != str(n):
         return None
-    return float(kv["hbm_bytes_per_launch"])
+    key = prefix + "hbm_bytes_per_launch"
+    return float(kv[key]) if key in kv else None
 
 
 def copy_probe() -> int:
@@ -248,15 +265,103 @@ def bench_insert(args) -> int:
     return 0
 
 
+def bench_policy(args) -> int:
+    """One comparison policy (FCFS / SJF / HPJF) on the n = 2^26 workload;
+    one step = the whole schedule under that policy."""
+    import torch
+    import paper_2506_12204_amd as ss
+    from workloads import generate
+
+    code = {"fcfs": ss.POLICY_FCFS, "sjf": ss.POLICY_SJF, "hpjf": ss.POLICY_HPJF}[args.policy]
+    w = generate(args.workload)
+    n = w.n
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    p = torch.from_numpy(w.priority).to(dev)
+    l = torch.from_numpy(w.length).to(dev)
+    sched = ss.PolicyScheduler(n, code, dev)
+    print(f"[bench] policy {args.policy} workload {args.workload} n={n}; warmup {args.warmup}",
+          file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        sched.run(p, l)
+    sched.check()
+    hip = HipEvents()
+    pairs = [(hip.create(), hip.create()) for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for k in range(args.steps):
+        ss.trace_stage(ss.STAGE_POLICY, *pairs[k])
+        sched.run(p, l)
+    t1.record()
+    torch.cuda.synchronize()
+    sched.check()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    pass_ms = sum(hip.elapsed_ms(a, b) for a, b in pairs) / args.steps
+    for a, b in pairs:
+        hip.destroy(a)
+        hip.destroy(b)
+    kernel, per_req = POLICY_PASS[args.policy]
+    print(f"[bench] {args.steps} schedules: {ms_step:.4f} ms each; {kernel}: {pass_ms:.4f} ms",
+          file=sys.stderr, flush=True)
+    pass_bytes = per_req * n
+    achieved = pass_bytes / (pass_ms * 1e-3) / 1e9
+    out = {
+        "metric": f"scheduled requests/s under {args.policy.upper()}, single queue, 1 GPU",
+        "value": n / (ms_step * 1e-3),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "n": n,
+                   "policy": args.policy, "parallelism": "single GPU"},
+        "roofline": {
+            "bound": "hbm", "kernel": kernel, "achieved": achieved,
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": counter_traffic(n, POLICY_COUNTERS, POLICY_SOURCE, args.policy + "."),
+            "bytes_per_launch": pass_bytes, "avg_launch_ms": pass_ms,
+        },
+    }
+    if not args.no_cpu_baseline:
+        from oracle import c_oracle_policy
+        t = time.perf_counter()
+        want = c_oracle_policy(w.priority, w.length, code)
+        dt = time.perf_counter() - t
+        same = (want[0].tobytes() == sched.order.cpu().numpy().tobytes()
+                and want[1].tobytes() == sched.wait.cpu().numpy().tobytes()
+                and list(want[2]) == ss.totals_to_ints(sched.totals))
+        out["cpu_baseline"] = {
+            "value": n / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": (f"the full workload (n={n}): the plain C oracle's merge sort by the "
+                       f"policy's key and running sum, single thread"),
+        }
+        out["parity"] = "bit-exact vs oracle" if same else "MISMATCH vs oracle"
+        if not same:
+            print(json.dumps(out))
+            return 1
+    print(json.dumps(out))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c3", choices=["c3", "c2"])
-    ap.add_argument("--op", default="schedule", choices=["schedule", "insert"],
+    ap.add_argument("--op", default="schedule", choices=["schedule", "insert", "policy"],
                     help="schedule (default): the whole queue; insert: 2^16 arrivals "
-                         "merged into the schedule of the rest")
+                         "merged into the schedule of the rest; policy: the queue under "
+                         "--policy")
+    ap.add_argument("--policy", default="fcfs", choices=["fcfs", "sjf", "hpjf"],
+                    help="comparison policy timed by --op policy")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle leg (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -270,6 +375,8 @@ def main() -> int:
         return 2
     if args.op == "insert":
         return bench_insert(args)
+    if args.op == "policy":
+        return bench_policy(args)
 
     import numpy as np
     import torch
@@ -333,10 +440,7 @@ def main() -> int:
         "dtype": "int64",
         "data": "synthetic",
         "config": {
-            "workload": ("single queue n=2^26, 5 urgency classes uniform, "
-                         "lengths uniform int32 in [1,32768], seed 2"
-                         if args.workload == "c3" else
-                         "single queue n=2^20, 10 Zipf(1.2) classes, lognormal lengths, seed 1"),
+            "workload": WORKLOAD_TEXT[args.workload],
             "n": n,
             "parallelism": "single GPU",
         },

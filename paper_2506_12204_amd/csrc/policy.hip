@@ -5,13 +5,18 @@
 // are split by each request's own rank, as for the semantic order.
 //
 // Every kernel gives each wave one range of kPolRange consecutive positions
-// (64 rounds of 64 lanes); a block's four waves are independent. Per-class
-// sums are formed once per round for each rank present among the round's
-// lanes (a uniform loop: pick a lane's rank, ballot its peers, reduce them)
-// and kept in lanes: class c in lane c % 64 of register set c / 64.
+// (64 rounds of 64 lanes); a block's four waves are independent. With at most
+// kRegClasses ranks every lane keeps its own per-class sums in registers
+// (one compare and two selects per class and element) and the wave reduces
+// them once per range. With more ranks the sums are formed once per round
+// for each rank present among the round's lanes (a uniform loop: pick a
+// lane's rank, ballot its peers, reduce them) and kept in lanes: class c in
+// lane c % 64 of register set c / 64. The two forms are separate kernels
+// (registers are allocated per kernel); both are launched and the one that
+// does not fit the class count returns at once.
 //
 //   p_range    largest rank (the class count P = largest + 1)
-//   FCFS       f_sums: length sum of every range, length check;
+//   FCFS       f_sums: length sum of every range, length check, largest rank;
 //              f_scan: exclusive scan of the range sums;
 //              f_write: order[k] = k, wait = range offset + in-range prefix
 //   HPJF       h_count: per range and class, count and length sum;
@@ -35,7 +40,7 @@ namespace {
 constexpr int PT = 256;                // threads of the range kernels (4 waves)
 constexpr int kWaves = PT / kWave;
 constexpr int kRounds = kPolRange / kWave;  // 64 rounds per range
-constexpr int kBatch = 16;             // rounds loaded together
+constexpr int kBatch = 8;              // rounds loaded together
 constexpr int kBatches = kRounds / kBatch;
 constexpr int ST = 1024;               // threads of the scan kernels
 static_assert(kRounds % kBatch == 0, "whole batches per range");
@@ -112,6 +117,54 @@ struct LaneAcc {
   }
 };
 
+constexpr int kRegClasses = 8;  // up to this many ranks, per-lane class sums in registers
+
+// Per-lane sums of 64-bit values (below 2^62) for classes c < PB, kept as the
+// sums of their low and high 32-bit halves: a lane adds at most kRounds
+// values per range, so each half-sum stays below 2^38.
+template <int PB>
+struct RegSums {
+  uint64_t lo[PB], hi[PB];
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int c = 0; c < PB; ++c) lo[c] = hi[c] = 0;
+  }
+  __device__ __forceinline__ void add(uint32_t cls, uint64_t v, uint32_t P) {
+#pragma unroll
+    for (int c = 0; c < PB; ++c) {
+      if (c < (int)P) {
+        const bool on = cls == (uint32_t)c;
+        lo[c] += on ? (uint32_t)v : 0u;
+        hi[c] += on ? (uint32_t)(v >> 32) : 0u;
+      }
+    }
+  }
+};
+
+// Per-lane element counts and length sums for classes c < PB.
+template <int PB>
+struct RegCounts {
+  uint32_t cnt[PB];
+  uint64_t len[PB];
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int c = 0; c < PB; ++c) {
+      cnt[c] = 0;
+      len[c] = 0;
+    }
+  }
+  __device__ __forceinline__ void add(uint32_t cls, uint32_t l, bool live, uint32_t P) {
+#pragma unroll
+    for (int c = 0; c < PB; ++c) {
+      if (c < (int)P) {
+        const bool on = live && cls == (uint32_t)c;
+        cnt[c] += on ? 1u : 0u;
+        len[c] += on ? l : 0u;
+      }
+    }
+  }
+};
+
 // Calls f(c, peers) once for every distinct rank c among the lanes of `live`
 // (`peers` = the live lanes holding c). All 64 lanes must be active.
 template <typename F>
@@ -140,20 +193,41 @@ struct PartShared {
 };
 
 template <int SETS>
-__device__ __forceinline__ void store_partials(const PolArgs& a, const LaneAcc<SETS>& acc,
-                                               PartShared& sh, uint32_t P) {
+__device__ __forceinline__ void store_lane_acc(const LaneAcc<SETS>& acc, PartShared& sh) {
 #pragma unroll
   for (int s = 0; s < SETS; ++s) {
     const U128 v = {acc.lo.v[s], acc.hi.v[s]};
     const int c = s * kWave + lane_id();
     if (v.lo | v.hi) atomic_add128(sh.lo + c, sh.hi + c, v);
   }
+}
+
+// Lane 0 adds a wave-uniform class sum into the block's LDS table.
+__device__ __forceinline__ void add_partial(PartShared& sh, uint32_t c, const U128& v) {
+  if (lane_id() == 0 && (v.lo | v.hi)) atomic_add128(sh.lo + c, sh.hi + c, v);
+}
+
+// The block's row of the partial table (after every wave has added its sums).
+__device__ __forceinline__ void write_partials(const PolArgs& a, PartShared& sh, uint32_t P) {
   block_sync();
   const int t = threadIdx.x;
   if (t < (int)P) {
     uint64_t* row = a.part + 2 * ((uint64_t)blockIdx.x * P + t);
     row[0] = sh.lo[t];
     row[1] = sh.hi[t];
+  }
+}
+
+template <int PB>
+__device__ __forceinline__ void flush_sums(PartShared& sh, const RegSums<PB>& s, uint32_t P) {
+#pragma unroll
+  for (int c = 0; c < PB; ++c) {
+    if (c < (int)P) {
+      const uint64_t l = wave_sum_u40(s.lo[c]), h = wave_sum_u40(s.hi[c]);
+      U128 v = {l, 0};
+      add128(v, U128{h << 32, h >> 32});
+      add_partial(sh, (uint32_t)c, v);
+    }
   }
 }
 
@@ -164,32 +238,57 @@ __device__ __forceinline__ void zero_partials(PartShared& sh) {
 
 // ---------------------------------------------------------------------------
 
-// Largest rank over all requests.
+__device__ __forceinline__ uint32_t max_byte(uint32_t m, uint32_t x) {
+  m = max(m, x & 0xffu);
+  m = max(m, (x >> 8) & 0xffu);
+  m = max(m, (x >> 16) & 0xffu);
+  return max(m, x >> 24);
+}
+
+// Largest rank over all requests: 16-byte loads over the aligned body,
+// single bytes before and after it.
 __global__ __launch_bounds__(PT) void p_range(PolArgs a) {
+  const uintptr_t addr = reinterpret_cast<uintptr_t>(a.priority);
+  const int64_t head = std::min<int64_t>(a.n, (int64_t)((16 - (addr & 15)) & 15));
+  const int64_t body = (a.n - head) / 16;
+  const uint4* v = reinterpret_cast<const uint4*>(a.priority + head);
   const int64_t stride = (int64_t)gridDim.x * PT;
+  const int64_t t = (int64_t)blockIdx.x * PT + threadIdx.x;
   uint32_t m = 0;
-  for (int64_t i = (int64_t)blockIdx.x * PT + threadIdx.x; i < a.n; i += stride)
-    m = max(m, (uint32_t)a.priority[i]);
+  for (int64_t i = t; i < body; i += stride) {
+    const uint4 x = v[i];
+    m = max_byte(max_byte(max_byte(max_byte(m, x.x), x.y), x.z), x.w);
+  }
+  if (t < head) m = max(m, (uint32_t)a.priority[t]);
+  const int64_t tail = head + body * 16;
+  if (tail + t < a.n) m = max(m, (uint32_t)a.priority[tail + t]);  // (fewer than 16 left)
   m = wave_max_u32(m);
   if (lane_id() == 0 && m) atomicMax(a.pmax, m);
 }
 
-// FCFS: length sum of every range; negative lengths are flagged.
+// FCFS: length sum of every range and the largest rank; negative lengths
+// are flagged.
 __global__ __launch_bounds__(PT) void f_sums(PolArgs a, int64_t ranges) {
   const int64_t w = wave_index();
   if (w >= ranges) return;
   const int64_t k0 = w * kPolRange;
   uint64_t s = 0;
+  uint32_t m = 0;
   bool bad = false;
+#pragma unroll 16
   for (int r = 0; r < kRounds; ++r) {
     const int64_t k = k0 + r * kWave + lane_id();
-    const int32_t l = k < a.n ? a.length[k] : 0;
+    const int64_t kc = min(k, a.n - 1);
+    const int32_t l = k < a.n ? a.length[kc] : 0;
+    m = max(m, (uint32_t)a.priority[kc]);
     bad |= l < 0;
     s += (uint32_t)l;
   }
   if (__ballot(bad)) {
     if (lane_id() == 0) atomicOr(a.flags, kFlagRange);
   }
+  m = wave_max_u32(m);
+  if (lane_id() == 0 && m) atomicMax(a.pmax, m);
   s = readlane_u64(wave_incl_scan_u64(s), 63);
   if (lane_id() == 0) a.rsum[w] = s;
 }
@@ -219,12 +318,19 @@ __global__ __launch_bounds__(ST) void f_scan(PolArgs a, int64_t ranges) {
 }
 
 // FCFS: order[k] = k, wait[k] = offset of the range + prefix inside it.
-template <int SETS>
-__device__ __forceinline__ void fcfs_range(const PolArgs& a, int64_t w, LaneAcc<SETS>& acc) {
+// PB > 0: per-class sums in registers (P <= PB); PB = 0: the class loop with
+// lane tables of SETS sets.
+template <int PB, int SETS>
+__device__ __forceinline__ void fcfs_range(const PolArgs& a, int64_t w, uint32_t P,
+                                           PartShared& sh) {
+  RegSums<PB == 0 ? 1 : PB> rs;
+  LaneAcc<SETS> acc;
+  rs.zero();
+  acc.zero();
   const int64_t k0 = w * kPolRange;
   uint64_t base = *((ConstU64*)(a.rsum + w));
-  int32_t len[2][kBatch];
-  uint8_t pri[2][kBatch];
+  int32_t len[kBatch], nlen[kBatch];  // this batch, the next one
+  uint8_t pri[kBatch], npri[kBatch];
   auto load = [&](int b, int32_t* l, uint8_t* p) {
 #pragma unroll
     for (int r = 0; r < kBatch; ++r) {
@@ -233,62 +339,77 @@ __device__ __forceinline__ void fcfs_range(const PolArgs& a, int64_t w, LaneAcc<
       p[r] = a.priority[k];
     }
   };
-  load(0, len[0], pri[0]);
-#pragma unroll
+  load(0, len, pri);
+#pragma unroll 1
   for (int b = 0; b < kBatches; ++b) {
-    const int cur = b & 1;
-    if (b + 1 < kBatches) load(b + 1, len[cur ^ 1], pri[cur ^ 1]);
+    load(min(b + 1, kBatches - 1), nlen, npri);  // (the last batch reloads itself)
 #pragma unroll
     for (int r = 0; r < kBatch; ++r) {
       const int64_t kr = k0 + (b * kBatch + r) * kWave;
       const int64_t k = kr + lane_id();
       const bool live = k < a.n;
-      const uint32_t lv = live ? (uint32_t)len[cur][r] : 0u;
+      const uint32_t lv = live ? (uint32_t)len[r] : 0u;
       const uint64_t incl = wave_incl_scan_len(lv);
       const uint64_t excl = incl - lv;
+      const uint64_t wt = base + excl;
       int32_t* po = live ? a.order + k : reinterpret_cast<int32_t*>(a.sink);
       int64_t* pw = live ? a.wait + k : reinterpret_cast<int64_t*>(a.sink + 1);
       *po = (int32_t)k;
-      *pw = (int64_t)(base + excl);
-      const uint64_t lmask = __ballot(live);
-      for_each_class((uint32_t)pri[cur][r], lmask, [&](uint32_t c, uint64_t peers) {
-        const uint64_t s = wave_sum_u40(in_mask(peers) ? excl : 0);
-        acc.add(c, mul_add(base, (uint32_t)__popcll(peers), s));
-      });
+      *pw = (int64_t)wt;
+      if constexpr (PB > 0) {
+        rs.add((uint32_t)pri[r], live ? wt : 0, P);
+      } else {
+        for_each_class((uint32_t)pri[r], __ballot(live), [&](uint32_t c, uint64_t peers) {
+          const uint64_t s2 = wave_sum_u40(in_mask(peers) ? excl : 0);
+          acc.add(c, mul_add(base, (uint32_t)__popcll(peers), s2));
+        });
+      }
       base += readlane_u64(incl, 63);
     }
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) {
+      len[r] = nlen[r];
+      pri[r] = npri[r];
+    }
   }
+  if constexpr (PB > 0) flush_sums<PB>(sh, rs, P);
+  else store_lane_acc<SETS>(acc, sh);
 }
 
-template <int SETS>
+template <int PB, int SETS>
 __device__ __forceinline__ void fcfs_write(const PolArgs& a, int64_t ranges, PartShared& sh,
                                            uint32_t P) {
-  LaneAcc<SETS> acc;
-  acc.zero();
   const int64_t w = wave_index();
-  if (w < ranges) fcfs_range<SETS>(a, w, acc);
-  store_partials<SETS>(a, acc, sh, P);
+  if (w < ranges) fcfs_range<PB, SETS>(a, w, P, sh);
+  write_partials(a, sh, P);
 }
 
+template <bool REG>
 __global__ __launch_bounds__(PT) void f_write(PolArgs a, int64_t ranges) {
   __shared__ PartShared sh;
-  zero_partials(sh);
   const uint32_t P = class_count(a);
-  if (P <= 64) fcfs_write<1>(a, ranges, sh, P);
-  else fcfs_write<4>(a, ranges, sh, P);
+  if (REG != (P <= kRegClasses)) return;
+  zero_partials(sh);
+  if constexpr (REG) fcfs_write<kRegClasses, 1>(a, ranges, sh, P);
+  else fcfs_write<0, 4>(a, ranges, sh, P);
 }
 
 // ---------------------------------------------------------------------------
 // HPJF
 
-template <int SETS>
+// Per-class counts and length sums of one range: in registers (PB > 0) or by
+// the class loop into lane tables of SETS sets.
+template <int PB, int SETS>
 __device__ __forceinline__ void hpjf_count(const PolArgs& a, int64_t w, uint32_t P) {
+  RegCounts<PB == 0 ? 1 : PB> rc;
   LaneTab<SETS, uint32_t> cnt;
   LaneTab<SETS, uint64_t> lsum;
+  rc.zero();
   cnt.zero();
   lsum.zero();
   const int64_t k0 = w * kPolRange;
   bool bad = false;
+#pragma unroll 16
   for (int r = 0; r < kRounds; ++r) {
     const int64_t k = k0 + r * kWave + lane_id();
     const bool live = k < a.n;
@@ -297,30 +418,50 @@ __device__ __forceinline__ void hpjf_count(const PolArgs& a, int64_t w, uint32_t
     const uint32_t p = a.priority[kc];
     bad |= live && l < 0;
     const uint32_t lv = live ? (uint32_t)l : 0u;
-    for_each_class(p, __ballot(live), [&](uint32_t c, uint64_t peers) {
-      cnt.add(c, (uint32_t)__popcll(peers));
-      lsum.add(c, readlane_u64(wave_incl_scan_len(in_mask(peers) ? lv : 0u), 63));
-    });
+    if constexpr (PB > 0) {
+      rc.add(p, lv, live, P);
+    } else {
+      for_each_class(p, __ballot(live), [&](uint32_t c, uint64_t peers) {
+        cnt.add(c, (uint32_t)__popcll(peers));
+        lsum.add(c, readlane_u64(wave_incl_scan_len(in_mask(peers) ? lv : 0u), 63));
+      });
+    }
   }
   if (__ballot(bad)) {
     if (lane_id() == 0) atomicOr(a.flags, kFlagRange);
   }
+  if constexpr (PB > 0) {
 #pragma unroll
-  for (int s = 0; s < SETS; ++s) {
-    const uint32_t c = s * kWave + lane_id();
-    if (c < P) {
-      a.tab_cnt[w * P + c] = cnt.v[s];
-      a.tab_len[w * P + c] = lsum.v[s];
+    for (int c = 0; c < PB; ++c) {
+      if (c < (int)P) {
+        const uint32_t tc = (uint32_t)__builtin_amdgcn_readlane(
+            (int)wave_incl_scan_u32(rc.cnt[c]), 63);
+        const uint64_t tl = wave_sum_u40(rc.len[c]);  // (a lane's sum is below 2^37)
+        if (lane_id() == 0) {
+          a.tab_cnt[w * P + c] = tc;
+          a.tab_len[w * P + c] = tl;
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int s = 0; s < SETS; ++s) {
+      const uint32_t c = s * kWave + lane_id();
+      if (c < P) {
+        a.tab_cnt[w * P + c] = cnt.v[s];
+        a.tab_len[w * P + c] = lsum.v[s];
+      }
     }
   }
 }
 
+template <bool REG>
 __global__ __launch_bounds__(PT) void h_count(PolArgs a, int64_t ranges) {
   const int64_t w = wave_index();
-  if (w >= ranges) return;
   const uint32_t P = class_count(a);
-  if (P <= 64) hpjf_count<1>(a, w, P);
-  else hpjf_count<4>(a, w, P);
+  if (w >= ranges || REG != (P <= kRegClasses)) return;
+  if constexpr (REG) hpjf_count<kRegClasses, 1>(a, w, P);
+  else hpjf_count<0, 4>(a, w, P);
 }
 
 // Block c: exclusive scans over the ranges of class c's counts and length
@@ -358,12 +499,18 @@ __global__ __launch_bounds__(ST) void h_scan(PolArgs a, int64_t ranges) {
   }
 }
 
-template <int SETS>
+// One range of the stable scatter by rank. Every lane's element goes to
+// (running position of its class) + (rank among the round's lanes of that
+// class) with wait = (running wait of its class) + (lengths of those lanes
+// before it). PB > 0: at most PB classes, walked in an unrolled loop with
+// their running position and wait in scalar registers, class sums of the
+// waits in lane registers. PB = 0: the class loop over the ranks present,
+// running values and sums in lane tables.
+template <int PB, int SETS>
 __device__ __forceinline__ void hpjf_range(const PolArgs& a, int64_t w, uint32_t P,
-                                           LaneAcc<SETS>& acc) {
-  // running output position and wait of every class in this range: class
-  // start (exclusive scan of the class sizes / length totals) + the range's
-  // offset inside the class
+                                           PartShared& sh) {
+  // start of every class in this range: class start (exclusive scan of the
+  // class sizes / length totals) + the range's offset inside the class
   LaneTab<SETS, uint32_t> pos;
   LaneTab<SETS, uint64_t> wb;
   uint32_t carry_c = 0;
@@ -380,9 +527,23 @@ __device__ __forceinline__ void hpjf_range(const PolArgs& a, int64_t w, uint32_t
     carry_c += (uint32_t)__builtin_amdgcn_readlane((int)ic, 63);
     carry_l += readlane_u64(il, 63);
   }
+  constexpr int NB = PB == 0 ? 1 : PB;
+  uint32_t spos[NB];
+  uint64_t swb[NB];
+  if constexpr (PB > 0) {
+#pragma unroll
+    for (int c = 0; c < PB; ++c) {
+      spos[c] = (uint32_t)__builtin_amdgcn_readlane((int)pos.v[0], c);
+      swb[c] = readlane_u64(wb.v[0], c);
+    }
+  }
+  RegSums<NB> rs;
+  LaneAcc<SETS> acc;
+  rs.zero();
+  acc.zero();
   const int64_t k0 = w * kPolRange;
-  int32_t len[2][kBatch];
-  uint8_t pri[2][kBatch];
+  int32_t len[kBatch], nlen[kBatch];  // this batch, the next one
+  uint8_t pri[kBatch], npri[kBatch];
   auto load = [&](int b, int32_t* l, uint8_t* p) {
 #pragma unroll
     for (int r = 0; r < kBatch; ++r) {
@@ -391,59 +552,86 @@ __device__ __forceinline__ void hpjf_range(const PolArgs& a, int64_t w, uint32_t
       p[r] = a.priority[k];
     }
   };
-  load(0, len[0], pri[0]);
-#pragma unroll
+  load(0, len, pri);
+#pragma unroll 1
   for (int b = 0; b < kBatches; ++b) {
-    const int cur = b & 1;
-    if (b + 1 < kBatches) load(b + 1, len[cur ^ 1], pri[cur ^ 1]);
+    load(min(b + 1, kBatches - 1), nlen, npri);  // (the last batch reloads itself)
 #pragma unroll
     for (int r = 0; r < kBatch; ++r) {
       const int64_t k = k0 + (b * kBatch + r) * kWave + lane_id();
       const bool live = k < a.n;
-      const uint32_t lv = live ? (uint32_t)len[cur][r] : 0u;
+      const uint32_t lv = live ? (uint32_t)len[r] : 0u;
+      const uint32_t cls = pri[r];
       uint32_t q = 0;
       uint64_t wt = 0;
-      for_each_class((uint32_t)pri[cur][r], __ballot(live), [&](uint32_t c, uint64_t peers) {
+      auto place = [&](uint64_t peers, uint32_t pc, uint64_t wc, uint32_t& pnext,
+                       uint64_t& wnext) {
         const bool mine = in_mask(peers);
         const uint32_t mv = mine ? lv : 0u;
         const uint64_t incl = wave_incl_scan_len(mv);
-        const uint64_t excl = incl - mv;
-        const uint32_t pc = pos.get(c);
-        const uint64_t wc = wb.get(c);
         const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
             (uint32_t)(peers >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
         q = mine ? pc + rank : q;
-        wt = mine ? wc + excl : wt;
-        const uint32_t cnt = (uint32_t)__popcll(peers);
-        acc.add(c, mul_add(wc, cnt, wave_sum_u40(mine ? excl : 0)));
-        pos.add(c, cnt);
-        wb.add(c, readlane_u64(incl, 63));
-      });
+        wt = mine ? wc + (incl - mv) : wt;
+        pnext = pc + (uint32_t)__popcll(peers);
+        wnext = wc + readlane_u64(incl, 63);
+        return incl - mv;
+      };
+      const uint64_t lmask = __ballot(live);
+      if constexpr (PB > 0) {
+#pragma unroll
+        for (int c = 0; c < PB; ++c) {
+          if (c < (int)P) {
+            const uint64_t peers = __ballot(cls == (uint32_t)c) & lmask;
+            if (peers) place(peers, spos[c], swb[c], spos[c], swb[c]);
+          }
+        }
+        rs.add(cls, live ? wt : 0, P);
+      } else {
+        for_each_class(cls, lmask, [&](uint32_t c, uint64_t peers) {
+          const uint32_t pc = pos.get(c);
+          const uint64_t wc = wb.get(c);
+          uint32_t pn;
+          uint64_t wn;
+          const uint64_t excl = place(peers, pc, wc, pn, wn);
+          const uint32_t cnt = pn - pc;
+          acc.add(c, mul_add(wc, cnt, wave_sum_u40(in_mask(peers) ? excl : 0)));
+          pos.add(c, cnt);
+          wb.add(c, wn - wc);
+        });
+      }
       const bool ok = live && (int64_t)q < a.n;  // (always, for consistent counts)
       int32_t* po = ok ? a.order + q : reinterpret_cast<int32_t*>(a.sink);
       int64_t* pw = ok ? a.wait + q : reinterpret_cast<int64_t*>(a.sink + 1);
       *po = (int32_t)k;
       *pw = (int64_t)wt;
     }
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) {
+      len[r] = nlen[r];
+      pri[r] = npri[r];
+    }
   }
+  if constexpr (PB > 0) flush_sums<PB>(sh, rs, P);
+  else store_lane_acc<SETS>(acc, sh);
 }
 
-template <int SETS>
+template <int PB, int SETS>
 __device__ __forceinline__ void hpjf_scatter(const PolArgs& a, int64_t ranges, PartShared& sh,
                                              uint32_t P) {
-  LaneAcc<SETS> acc;
-  acc.zero();
   const int64_t w = wave_index();
-  if (w < ranges) hpjf_range<SETS>(a, w, P, acc);
-  store_partials<SETS>(a, acc, sh, P);
+  if (w < ranges) hpjf_range<PB, SETS>(a, w, P, sh);
+  write_partials(a, sh, P);
 }
 
+template <bool REG>
 __global__ __launch_bounds__(PT) void h_scatter(PolArgs a, int64_t ranges) {
   __shared__ PartShared sh;
-  zero_partials(sh);
   const uint32_t P = class_count(a);
-  if (P <= 64) hpjf_scatter<1>(a, ranges, sh, P);
-  else hpjf_scatter<4>(a, ranges, sh, P);
+  if (REG != (P <= kRegClasses)) return;
+  zero_partials(sh);
+  if constexpr (REG) hpjf_scatter<kRegClasses, 1>(a, ranges, sh, P);
+  else hpjf_scatter<0, 4>(a, ranges, sh, P);
 }
 
 // ---------------------------------------------------------------------------
@@ -451,9 +639,15 @@ __global__ __launch_bounds__(PT) void h_scatter(PolArgs a, int64_t ranges) {
 // position gathered through its id. Waits grow along the schedule, so each
 // round's waits are lane 0's plus a difference below 2^37.
 
-template <int SETS>
-__device__ __forceinline__ void class_range(const PolArgs& a, int64_t w, LaneAcc<SETS>& acc) {
+template <int PB, int SETS>
+__device__ __forceinline__ void class_range(const PolArgs& a, int64_t w, uint32_t P,
+                                            PartShared& sh) {
+  RegSums<PB == 0 ? 1 : PB> rs;
+  LaneAcc<SETS> acc;
+  rs.zero();
+  acc.zero();
   const int64_t k0 = w * kPolRange;
+#pragma unroll 1
   for (int b = 0; b < kBatches; ++b) {
     int32_t id[kBatch];
     uint64_t wt[kBatch];
@@ -471,31 +665,38 @@ __device__ __forceinline__ void class_range(const PolArgs& a, int64_t w, LaneAcc
     for (int r = 0; r < kBatch; ++r) {
       const int64_t k = k0 + (b * kBatch + r) * kWave + lane_id();
       const bool live = k < a.n;
-      const uint64_t w0 = readlane_u64(wt[r], 0);
-      const uint64_t d = wt[r] - w0;
-      for_each_class(p[r], __ballot(live), [&](uint32_t c, uint64_t peers) {
-        acc.add(c, mul_add(w0, (uint32_t)__popcll(peers), wave_sum_u40(in_mask(peers) ? d : 0)));
-      });
+      if constexpr (PB > 0) {
+        rs.add(p[r], live ? wt[r] : 0, P);
+      } else {
+        const uint64_t w0 = readlane_u64(wt[r], 0);
+        const uint64_t d = wt[r] - w0;
+        for_each_class(p[r], __ballot(live), [&](uint32_t c, uint64_t peers) {
+          acc.add(c, mul_add(w0, (uint32_t)__popcll(peers),
+                             wave_sum_u40(in_mask(peers) ? d : 0)));
+        });
+      }
     }
   }
+  if constexpr (PB > 0) flush_sums<PB>(sh, rs, P);
+  else store_lane_acc<SETS>(acc, sh);
 }
 
-template <int SETS>
+template <int PB, int SETS>
 __device__ __forceinline__ void class_sums(const PolArgs& a, int64_t ranges, PartShared& sh,
                                            uint32_t P) {
-  LaneAcc<SETS> acc;
-  acc.zero();
   const int64_t w = wave_index();
-  if (w < ranges) class_range<SETS>(a, w, acc);
-  store_partials<SETS>(a, acc, sh, P);
+  if (w < ranges) class_range<PB, SETS>(a, w, P, sh);
+  write_partials(a, sh, P);
 }
 
+template <bool REG>
 __global__ __launch_bounds__(PT) void s_classes(PolArgs a, int64_t ranges) {
   __shared__ PartShared sh;
-  zero_partials(sh);
   const uint32_t P = class_count(a);
-  if (P <= 64) class_sums<1>(a, ranges, sh, P);
-  else class_sums<4>(a, ranges, sh, P);
+  if (REG != (P <= kRegClasses)) return;
+  zero_partials(sh);
+  if constexpr (REG) class_sums<kRegClasses, 1>(a, ranges, sh, P);
+  else class_sums<0, 4>(a, ranges, sh, P);
 }
 
 // Block c: class c's total from the blocks' partial sums; added to the grand
@@ -526,7 +727,7 @@ int64_t ranges_of(int64_t n) { return (n + kPolRange - 1) / kPolRange; }
 int64_t blocks_of(int64_t n) { return (ranges_of(n) + kWaves - 1) / kWaves; }
 
 hipError_t launch_p_range(const PolArgs& a, hipStream_t st) {
-  const int64_t g = std::min<int64_t>((a.n + PT * 16 - 1) / (PT * 16), 2048);
+  const int64_t g = std::min<int64_t>((a.n + PT * 64 - 1) / (PT * 64), 4096);
   hipLaunchKernelGGL(p_range, dim3((unsigned)std::max<int64_t>(g, 1)), dim3(PT), 0, st, a);
   return hipGetLastError();
 }
@@ -542,11 +743,11 @@ int64_t policy_blocks(int64_t n) { return blocks_of(n); }
 
 hipError_t launch_fcfs(const PolArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after) {
   const int64_t ranges = ranges_of(a.n), blocks = blocks_of(a.n);
-  if (launch_p_range(a, st) != hipSuccess) return hipGetLastError();
   hipLaunchKernelGGL(f_sums, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
   hipLaunchKernelGGL(f_scan, dim3(1), dim3(ST), 0, st, a, ranges);
   mark(before, st);
-  hipLaunchKernelGGL(f_write, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(f_write<true>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(f_write<false>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
   mark(after, st);
   hipLaunchKernelGGL(p_total, dim3(256), dim3(PT), 0, st, a, blocks);
   return hipGetLastError();
@@ -555,10 +756,12 @@ hipError_t launch_fcfs(const PolArgs& a, hipStream_t st, hipEvent_t before, hipE
 hipError_t launch_hpjf(const PolArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after) {
   const int64_t ranges = ranges_of(a.n), blocks = blocks_of(a.n);
   if (launch_p_range(a, st) != hipSuccess) return hipGetLastError();
-  hipLaunchKernelGGL(h_count, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(h_count<true>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(h_count<false>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
   hipLaunchKernelGGL(h_scan, dim3(256), dim3(ST), 0, st, a, ranges);
   mark(before, st);
-  hipLaunchKernelGGL(h_scatter, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(h_scatter<true>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(h_scatter<false>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
   mark(after, st);
   hipLaunchKernelGGL(p_total, dim3(256), dim3(PT), 0, st, a, blocks);
   return hipGetLastError();
@@ -569,7 +772,8 @@ hipError_t launch_class_totals(const PolArgs& a, hipStream_t st, hipEvent_t befo
   const int64_t ranges = ranges_of(a.n), blocks = blocks_of(a.n);
   if (launch_p_range(a, st) != hipSuccess) return hipGetLastError();
   mark(before, st);
-  hipLaunchKernelGGL(s_classes, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(s_classes<true>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
+  hipLaunchKernelGGL(s_classes<false>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
   mark(after, st);
   hipLaunchKernelGGL(p_total, dim3(256), dim3(PT), 0, st, a, blocks);
   return hipGetLastError();
