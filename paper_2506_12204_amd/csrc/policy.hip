@@ -293,28 +293,49 @@ __global__ __launch_bounds__(PT) void f_sums(PolArgs a, int64_t ranges) {
   if (lane_id() == 0) a.rsum[w] = s;
 }
 
-// Exclusive scan of `count` u64 values in place (one block; each thread
-// scans a contiguous chunk). Writes the grand total to *total if non-null.
-__device__ __forceinline__ void chunk_scan_u64(uint64_t* v, int64_t count, int64_t stride,
-                                               uint64_t* total, uint64_t* scratch) {
+// Exclusive scan in place of `count` contiguous values (one block; thread t
+// scans the t-th chunk of ceil(count / ST) values). Chunks of up to kChunk
+// values are loaded in one unrolled batch. Returns the total to every thread.
+constexpr int kChunk = 16;
+
+template <typename T>
+__device__ __forceinline__ T chunk_scan(T* v, int64_t count, T* scratch) {
   const int t = threadIdx.x;
   const int64_t per = (count + ST - 1) / ST;
   const int64_t lo = min(count, t * per), hi = min(count, lo + per);
-  uint64_t s = 0;
-  for (int64_t i = lo; i < hi; ++i) s += v[i * stride];
-  uint64_t tot;
-  uint64_t run = block_excl_scan_u64<ST>(s, scratch, tot);
-  for (int64_t i = lo; i < hi; ++i) {
-    const uint64_t x = v[i * stride];
-    v[i * stride] = run;
-    run += x;
+  T x[kChunk];
+  T s = 0;
+  if (per <= kChunk) {
+#pragma unroll
+    for (int i = 0; i < kChunk; ++i) x[i] = lo + i < hi ? v[lo + i] : (T)0;
+#pragma unroll
+    for (int i = 0; i < kChunk; ++i) s += x[i];
+  } else {
+    for (int64_t i = lo; i < hi; ++i) s += v[i];
   }
-  if (total && t == 0) *total = tot;
+  T tot;
+  T run;
+  if constexpr (sizeof(T) == 8) run = block_excl_scan_u64<ST>(s, scratch, tot);
+  else run = block_excl_scan_u32<ST>(s, scratch, tot);
+  if (per <= kChunk) {
+#pragma unroll
+    for (int i = 0; i < kChunk; ++i) {
+      if (lo + i < hi) v[lo + i] = run;
+      run += x[i];
+    }
+  } else {
+    for (int64_t i = lo; i < hi; ++i) {
+      const T y = v[i];
+      v[i] = run;
+      run += y;
+    }
+  }
+  return tot;
 }
 
 __global__ __launch_bounds__(ST) void f_scan(PolArgs a, int64_t ranges) {
   __shared__ uint64_t scratch[ST / kWave + 1];
-  chunk_scan_u64(a.rsum, ranges, 1, nullptr, scratch);
+  chunk_scan<uint64_t>(a.rsum, ranges, scratch);
 }
 
 // FCFS: order[k] = k, wait[k] = offset of the range + prefix inside it.
@@ -400,7 +421,8 @@ __global__ __launch_bounds__(PT) void f_write(PolArgs a, int64_t ranges) {
 // Per-class counts and length sums of one range: in registers (PB > 0) or by
 // the class loop into lane tables of SETS sets.
 template <int PB, int SETS>
-__device__ __forceinline__ void hpjf_count(const PolArgs& a, int64_t w, uint32_t P) {
+__device__ __forceinline__ void hpjf_count(const PolArgs& a, int64_t w, int64_t ranges,
+                                           uint32_t P) {
   RegCounts<PB == 0 ? 1 : PB> rc;
   LaneTab<SETS, uint32_t> cnt;
   LaneTab<SETS, uint64_t> lsum;
@@ -438,8 +460,8 @@ __device__ __forceinline__ void hpjf_count(const PolArgs& a, int64_t w, uint32_t
             (int)wave_incl_scan_u32(rc.cnt[c]), 63);
         const uint64_t tl = wave_sum_u40(rc.len[c]);  // (a lane's sum is below 2^37)
         if (lane_id() == 0) {
-          a.tab_cnt[w * P + c] = tc;
-          a.tab_len[w * P + c] = tl;
+          a.tab_cnt[c * ranges + w] = tc;
+          a.tab_len[c * ranges + w] = tl;
         }
       }
     }
@@ -448,8 +470,8 @@ __device__ __forceinline__ void hpjf_count(const PolArgs& a, int64_t w, uint32_t
     for (int s = 0; s < SETS; ++s) {
       const uint32_t c = s * kWave + lane_id();
       if (c < P) {
-        a.tab_cnt[w * P + c] = cnt.v[s];
-        a.tab_len[w * P + c] = lsum.v[s];
+        a.tab_cnt[c * ranges + w] = cnt.v[s];
+        a.tab_len[c * ranges + w] = lsum.v[s];
       }
     }
   }
@@ -460,40 +482,22 @@ __global__ __launch_bounds__(PT) void h_count(PolArgs a, int64_t ranges) {
   const int64_t w = wave_index();
   const uint32_t P = class_count(a);
   if (w >= ranges || REG != (P <= kRegClasses)) return;
-  if constexpr (REG) hpjf_count<kRegClasses, 1>(a, w, P);
-  else hpjf_count<0, 4>(a, w, P);
+  if constexpr (REG) hpjf_count<kRegClasses, 1>(a, w, ranges, P);
+  else hpjf_count<0, 4>(a, w, ranges, P);
 }
 
 // Block c: exclusive scans over the ranges of class c's counts and length
-// sums (in place); the class's size and length total.
+// sums (in place; the tables are class-major); the class's size and length
+// total.
 __global__ __launch_bounds__(ST) void h_scan(PolArgs a, int64_t ranges) {
   __shared__ uint32_t s32[ST / kWave + 1];
   __shared__ uint64_t s64[ST / kWave + 1];
   const uint32_t P = class_count(a);
   const uint32_t c = blockIdx.x;
   if (c >= P) return;
-  const int t = threadIdx.x;
-  const int64_t per = (ranges + ST - 1) / ST;
-  const int64_t lo = min(ranges, t * per), hi = min(ranges, lo + per);
-  uint32_t sc = 0;
-  uint64_t sl = 0;
-  for (int64_t i = lo; i < hi; ++i) {
-    sc += a.tab_cnt[i * P + c];
-    sl += a.tab_len[i * P + c];
-  }
-  uint32_t tc;
-  uint64_t tl;
-  uint32_t rc = block_excl_scan_u32<ST>(sc, s32, tc);
-  uint64_t rl = block_excl_scan_u64<ST>(sl, s64, tl);
-  for (int64_t i = lo; i < hi; ++i) {
-    const uint32_t x = a.tab_cnt[i * P + c];
-    const uint64_t y = a.tab_len[i * P + c];
-    a.tab_cnt[i * P + c] = rc;
-    a.tab_len[i * P + c] = rl;
-    rc += x;
-    rl += y;
-  }
-  if (t == 0) {
+  const uint32_t tc = chunk_scan<uint32_t>(a.tab_cnt + (int64_t)c * ranges, ranges, s32);
+  const uint64_t tl = chunk_scan<uint64_t>(a.tab_len + (int64_t)c * ranges, ranges, s64);
+  if (threadIdx.x == 0) {
     a.ctot_cnt[c] = tc;
     a.ctot_len[c] = tl;
   }
@@ -507,8 +511,8 @@ __global__ __launch_bounds__(ST) void h_scan(PolArgs a, int64_t ranges) {
 // waits in lane registers. PB = 0: the class loop over the ranks present,
 // running values and sums in lane tables.
 template <int PB, int SETS>
-__device__ __forceinline__ void hpjf_range(const PolArgs& a, int64_t w, uint32_t P,
-                                           PartShared& sh) {
+__device__ __forceinline__ void hpjf_range(const PolArgs& a, int64_t w, int64_t ranges,
+                                           uint32_t P, PartShared& sh) {
   // start of every class in this range: class start (exclusive scan of the
   // class sizes / length totals) + the range's offset inside the class
   LaneTab<SETS, uint32_t> pos;
@@ -522,8 +526,8 @@ __device__ __forceinline__ void hpjf_range(const PolArgs& a, int64_t w, uint32_t
     const uint64_t cl = c < P ? a.ctot_len[c] : 0u;
     const uint32_t ic = wave_incl_scan_u32(cc);
     const uint64_t il = wave_incl_scan_u64(cl);
-    pos.v[s] = carry_c + ic - cc + (c < P ? a.tab_cnt[w * P + c] : 0u);
-    wb.v[s] = carry_l + il - cl + (c < P ? a.tab_len[w * P + c] : 0u);
+    pos.v[s] = carry_c + ic - cc + (c < P ? a.tab_cnt[c * ranges + w] : 0u);
+    wb.v[s] = carry_l + il - cl + (c < P ? a.tab_len[c * ranges + w] : 0u);
     carry_c += (uint32_t)__builtin_amdgcn_readlane((int)ic, 63);
     carry_l += readlane_u64(il, 63);
   }
@@ -620,7 +624,7 @@ template <int PB, int SETS>
 __device__ __forceinline__ void hpjf_scatter(const PolArgs& a, int64_t ranges, PartShared& sh,
                                              uint32_t P) {
   const int64_t w = wave_index();
-  if (w < ranges) hpjf_range<PB, SETS>(a, w, P, sh);
+  if (w < ranges) hpjf_range<PB, SETS>(a, w, ranges, P, sh);
   write_partials(a, sh, P);
 }
 
