@@ -5,6 +5,8 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 and shares no code with it.
 
 * ``semsched_oracle``: the pure-Python oracle (the plain definition).
+* ``cost_oracle``: the cost model of Section 3.4 (service times, the cache
+  and recompute decisions of an eviction) in exact integers.
 * ``c_oracle_*``: ctypes wrappers of ``oracle.c``, the same definition in
   plain C for large queues and for the timed CPU baseline.
 """
@@ -17,6 +19,14 @@ import subprocess
 
 import numpy as np
 
+from .cost_oracle import (  # noqa: F401
+    CostModel,
+    evict_plan,
+    keep_prefill_cache,
+    schedule_cost,
+    service_times,
+    tokens_to_save,
+)
 from .semsched_oracle import (  # noqa: F401
     MAX_CLASSES,
     POLICIES,
@@ -66,6 +76,10 @@ def _load():
     lib.oracle_schedule_batched.restype = ctypes.c_int
     lib.oracle_schedule_policy.argtypes = [ctypes.c_int, vp, vp, i64, vp, vp, vp, vp]
     lib.oracle_schedule_policy.restype = ctypes.c_int
+    lib.oracle_service_times.argtypes = [vp, vp, vp, i64, vp, vp]
+    lib.oracle_service_times.restype = ctypes.c_int
+    lib.oracle_evict_plan.argtypes = [vp, vp, i64, vp, vp, vp]
+    lib.oracle_evict_plan.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -112,6 +126,44 @@ def c_oracle_policy(p: np.ndarray, l: np.ndarray, policy: int):
     if rc != ORACLE_OK:
         raise ValueError(f"oracle_schedule_policy failed: {rc}")
     return order, wait, _join128(lo, hi)
+
+
+def _coeffs(cm) -> np.ndarray:
+    return np.array([cm.alpha1, cm.alpha2, cm.beta, cm.gamma1, cm.gamma2], dtype=np.uint64)
+
+
+def c_oracle_service_times(prompt, output, decoded, cm) -> np.ndarray:
+    """``service_times`` through oracle.c (int32 array)."""
+    prompt = np.ascontiguousarray(prompt, dtype=np.int32)
+    output = np.ascontiguousarray(output, dtype=np.int32)
+    dec = None if decoded is None else np.ascontiguousarray(decoded, dtype=np.int32)
+    n = prompt.shape[0]
+    out = np.empty(n, np.int32)
+    c = _coeffs(cm)
+    rc = _load().oracle_service_times(_ptr(prompt), _ptr(output),
+                                      ctypes.c_void_p(0) if dec is None else _ptr(dec), n,
+                                      _ptr(c), _ptr(out))
+    if rc == ORACLE_ERANGE:
+        raise OracleRangeError("negative token count")
+    if rc != ORACLE_OK:
+        raise ValueError(f"oracle_service_times failed: {rc}")
+    return out
+
+
+def c_oracle_evict_plan(prompt, decoded, cm):
+    """``evict_plan`` through oracle.c: (keep uint8, save int32)."""
+    prompt = np.ascontiguousarray(prompt, dtype=np.int32)
+    dec = np.ascontiguousarray(decoded, dtype=np.int32)
+    n = prompt.shape[0]
+    keep = np.empty(n, np.uint8)
+    save = np.empty(n, np.int32)
+    c = _coeffs(cm)
+    rc = _load().oracle_evict_plan(_ptr(prompt), _ptr(dec), n, _ptr(c), _ptr(keep), _ptr(save))
+    if rc == ORACLE_ERANGE:
+        raise OracleRangeError("negative token count")
+    if rc != ORACLE_OK:
+        raise ValueError(f"oracle_evict_plan failed: {rc}")
+    return keep, save
 
 
 def c_oracle_batched(p: np.ndarray, l: np.ndarray, offsets: np.ndarray,
