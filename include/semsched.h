@@ -215,6 +215,75 @@ int sem_schedule_policy_async(int policy, const uint8_t *priority, const int32_t
                               sem_i128 *totals_out, void *workspace, size_t ws_bytes,
                               void *stream);
 
+/*
+ * Cost model of Section 3.4. Constants are unsigned Q32.32 fixed point: a
+ * value v means v / 2^32 time units (the caller's unit, e.g. microseconds)
+ * per token (alpha2, beta, gamma1, gamma2) or per token^2 (alpha1):
+ *   prefill of n prompt tokens:     alpha1 * n^2 + alpha2 * n
+ *   reloading n tokens of KV cache: beta * n
+ *   decoding tokens n+1 .. n+m:     gamma1 * (m^2/2 + n*m + m/2) + gamma2 * m  (Eq. 4)
+ * Every product and sum is exact (128-bit); results are deterministic integers.
+ */
+typedef struct {
+  uint64_t alpha1, alpha2, beta, gamma1, gamma2;
+} sem_cost_model;
+
+/*
+ * Remaining computation time of each request (blocking), the f_t of the
+ * scheduling tuple: for prompt[i] tokens, output[i] predicted output tokens
+ * and decoded[i] tokens decoded so far (decoded may be NULL: all 0), the
+ * cost of decoding tokens prompt+decoded+1 .. prompt+output (none once
+ * decoded >= output) plus the prefill while decoded = 0, as
+ * floor(cost / 2^32) time units, saturated at 2^31 - 1.
+ *   prompt, output, decoded [n] int32 DEVICE; model HOST pointer;
+ *   service_out [n] int32 DEVICE.
+ * Errors: SEM_EINVAL (n < 0 or > INT32_MAX, null pointers), SEM_ERANGE (a
+ * negative count; that request's service time is written as 0).
+ */
+int sem_service_times(const int32_t *prompt, const int32_t *output, const int32_t *decoded,
+                      int64_t n, const sem_cost_model *model, int32_t *service_out);
+
+/*
+ * Cache decisions for n evicted requests (blocking; Algorithm 4's
+ * ShouldRecompute and the decode-stage split of Section 3.4):
+ *   keep_prefill_out[i] = 1 when reloading the prompt's cache is cheaper
+ *     than recomputing it: beta * p < alpha1 * p^2 + alpha2 * p for
+ *     p = prompt[i] (Eq. 3 with the comparison its explanation implies);
+ *   save_tokens_out[i] = the number x in [0, decoded[i]] of decoded tokens
+ *     whose cache to save that minimises Eq. 5,
+ *     beta * x + gamma1 * (y^2/2 + p*y + y/2) + gamma2 * y with y = decoded - x,
+ *     the largest such x among equal costs (exact integer minimiser).
+ *   prompt, decoded [n] int32 DEVICE; keep_prefill_out [n] uint8 and
+ *   save_tokens_out [n] int32 DEVICE. Errors as sem_service_times.
+ */
+int sem_evict_plan(const int32_t *prompt, const int32_t *decoded, int64_t n,
+                   const sem_cost_model *model, uint8_t *keep_prefill_out,
+                   int32_t *save_tokens_out);
+
+/*
+ * Schedule one queue by (priority, cost-model service time, id) (blocking):
+ * sem_service_times followed by sem_schedule on those times. service_out
+ * ([n] int32 DEVICE) receives the service times when not NULL. Outputs and
+ * errors as sem_schedule and sem_service_times.
+ */
+int sem_schedule_cost(const uint8_t *priority, const int32_t *prompt, const int32_t *output,
+                      const int32_t *decoded, int64_t n, const sem_cost_model *model,
+                      int32_t *order_out, int64_t *wait_out, sem_i128 *totals_out,
+                      int32_t *service_out);
+
+/* Workspace size in bytes of sem_schedule_cost_async for n requests. */
+size_t sem_cost_workspace_bytes(int64_t n);
+
+/* Asynchronous sem_schedule_cost: a caller-owned DEVICE workspace of at least
+ * sem_cost_workspace_bytes(n) bytes (256-byte aligned) and the stream;
+ * allocates nothing, does not synchronise; range errors are returned by
+ * sem_check(workspace, stream). */
+int sem_schedule_cost_async(const uint8_t *priority, const int32_t *prompt,
+                            const int32_t *output, const int32_t *decoded, int64_t n,
+                            const sem_cost_model *model, int32_t *order_out,
+                            int64_t *wait_out, sem_i128 *totals_out, int32_t *service_out,
+                            void *workspace, size_t ws_bytes, void *stream);
+
 /* Stream used by the blocking calls (NULL = null stream). */
 int sem_set_stream(void *stream);
 
@@ -240,7 +309,8 @@ const char *sem_strerror(int code);
  *                           moves the earlier entries and places the arrivals),
  *          SEM_STAGE_POLICY (sem_schedule_policy*: for FCFS and HPJF the pass
  *                           that writes order and waits, for SJF the pass
- *                           that sums the waits per class).
+ *                           that sums the waits per class),
+ *          SEM_STAGE_COST  (sem_schedule_cost*: the service-time pass).
  * Passing NULL events disarms the stage. Returns SEM_EINVAL for an unknown
  * stage. The events are owned by the caller and must outlive the call.
  */
@@ -249,6 +319,7 @@ const char *sem_strerror(int code);
 #define SEM_STAGE_FINAL 2
 #define SEM_STAGE_MERGE 3
 #define SEM_STAGE_POLICY 4
+#define SEM_STAGE_COST 5
 int sem_trace_stage(int stage, void *before, void *after);
 
 #ifdef __cplusplus

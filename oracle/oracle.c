@@ -169,8 +169,16 @@ int oracle_schedule_batched(const uint8_t *pri, const int32_t *len,
  */
 typedef unsigned __int128 u128;
 
-static u128 decode_cost_q(const uint64_t *c, u128 n, u128 m) {
-  return (u128)c[3] * ((m * m + m) / 2 + n * m) + (u128)c[4] * m;
+/* a + b, setting *over when the sum passes 2^128 (the service time then
+ * saturates). */
+static u128 add_q(u128 a, u128 b, int *over) {
+  const u128 s = a + b;
+  if (s < a) *over = 1;
+  return s;
+}
+
+static u128 decode_cost_q(const uint64_t *c, u128 n, u128 m, int *over) {
+  return add_q((u128)c[3] * ((m * m + m) / 2 + n * m), (u128)c[4] * m, over);
 }
 
 int oracle_service_times(const int32_t *prompt, const int32_t *output,
@@ -181,10 +189,14 @@ int oracle_service_times(const int32_t *prompt, const int32_t *output,
     const int64_t a = prompt[i], m = output[i], d = decoded ? decoded[i] : 0;
     if (a < 0 || m < 0 || d < 0) return ORACLE_ERANGE;
     const int64_t r = m > d ? m - d : 0;
-    u128 cost = decode_cost_q(c, (u128)(a + d), (u128)r);
-    if (d == 0) cost += (u128)c[0] * (u128)a * (u128)a + (u128)c[1] * (u128)a;
+    int over = 0;
+    u128 cost = decode_cost_q(c, (u128)(a + d), (u128)r, &over);
+    if (d == 0) {
+      cost = add_q(cost, (u128)c[0] * (u128)a * (u128)a, &over);
+      cost = add_q(cost, (u128)c[1] * (u128)a, &over);
+    }
     const u128 s = cost >> 32;
-    out[i] = s > (u128)INT32_MAX ? INT32_MAX : (int32_t)s;
+    out[i] = (over || s > (u128)INT32_MAX) ? INT32_MAX : (int32_t)s;
   }
   return ORACLE_OK;
 }
@@ -196,8 +208,9 @@ int oracle_evict_plan(const int32_t *prompt, const int32_t *decoded, int64_t n,
     const int64_t a = prompt[i], mp = decoded[i];
     if (a < 0 || mp < 0) return ORACLE_ERANGE;
     const u128 reload = (u128)c[2] * (u128)a;
-    const u128 recompute = (u128)c[0] * (u128)a * (u128)a + (u128)c[1] * (u128)a;
-    keep[i] = reload < recompute ? 1 : 0;
+    int over = 0;
+    const u128 recompute = add_q((u128)c[0] * (u128)a * (u128)a, (u128)c[1] * (u128)a, &over);
+    keep[i] = (over || reload < recompute) ? 1 : 0;
     /* first y whose next recomputed token does not pay: gamma1*(y+1+n)+gamma2 >= beta */
     int64_t y = 0;
     while (y < mp && (u128)c[3] * (u128)(y + 1 + a) + (u128)c[4] < (u128)c[2]) ++y;

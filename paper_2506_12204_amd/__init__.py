@@ -49,10 +49,28 @@ SYMBOLS = (
     "sem_schedule_policy",
     "sem_policy_workspace_bytes",
     "sem_schedule_policy_async",
+    "sem_service_times",
+    "sem_evict_plan",
+    "sem_schedule_cost",
+    "sem_cost_workspace_bytes",
+    "sem_schedule_cost_async",
 )
-STAGE_HIST, STAGE_FIRST, STAGE_FINAL, STAGE_MERGE, STAGE_POLICY = 0, 1, 2, 3, 4
+STAGE_HIST, STAGE_FIRST, STAGE_FINAL, STAGE_MERGE, STAGE_POLICY, STAGE_COST = 0, 1, 2, 3, 4, 5
 # comparison policies (Section 4): the key fields before the id
 POLICY_SEMANTIC, POLICY_FCFS, POLICY_SJF, POLICY_HPJF = 0, 1, 2, 3
+
+
+class CostModelC(ctypes.Structure):
+    """sem_cost_model: Q32.32 constants (time unit x 2^32 per token, per token^2
+    for alpha1)."""
+    _fields_ = [(name, ctypes.c_uint64)
+                for name in ("alpha1", "alpha2", "beta", "gamma1", "gamma2")]
+
+
+def cost_model(model) -> CostModelC:
+    """Any object with integer attributes alpha1, alpha2, beta, gamma1, gamma2."""
+    return CostModelC(*(int(getattr(model, k)) for k in ("alpha1", "alpha2", "beta",
+                                                          "gamma1", "gamma2")))
 
 
 class SemschedError(RuntimeError):
@@ -92,11 +110,20 @@ def _load() -> ctypes.CDLL:
     lib.sem_policy_workspace_bytes.argtypes = [ctypes.c_int, i64]
     lib.sem_policy_workspace_bytes.restype = sz
     lib.sem_schedule_policy_async.argtypes = [ctypes.c_int, vp, vp, i64, vp, vp, vp, vp, sz, vp]
+    cm = ctypes.POINTER(CostModelC)
+    lib.sem_service_times.argtypes = [vp, vp, vp, i64, cm, vp]
+    lib.sem_evict_plan.argtypes = [vp, vp, i64, cm, vp, vp]
+    lib.sem_schedule_cost.argtypes = [vp, vp, vp, vp, i64, cm, vp, vp, vp, vp]
+    lib.sem_cost_workspace_bytes.argtypes = [i64]
+    lib.sem_cost_workspace_bytes.restype = sz
+    lib.sem_schedule_cost_async.argtypes = [vp, vp, vp, vp, i64, cm, vp, vp, vp, vp, vp, sz, vp]
     lib.sem_strerror.argtypes = [ctypes.c_int]
     lib.sem_strerror.restype = ctypes.c_char_p
     for name in ("sem_schedule", "sem_schedule_batched", "sem_schedule_async",
                  "sem_schedule_batched_async", "sem_set_stream", "sem_check", "sem_insert",
-                 "sem_insert_async", "sem_schedule_policy", "sem_schedule_policy_async"):
+                 "sem_insert_async", "sem_schedule_policy", "sem_schedule_policy_async",
+                 "sem_service_times", "sem_evict_plan", "sem_schedule_cost",
+                 "sem_schedule_cost_async"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -319,3 +346,84 @@ def schedule_policy(priority: torch.Tensor, length: torch.Tensor, policy: int
     s.run(priority, length)
     s.check()
     return s.order, s.wait, totals_to_ints(s.totals)
+
+
+def _check_counts(*arrays: Optional[torch.Tensor]) -> int:
+    ref = next(a for a in arrays if a is not None)
+    for a in arrays:
+        if a is None:
+            continue
+        if a.dtype != torch.int32 or a.device != ref.device or a.device.type != "cuda":
+            raise TypeError("token counts must be int32 tensors on one GPU")
+        if a.dim() != 1 or a.numel() != ref.numel() or not a.is_contiguous():
+            raise ValueError("token counts must be contiguous 1-D tensors of one size")
+    return ref.numel()
+
+
+def service_times(prompt: torch.Tensor, output: torch.Tensor, decoded: Optional[torch.Tensor],
+                  model) -> torch.Tensor:
+    """Remaining computation time of every request under the cost model (int32)."""
+    n = _check_counts(prompt, output, decoded)
+    out = torch.empty(n, dtype=torch.int32, device=prompt.device)
+    lib.sem_set_stream(_stream_handle(prompt.device))
+    cm = cost_model(model)
+    _raise(lib.sem_service_times(_ptr(prompt), _ptr(output), _ptr(decoded), n, ctypes.byref(cm),
+                                 _ptr(out)), "sem_service_times")
+    return out
+
+
+def evict_plan(prompt: torch.Tensor, decoded: torch.Tensor, model
+               ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Per evicted request: keep its prefill cache (uint8 0/1) and how many of
+    its decoded tokens' cache to save (int32)."""
+    n = _check_counts(prompt, decoded)
+    keep = torch.empty(n, dtype=torch.uint8, device=prompt.device)
+    save = torch.empty(n, dtype=torch.int32, device=prompt.device)
+    lib.sem_set_stream(_stream_handle(prompt.device))
+    cm = cost_model(model)
+    _raise(lib.sem_evict_plan(_ptr(prompt), _ptr(decoded), n, ctypes.byref(cm), _ptr(keep),
+                              _ptr(save)), "sem_evict_plan")
+    return keep, save
+
+
+class CostScheduler:
+    """Reusable schedule of n requests by (priority, cost-model service time,
+    id); ``run`` enqueues sem_schedule_cost_async on the current stream and
+    leaves the service times in ``service``."""
+
+    def __init__(self, n: int, model, device="cuda"):
+        self.n = int(n)
+        self.device = torch.device(device)
+        self.model = cost_model(model)
+        self.order = torch.empty(self.n, dtype=torch.int32, device=self.device)
+        self.wait = torch.empty(self.n, dtype=torch.int64, device=self.device)
+        self.service = torch.empty(self.n, dtype=torch.int32, device=self.device)
+        self.totals = torch.empty((1 + MAX_CLASSES, 2), dtype=torch.int64, device=self.device)
+        self.ws_bytes = int(lib.sem_cost_workspace_bytes(self.n))
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+
+    def run(self, priority: torch.Tensor, prompt: torch.Tensor, output: torch.Tensor,
+            decoded: Optional[torch.Tensor] = None) -> None:
+        if priority.dtype != torch.uint8 or priority.numel() != self.n:
+            raise TypeError("priority must be uint8 with n entries")
+        if _check_counts(prompt, output, decoded) != self.n:
+            raise ValueError("size differs from the CostScheduler's n")
+        rc = lib.sem_schedule_cost_async(_ptr(priority), _ptr(prompt), _ptr(output),
+                                         _ptr(decoded), self.n, ctypes.byref(self.model),
+                                         _ptr(self.order), _ptr(self.wait), _ptr(self.totals),
+                                         _ptr(self.service), _ptr(self.workspace), self.ws_bytes,
+                                         _stream_handle(self.device))
+        _raise(rc, "sem_schedule_cost_async")
+
+    def check(self) -> None:
+        _raise(lib.sem_check(_ptr(self.workspace), _stream_handle(self.device)), "sem_check")
+
+
+def schedule_cost(priority: torch.Tensor, prompt: torch.Tensor, output: torch.Tensor,
+                  decoded: Optional[torch.Tensor], model):
+    """Schedule by (priority, service time, id); returns (order, wait,
+    totals[257] ints, service times)."""
+    s = CostScheduler(priority.numel(), model, priority.device)
+    s.run(priority, prompt, output, decoded)
+    s.check()
+    return s.order, s.wait, totals_to_ints(s.totals), s.service

@@ -372,6 +372,71 @@ bool known_policy(int policy) {
 int check_queue_args(const uint8_t* p, const int32_t* l, int64_t n, int32_t* order,
                      int64_t* wait, sem_i128* totals);
 
+// Workspace of a cost-model schedule: the queue workspace (error flags at
+// offset 0), the cost pass's own error word, the service times.
+struct CostLayout {
+  size_t cflags = 0, service = 0, total = 0;
+};
+
+CostLayout cost_layout(int64_t n) {
+  CostLayout L;
+  size_t off = align_up(layout_for(n).total);
+  L.cflags = off;
+  off = align_up(off + 4);
+  L.service = off;
+  off = align_up(off + 4 * (size_t)std::max<int64_t>(n, 1));
+  L.total = off;
+  return L;
+}
+
+CostArgs cost_args(const int32_t* prompt, const int32_t* output, const int32_t* decoded,
+                   int64_t n, const sem_cost_model* m) {
+  CostArgs a = {};
+  a.prompt = prompt;
+  a.output = output;
+  a.decoded = decoded;
+  a.n = n;
+  a.alpha1 = m->alpha1;
+  a.alpha2 = m->alpha2;
+  a.beta = m->beta;
+  a.gamma1 = m->gamma1;
+  a.gamma2 = m->gamma2;
+  return a;
+}
+
+int check_cost_args(const int32_t* prompt, const int32_t* output, int64_t n,
+                    const sem_cost_model* model, const void* out) {
+  if (n < 0 || n > INT32_MAX || !model) return SEM_EINVAL;
+  if (n > 0 && (!prompt || !output || !out)) return SEM_EINVAL;
+  return SEM_OK;
+}
+
+int enqueue_cost_schedule(const uint8_t* p, const int32_t* prompt, const int32_t* output,
+                          const int32_t* decoded, int64_t n, const sem_cost_model* model,
+                          int32_t* order, int64_t* wait, sem_i128* totals, int32_t* service,
+                          void* ws, hipStream_t st) {
+  char* base = static_cast<char*>(ws);
+  const CostLayout L = cost_layout(n);
+  uint32_t* cflags = reinterpret_cast<uint32_t*>(base + L.cflags);
+  CostArgs a = cost_args(prompt, output, decoded, n, model);
+  a.service = service ? service : reinterpret_cast<int32_t*>(base + L.service);
+  a.flags = cflags;
+  if (launch_fill_zero(cflags, 1, st) != hipSuccess) return SEM_EDEVICE;
+  hipEvent_t before = nullptr, after = nullptr;
+  {
+    std::lock_guard<std::mutex> guard(trace_mu());
+    before = trace_slots().before[SEM_STAGE_COST];
+    after = trace_slots().after[SEM_STAGE_COST];
+    trace_slots().before[SEM_STAGE_COST] = trace_slots().after[SEM_STAGE_COST] = nullptr;
+  }
+  if (launch_service(a, st, before, after) != hipSuccess) return SEM_EDEVICE;
+  const int rc = enqueue_queue(p, a.service, n, SEM_MAX_CLASSES, order, wait, totals, ws, st);
+  if (rc != SEM_OK) return rc;
+  return launch_merge_flags(reinterpret_cast<uint32_t*>(base), cflags, st) == hipSuccess
+             ? SEM_OK
+             : SEM_EDEVICE;
+}
+
 int enqueue_policy(int policy, const uint8_t* p, const int32_t* l, int64_t n, int32_t* order,
                    int64_t* wait, sem_i128* totals, void* ws, hipStream_t st) {
   if (policy == SEM_POLICY_SEMANTIC)
@@ -479,7 +544,7 @@ const char* sem_strerror(int code) {
 }
 
 int sem_trace_stage(int stage, void* before, void* after) {
-  if (stage < SEM_STAGE_HIST || stage > SEM_STAGE_POLICY) return SEM_EINVAL;
+  if (stage < SEM_STAGE_HIST || stage > SEM_STAGE_COST) return SEM_EINVAL;
   std::lock_guard<std::mutex> guard(trace_mu());
   trace_slots().before[stage] = static_cast<hipEvent_t>(before);
   trace_slots().after[stage] = static_cast<hipEvent_t>(after);
@@ -582,6 +647,85 @@ int sem_schedule_policy(int policy, const uint8_t* priority, const int32_t* leng
   if (rc != SEM_OK) return rc;
   const hipStream_t st = state().stream;
   rc = enqueue_policy(policy, priority, length, n, order_out, wait_out, totals_out, ws, st);
+  if (rc != SEM_OK) return rc;
+  return finish(ws, st);
+}
+
+int sem_service_times(const int32_t* prompt, const int32_t* output, const int32_t* decoded,
+                      int64_t n, const sem_cost_model* model, int32_t* service_out) {
+  int rc = check_cost_args(prompt, output, n, model, service_out);
+  if (rc != SEM_OK) return rc;
+  std::lock_guard<std::mutex> g(state().mu);
+  void* ws = nullptr;
+  rc = cached_workspace(kHeaderBytes, &ws);
+  if (rc != SEM_OK) return rc;
+  const hipStream_t st = state().stream;
+  CostArgs a = cost_args(prompt, output, decoded, n, model);
+  a.service = service_out;
+  a.flags = static_cast<uint32_t*>(ws);
+  if (launch_fill_zero(a.flags, 1, st) != hipSuccess ||
+      launch_service(a, st, nullptr, nullptr) != hipSuccess)
+    return SEM_EDEVICE;
+  return finish(ws, st);
+}
+
+int sem_evict_plan(const int32_t* prompt, const int32_t* decoded, int64_t n,
+                   const sem_cost_model* model, uint8_t* keep_prefill_out,
+                   int32_t* save_tokens_out) {
+  int rc = check_cost_args(prompt, decoded, n, model, keep_prefill_out);
+  if (rc != SEM_OK) return rc;
+  if (n > 0 && !save_tokens_out) return SEM_EINVAL;
+  std::lock_guard<std::mutex> g(state().mu);
+  void* ws = nullptr;
+  rc = cached_workspace(kHeaderBytes, &ws);
+  if (rc != SEM_OK) return rc;
+  const hipStream_t st = state().stream;
+  CostArgs a = cost_args(prompt, nullptr, decoded, n, model);
+  a.keep = keep_prefill_out;
+  a.save = save_tokens_out;
+  a.flags = static_cast<uint32_t*>(ws);
+  if (launch_fill_zero(a.flags, 1, st) != hipSuccess || launch_evict(a, st) != hipSuccess)
+    return SEM_EDEVICE;
+  return finish(ws, st);
+}
+
+size_t sem_cost_workspace_bytes(int64_t n) {
+  if (n < 0) return 0;
+  return cost_layout(n).total;
+}
+
+int sem_schedule_cost_async(const uint8_t* priority, const int32_t* prompt, const int32_t* output,
+                            const int32_t* decoded, int64_t n, const sem_cost_model* model,
+                            int32_t* order_out, int64_t* wait_out, sem_i128* totals_out,
+                            int32_t* service_out, void* workspace, size_t ws_bytes,
+                            void* stream) {
+  int rc = check_cost_args(prompt, output, n, model, order_out);
+  if (rc != SEM_OK) return rc;
+  rc = check_queue_args(priority, prompt, n, order_out, wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  if (!workspace || ws_bytes < sem_cost_workspace_bytes(n) ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return SEM_EINVAL;
+  return enqueue_cost_schedule(priority, prompt, output, decoded, n, model, order_out, wait_out,
+                               totals_out, service_out, workspace,
+                               static_cast<hipStream_t>(stream));
+}
+
+int sem_schedule_cost(const uint8_t* priority, const int32_t* prompt, const int32_t* output,
+                      const int32_t* decoded, int64_t n, const sem_cost_model* model,
+                      int32_t* order_out, int64_t* wait_out, sem_i128* totals_out,
+                      int32_t* service_out) {
+  int rc = check_cost_args(prompt, output, n, model, order_out);
+  if (rc != SEM_OK) return rc;
+  rc = check_queue_args(priority, prompt, n, order_out, wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  std::lock_guard<std::mutex> g(state().mu);
+  void* ws = nullptr;
+  rc = cached_workspace(sem_cost_workspace_bytes(n), &ws);
+  if (rc != SEM_OK) return rc;
+  const hipStream_t st = state().stream;
+  rc = enqueue_cost_schedule(priority, prompt, output, decoded, n, model, order_out, wait_out,
+                             totals_out, service_out, ws, st);
   if (rc != SEM_OK) return rc;
   return finish(ws, st);
 }

@@ -125,7 +125,7 @@ struct GArgs {
 };
 
 // Optional events recorded around one stage's kernel (null: not armed).
-constexpr int kStages = 5;  // hist, first, final (long queues); merge (insertion); policy pass
+constexpr int kStages = 6;  // hist, first, final (long queues); merge; policy pass; cost pass
 struct StageEvents {
   hipEvent_t before[kStages];
   hipEvent_t after[kStages];
@@ -199,5 +199,23 @@ hipError_t launch_fcfs(const PolArgs& a, hipStream_t st, hipEvent_t before, hipE
 hipError_t launch_hpjf(const PolArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after);
 hipError_t launch_class_totals(const PolArgs& a, hipStream_t st, hipEvent_t before,
                                hipEvent_t after);
+
+// ---------------------------------------------------------------------------
+// Cost model (cost.hip).
+struct CostArgs {
+  const int32_t* prompt;   // [n] prompt tokens
+  const int32_t* output;   // [n] predicted output tokens (service times only)
+  const int32_t* decoded;  // [n] tokens decoded so far (null: all 0)
+  int64_t n;
+  uint64_t alpha1, alpha2, beta, gamma1, gamma2;  // Q32.32
+  int32_t* service;        // [n] out: remaining computation time
+  uint8_t* keep;           // [n] out: 1 = keep the prefill cache of an eviction
+  int32_t* save;           // [n] out: decoded tokens whose cache is saved
+  uint32_t* flags;         // device error bits
+};
+
+hipError_t launch_service(const CostArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after);
+hipError_t launch_evict(const CostArgs& a, hipStream_t st);
+hipError_t launch_merge_flags(uint32_t* dst, const uint32_t* src, hipStream_t st);
 
 }  // namespace semsched

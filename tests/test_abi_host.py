@@ -130,3 +130,27 @@ def test_policy_argument_errors(ss):
         assert L.sem_policy_workspace_bytes(bad, 5) == 0
     assert L.sem_policy_workspace_bytes(ss.POLICY_SEMANTIC, 1 << 20) == ss.workspace_bytes(1 << 20)
     assert L.sem_policy_workspace_bytes(ss.POLICY_FCFS, -1) == 0
+
+
+def test_cost_argument_errors(ss):
+    L = ss.lib
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 40)  # never dereferenced: the call fails first
+    cm = ss.CostModelC(1, 2, 3, 4, 5)
+    ref = ctypes.byref(cm)
+    nocm = ctypes.cast(None, ctypes.POINTER(ss.CostModelC))
+    assert L.sem_service_times(fake, fake, nul, -1, ref, fake) == ss.SEM_EINVAL
+    assert L.sem_service_times(fake, fake, nul, 1 << 31, ref, fake) == ss.SEM_EINVAL
+    assert L.sem_service_times(nul, fake, nul, 5, ref, fake) == ss.SEM_EINVAL
+    assert L.sem_service_times(fake, fake, nul, 5, nocm, fake) == ss.SEM_EINVAL
+    assert L.sem_service_times(fake, fake, nul, 5, ref, nul) == ss.SEM_EINVAL
+    assert L.sem_evict_plan(fake, nul, 5, ref, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_evict_plan(fake, fake, 5, ref, fake, nul) == ss.SEM_EINVAL
+    assert L.sem_schedule_cost(fake, fake, fake, nul, 5, ref, fake, fake, nul,
+                               nul) == ss.SEM_EINVAL
+    assert L.sem_schedule_cost(nul, fake, fake, nul, 5, ref, fake, fake, fake,
+                               nul) == ss.SEM_EINVAL
+    assert L.sem_cost_workspace_bytes(-1) == 0
+    assert L.sem_cost_workspace_bytes(1 << 20) >= ss.workspace_bytes(1 << 20) + 4 * (1 << 20)
+    assert L.sem_schedule_cost_async(fake, fake, fake, nul, 1 << 20, ref, fake, fake, fake, nul,
+                                     fake, 256, nul) == ss.SEM_EINVAL

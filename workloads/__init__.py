@@ -14,4 +14,5 @@ from .gen import (  # noqa: F401
     fuzz_queue,
     fuzz_segments,
     sha256_arrays,
+    cost_tokens,
 )

@@ -25,6 +25,11 @@ duplicate masks):
   form, so +1 gives a classical Pareto with x_min = 1); 30 % of lengths copy
   the left neighbour in the same queue from the pre-copy array (a queue's
   first request copies its right neighbour; queues of size 1 are untouched).
+
+Token counts for the cost model of Section 3.4 (``cost_tokens``), seed 5
+unless given: prompt = U{1..4096}; output = the workload's predicted lengths;
+25 % of the requests are part-way through decoding with decoded ~
+U{1..output}, the rest have decoded nothing (decoded = 0).
 """
 
 from __future__ import annotations
@@ -42,6 +47,7 @@ __all__ = [
     "fuzz_queue",
     "fuzz_segments",
     "sha256_arrays",
+    "cost_tokens",
 ]
 
 
@@ -213,3 +219,15 @@ def sha256_arrays(*arrays) -> str:
         h.update(str(a.shape).encode())
         h.update(a.tobytes())
     return h.hexdigest()
+
+
+def cost_tokens(output: np.ndarray, seed: int = 5) -> tuple:
+    """(prompt, decoded) token counts for requests whose predicted output
+    lengths are ``output`` (int32 arrays of the same size)."""
+    rng = np.random.default_rng(seed)
+    n = output.shape[0]
+    prompt = rng.integers(1, 4097, n).astype(np.int32)
+    started = rng.random(n) < 0.25
+    dec = (rng.random(n) * output.astype(np.float64)).astype(np.int64) + 1
+    decoded = np.where(started, np.minimum(dec, output), 0).astype(np.int32)
+    return prompt, decoded
