@@ -350,16 +350,137 @@ def bench_policy(args) -> int:
     return 0
 
 
+# the A100 / Qwen1.5-7B constants of the paper's appendix (seconds per token or
+# token^2: alpha1, alpha2, beta, gamma1, gamma2), used in microseconds. (The
+# A100 / 4B prefill constant as printed, 1.466e-2 s per token^2, would put
+# most service times at the 2^31 - 1 ceiling.)
+COST_A100_7B = (5.135e-7, 1.481e-4, 1e-4, 1.349e-8, 1.330e-2)
+COST_COUNTERS = os.path.join(ROOT, "profiles", "cost_c3_counters.md")
+
+
+def bench_cost(args) -> int:
+    """Schedule the n = 2^26 workload by (priority, cost-model service time,
+    id): the service-time pass and the queue kernels; one step = one call."""
+    import numpy as np
+    import torch
+    import paper_2506_12204_amd as ss
+    from workloads import cost_tokens, generate
+
+    class Model:  # Q32.32 microseconds, rounded to nearest
+        pass
+    model = Model()
+    for name, v in zip(("alpha1", "alpha2", "beta", "gamma1", "gamma2"), COST_A100_7B):
+        setattr(model, name, int(round(v / 1e-6 * (1 << 32))))
+    w = generate(args.workload)
+    n = w.n
+    prompt, decoded = cost_tokens(w.length)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    p = torch.from_numpy(w.priority).to(dev)
+    out_t = torch.from_numpy(w.length).to(dev)
+    pr_t = torch.from_numpy(prompt).to(dev)
+    de_t = torch.from_numpy(decoded).to(dev)
+    sched = ss.CostScheduler(n, model, dev)
+    print(f"[bench] cost-model schedule, workload {args.workload} n={n}; warmup {args.warmup}",
+          file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        sched.run(p, pr_t, out_t, de_t)
+    sched.check()
+    hip = HipEvents()
+    stages = [("cost", ss.STAGE_COST), ("hist", ss.STAGE_HIST), ("first", ss.STAGE_FIRST),
+              ("mid", ss.STAGE_MID), ("final", ss.STAGE_FINAL)]
+    pairs = {name: [(hip.create(), hip.create()) for _ in range(args.steps)]
+             for name, _ in stages}
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for k in range(args.steps):
+        for name, code in stages:
+            ss.trace_stage(code, *pairs[name][k])
+        sched.run(p, pr_t, out_t, de_t)
+    t1.record()
+    torch.cuda.synchronize()
+    sched.check()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    stage_ms = {name: sum(hip.elapsed_ms(a, b) for a, b in pairs[name]) / args.steps
+                for name, _ in stages}
+    for lst in pairs.values():
+        for a, b in lst:
+            hip.destroy(a)
+            hip.destroy(b)
+    print(f"[bench] {args.steps} steps: {ms_step:.4f} ms/step; stages {stage_ms}",
+          file=sys.stderr, flush=True)
+    # algorithmic bytes per request: the service pass reads three counts and
+    # writes one; these keys (3 rank bits, about 29 service-time bits) and 26
+    # id bits share one u64 element: the first pass reads 5 and writes 8
+    # bytes, each of the two middle passes reads 8 to count and 8 to move and
+    # writes 8, the final pass reads 8 and writes order and wait
+    bytes_per_req = {"cost": 16, "hist": 5, "first": 13, "mid": 48, "final": 20}
+    dom = max(stage_ms, key=stage_ms.get)
+    achieved = bytes_per_req[dom] * n / (stage_ms[dom] * 1e-3) / 1e9
+    out = {
+        "metric": "requests/s scheduled by (urgency, cost-model service time), single queue, 1 GPU",
+        "value": n / (ms_step * 1e-3),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {
+            "workload": (WORKLOAD_TEXT[args.workload] + "; predicted output = those lengths, "
+                         "prompt U[1,4096], 25 % part-way decoded (seed 5); A100 / "
+                         "Qwen1.5-7B constants of the paper's appendix, microseconds"),
+            "n": n, "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": f"{dom} pass", "achieved": achieved,
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": counter_traffic(n, COST_COUNTERS, FINAL_SOURCE, dom + "."),
+            "bytes_per_request": bytes_per_req[dom], "avg_launch_ms": stage_ms[dom],
+        },
+        "stage_ms": stage_ms,
+    }
+    if not args.no_cpu_baseline:
+        from oracle import c_oracle_queue, c_oracle_service_times
+        from oracle import CostModel
+        cm = CostModel(model.alpha1, model.alpha2, model.beta, model.gamma1, model.gamma2)
+        t = time.perf_counter()
+        s = c_oracle_service_times(prompt, w.length, decoded, cm)
+        want = c_oracle_queue(w.priority, s)
+        dt = time.perf_counter() - t
+        same = (want[0].tobytes() == sched.order.cpu().numpy().tobytes()
+                and want[1].tobytes() == sched.wait.cpu().numpy().tobytes()
+                and list(want[2]) == ss.totals_to_ints(sched.totals)
+                and s.tobytes() == sched.service.cpu().numpy().tobytes())
+        out["cpu_baseline"] = {
+            "value": n / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": (f"the full workload (n={n}): the plain C oracle's service times "
+                       f"(128-bit integers) and merge-sort schedule, single thread"),
+        }
+        out["parity"] = "bit-exact vs oracle" if same else "MISMATCH vs oracle"
+        if not same:
+            print(json.dumps(out))
+            return 1
+    print(json.dumps(out))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c3", choices=["c3", "c2"])
-    ap.add_argument("--op", default="schedule", choices=["schedule", "insert", "policy"],
+    ap.add_argument("--op", default="schedule", choices=["schedule", "insert", "policy", "cost"],
                     help="schedule (default): the whole queue; insert: 2^16 arrivals "
                          "merged into the schedule of the rest; policy: the queue under "
-                         "--policy")
+                         "--policy; cost: ordered by cost-model service times")
     ap.add_argument("--policy", default="fcfs", choices=["fcfs", "sjf", "hpjf"],
                     help="comparison policy timed by --op policy")
     ap.add_argument("--no-cpu-baseline", action="store_true",
@@ -377,6 +498,8 @@ def main() -> int:
         return bench_insert(args)
     if args.op == "policy":
         return bench_policy(args)
+    if args.op == "cost":
+        return bench_cost(args)
 
     import numpy as np
     import torch

@@ -310,7 +310,10 @@ const char *sem_strerror(int code);
  *          SEM_STAGE_POLICY (sem_schedule_policy*: for FCFS and HPJF the pass
  *                           that writes order and waits, for SJF the pass
  *                           that sums the waits per class),
- *          SEM_STAGE_COST  (sem_schedule_cost*: the service-time pass).
+ *          SEM_STAGE_COST  (sem_schedule_cost*: the service-time pass),
+ *          SEM_STAGE_MID   (multi-pass path: the middle scatter passes that keys
+ *                           wider than two digits need; nothing is launched
+ *                           in between for narrower keys).
  * Passing NULL events disarms the stage. Returns SEM_EINVAL for an unknown
  * stage. The events are owned by the caller and must outlive the call.
  */
@@ -320,6 +323,7 @@ const char *sem_strerror(int code);
 #define SEM_STAGE_MERGE 3
 #define SEM_STAGE_POLICY 4
 #define SEM_STAGE_COST 5
+#define SEM_STAGE_MID 6
 int sem_trace_stage(int stage, void *before, void *after);
 
 #ifdef __cplusplus

@@ -55,7 +55,7 @@ SYMBOLS = (
     "sem_cost_workspace_bytes",
     "sem_schedule_cost_async",
 )
-STAGE_HIST, STAGE_FIRST, STAGE_FINAL, STAGE_MERGE, STAGE_POLICY, STAGE_COST = 0, 1, 2, 3, 4, 5
+STAGE_HIST, STAGE_FIRST, STAGE_FINAL, STAGE_MERGE, STAGE_POLICY, STAGE_COST, STAGE_MID = range(7)
 # comparison policies (Section 4): the key fields before the id
 POLICY_SEMANTIC, POLICY_FCFS, POLICY_SJF, POLICY_HPJF = 0, 1, 2, 3
 

@@ -230,7 +230,7 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   bool armed = false;
   {
     std::lock_guard<std::mutex> guard(trace_mu());
-    for (int k = SEM_STAGE_HIST; k <= SEM_STAGE_FINAL; ++k) {
+    for (int k : {SEM_STAGE_HIST, SEM_STAGE_FIRST, SEM_STAGE_FINAL, SEM_STAGE_MID}) {
       ev.before[k] = trace_slots().before[k];
       ev.after[k] = trace_slots().after[k];
       armed = armed || ev.before[k] || ev.after[k];
@@ -544,7 +544,7 @@ const char* sem_strerror(int code) {
 }
 
 int sem_trace_stage(int stage, void* before, void* after) {
-  if (stage < SEM_STAGE_HIST || stage > SEM_STAGE_COST) return SEM_EINVAL;
+  if (stage < SEM_STAGE_HIST || stage > SEM_STAGE_MID) return SEM_EINVAL;
   std::lock_guard<std::mutex> guard(trace_mu());
   trace_slots().before[stage] = static_cast<hipEvent_t>(before);
   trace_slots().after[stage] = static_cast<hipEvent_t>(after);

@@ -2200,7 +2200,9 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   else
     hipLaunchKernelGGL(g_first<8>, gm, dim3(NT), 0, st, a);
   mark(ev, 1, true, st);
+  mark(ev, 6, false, st);
   hipLaunchKernelGGL(g_mid, dim3(a.mid.blocks), dim3(NT), 0, st, a);
+  mark(ev, 6, true, st);
   const dim3 gf(a.fin.blocks);
   hipLaunchKernelGGL(g_histF, dim3(a.fin.blocks * kHistRows), dim3(HT), 0, st, a);
   hipLaunchKernelGGL(g_scan, dim3(kMaxBins), dim3(SCT), 0, st, a, 1);

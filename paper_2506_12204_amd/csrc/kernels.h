@@ -125,7 +125,7 @@ struct GArgs {
 };
 
 // Optional events recorded around one stage's kernel (null: not armed).
-constexpr int kStages = 6;  // hist, first, final (long queues); merge; policy pass; cost pass
+constexpr int kStages = 7;  // hist, first, final (long queues); merge; policy; cost; middle passes
 struct StageEvents {
   hipEvent_t before[kStages];
   hipEvent_t after[kStages];
