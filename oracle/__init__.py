@@ -7,6 +7,8 @@ and shares no code with it.
 * ``semsched_oracle``: the pure-Python oracle (the plain definition).
 * ``cost_oracle``: the cost model of Section 3.4 (service times, the cache
   and recompute decisions of an eviction) in exact integers.
+* ``batch_oracle``: stage-aware batch selection and priority-based eviction
+  (Algorithms 2-4) as literal heap simulations.
 * ``c_oracle_*``: ctypes wrappers of ``oracle.c``, the same definition in
   plain C for large queues and for the timed CPU baseline.
 """
@@ -19,6 +21,7 @@ import subprocess
 
 import numpy as np
 
+from .batch_oracle import evict, eviction_order, select_batch  # noqa: F401
 from .cost_oracle import (  # noqa: F401
     CostModel,
     evict_plan,
