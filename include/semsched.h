@@ -284,6 +284,73 @@ int sem_schedule_cost_async(const uint8_t *priority, const int32_t *prompt,
                             int64_t *wait_out, sem_i128 *totals_out, int32_t *service_out,
                             void *workspace, size_t ws_bytes, void *stream);
 
+/*
+ * Stage-aware selection of the next batch (Algorithm 2, blocking). Every
+ * request has the key (priority, length, id) of the schedule and a stage
+ * (0 = prefill, 1 = decoding):
+ *   priority, length, stage [n_ids] DEVICE, indexed by request id;
+ *   heap_order [n_heap] DEVICE: the waiting requests in schedule order (as
+ *     sem_schedule / sem_insert return them; only the first b are read);
+ *   buffer [n_buffer] DEVICE: waiting requests not yet in that schedule;
+ *   ongoing [n_ongoing] DEVICE: the requests of the running batch.
+ * C = the b smallest keys among heap and buffer. If the smallest key of C
+ * and the ongoing requests is in the prefill stage, M = C and the ongoing
+ * requests merged by key; otherwise M = C's decoding members and the ongoing
+ * requests, and C's prefill members are pushed back. The next batch is M's
+ * first b; the rest of M is pushed back too.
+ *   batch_out [b] DEVICE: the next batch in key order;
+ *   pushed_out [b + n_ongoing] DEVICE: the pushed-back requests in key order;
+ *   counts_out [2] int64 DEVICE: batch size, pushed-back count.
+ * Errors: SEM_EINVAL (negative sizes, null pointers, an id outside
+ * [0, n_ids)), SEM_ENOTIMPL (b, n_buffer or n_ongoing above SEM_SELECT_CAP).
+ */
+#define SEM_SELECT_CAP 4096
+int sem_select_batch(const uint8_t *priority, const int32_t *length, const uint8_t *stage,
+                     int64_t n_ids, const int32_t *heap_order, int64_t n_heap,
+                     const int32_t *buffer, int64_t n_buffer, const int32_t *ongoing,
+                     int64_t n_ongoing, int64_t b, int32_t *batch_out, int32_t *pushed_out,
+                     int64_t *counts_out);
+
+/* Asynchronous sem_select_batch: workspace of at least 256 bytes (DEVICE,
+ * 256-byte aligned) and the stream; errors by sem_check(workspace, stream). */
+int sem_select_batch_async(const uint8_t *priority, const int32_t *length,
+                           const uint8_t *stage, int64_t n_ids, const int32_t *heap_order,
+                           int64_t n_heap, const int32_t *buffer, int64_t n_buffer,
+                           const int32_t *ongoing, int64_t n_ongoing, int64_t b,
+                           int32_t *batch_out, int32_t *pushed_out, int64_t *counts_out,
+                           void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Priority-based eviction (Algorithms 3 and 4, blocking). The cached
+ * requests leave the device in the inverse of the schedule order (least
+ * urgent rank first, then longest remaining time, then the later arrival).
+ * For incoming requests j = 0, 1, ... with KV demands demands[j], request j
+ * evicts until its demand fits: victims are the shortest prefix of that
+ * order whose KV sizes cover usage + (demands 0..j) - capacity (all cached
+ * requests if they do not). Incoming requests are not victims of each other.
+ *   priority, length [n_ids] DEVICE; cached [n_cached] int32 ids and
+ *   kv [n_cached] int64 sizes DEVICE; demands [n_demands] int64 DEVICE;
+ *   victims_out [n_cached] DEVICE: the first upto_out[n_demands-1] entries
+ *     receive the victims in eviction order;
+ *   upto_out [n_demands] int64 DEVICE: victims after each incoming request.
+ * Sums of usage and demands must stay below 2^63.
+ * Errors: SEM_EINVAL (negative sizes, null pointers, an id outside [0, n_ids)),
+ * SEM_ERANGE (a negative KV size or demand), SEM_ENOTIMPL (n_cached above
+ * SEM_EVICT_CAP).
+ */
+#define SEM_EVICT_CAP 8192
+int sem_evict(const uint8_t *priority, const int32_t *length, int64_t n_ids,
+              const int32_t *cached, const int64_t *kv, int64_t n_cached, int64_t usage,
+              int64_t capacity, const int64_t *demands, int64_t n_demands,
+              int32_t *victims_out, int64_t *upto_out);
+
+/* Asynchronous sem_evict: workspace of at least 256 bytes and the stream. */
+int sem_evict_async(const uint8_t *priority, const int32_t *length, int64_t n_ids,
+                    const int32_t *cached, const int64_t *kv, int64_t n_cached, int64_t usage,
+                    int64_t capacity, const int64_t *demands, int64_t n_demands,
+                    int32_t *victims_out, int64_t *upto_out, void *workspace, size_t ws_bytes,
+                    void *stream);
+
 /* Stream used by the blocking calls (NULL = null stream). */
 int sem_set_stream(void *stream);
 

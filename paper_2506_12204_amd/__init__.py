@@ -54,7 +54,14 @@ SYMBOLS = (
     "sem_schedule_cost",
     "sem_cost_workspace_bytes",
     "sem_schedule_cost_async",
+    "sem_select_batch",
+    "sem_select_batch_async",
+    "sem_evict",
+    "sem_evict_async",
 )
+SELECT_CAP = 4096
+EVICT_CAP = 8192
+PREFILL, DECODE = 0, 1
 STAGE_HIST, STAGE_FIRST, STAGE_FINAL, STAGE_MERGE, STAGE_POLICY, STAGE_COST, STAGE_MID = range(7)
 # comparison policies (Section 4): the key fields before the id
 POLICY_SEMANTIC, POLICY_FCFS, POLICY_SJF, POLICY_HPJF = 0, 1, 2, 3
@@ -117,13 +124,20 @@ def _load() -> ctypes.CDLL:
     lib.sem_cost_workspace_bytes.argtypes = [i64]
     lib.sem_cost_workspace_bytes.restype = sz
     lib.sem_schedule_cost_async.argtypes = [vp, vp, vp, vp, i64, cm, vp, vp, vp, vp, vp, sz, vp]
+    lib.sem_select_batch.argtypes = [vp, vp, vp, i64, vp, i64, vp, i64, vp, i64, i64, vp, vp, vp]
+    lib.sem_select_batch_async.argtypes = [vp, vp, vp, i64, vp, i64, vp, i64, vp, i64, i64, vp,
+                                           vp, vp, vp, sz, vp]
+    lib.sem_evict.argtypes = [vp, vp, i64, vp, vp, i64, i64, i64, vp, i64, vp, vp]
+    lib.sem_evict_async.argtypes = [vp, vp, i64, vp, vp, i64, i64, i64, vp, i64, vp, vp, vp, sz,
+                                    vp]
     lib.sem_strerror.argtypes = [ctypes.c_int]
     lib.sem_strerror.restype = ctypes.c_char_p
     for name in ("sem_schedule", "sem_schedule_batched", "sem_schedule_async",
                  "sem_schedule_batched_async", "sem_set_stream", "sem_check", "sem_insert",
                  "sem_insert_async", "sem_schedule_policy", "sem_schedule_policy_async",
                  "sem_service_times", "sem_evict_plan", "sem_schedule_cost",
-                 "sem_schedule_cost_async"):
+                 "sem_schedule_cost_async", "sem_select_batch", "sem_select_batch_async",
+                 "sem_evict", "sem_evict_async"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -427,3 +441,57 @@ def schedule_cost(priority: torch.Tensor, prompt: torch.Tensor, output: torch.Te
     s.run(priority, prompt, output, decoded)
     s.check()
     return s.order, s.wait, totals_to_ints(s.totals), s.service
+
+
+def _ids(t: Optional[torch.Tensor], device) -> Optional[torch.Tensor]:
+    if t is None:
+        return None
+    if t.dtype != torch.int32 or t.device != device or t.dim() != 1 or not t.is_contiguous():
+        raise TypeError("id lists must be contiguous 1-D int32 tensors on the inputs' GPU")
+    return t
+
+
+def select_batch(priority: torch.Tensor, length: torch.Tensor, stage: torch.Tensor,
+                 heap_order: torch.Tensor, buffer: Optional[torch.Tensor],
+                 ongoing: Optional[torch.Tensor], b: int) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Algorithm 2: (next batch, pushed-back requests), both in key order."""
+    _check_inputs(priority, length)
+    dev = priority.device
+    if stage.dtype != torch.uint8 or stage.shape != priority.shape or stage.device != dev:
+        raise TypeError("stage must be uint8 with one entry per request")
+    heap_order, buffer, ongoing = (_ids(heap_order, dev), _ids(buffer, dev), _ids(ongoing, dev))
+    nh = heap_order.numel() if heap_order is not None else 0
+    nb = buffer.numel() if buffer is not None else 0
+    no = ongoing.numel() if ongoing is not None else 0
+    batch = torch.empty(max(int(b), 1), dtype=torch.int32, device=dev)
+    pushed = torch.empty(max(int(b) + no, 1), dtype=torch.int32, device=dev)
+    counts = torch.zeros(2, dtype=torch.int64, device=dev)
+    lib.sem_set_stream(_stream_handle(dev))
+    _raise(lib.sem_select_batch(_ptr(priority), _ptr(length), _ptr(stage), priority.numel(),
+                                _ptr(heap_order), nh, _ptr(buffer), nb, _ptr(ongoing), no, int(b),
+                                _ptr(batch), _ptr(pushed), _ptr(counts)), "sem_select_batch")
+    nbat, npush = counts.tolist()
+    return batch[:nbat], pushed[:npush]
+
+
+def evict(priority: torch.Tensor, length: torch.Tensor, cached: torch.Tensor, kv: torch.Tensor,
+          usage: int, capacity: int, demands: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Algorithms 3-4: (victims in eviction order, victims after each incoming
+    request)."""
+    _check_inputs(priority, length)
+    dev = priority.device
+    cached = _ids(cached, dev)
+    if kv.dtype != torch.int64 or kv.shape != cached.shape or kv.device != dev:
+        raise TypeError("kv must be int64 with one entry per cached request")
+    if demands.dtype != torch.int64 or demands.device != dev or demands.dim() != 1:
+        raise TypeError("demands must be a 1-D int64 tensor")
+    kv, demands = kv.contiguous(), demands.contiguous()
+    victims = torch.empty(max(cached.numel(), 1), dtype=torch.int32, device=dev)
+    upto = torch.empty(max(demands.numel(), 1), dtype=torch.int64, device=dev)
+    lib.sem_set_stream(_stream_handle(dev))
+    _raise(lib.sem_evict(_ptr(priority), _ptr(length), priority.numel(), _ptr(cached), _ptr(kv),
+                         cached.numel(), int(usage), int(capacity), _ptr(demands),
+                         demands.numel(), _ptr(victims), _ptr(upto)), "sem_evict")
+    upto = upto[:demands.numel()]
+    k = int(upto[-1]) if demands.numel() else 0
+    return victims[:k], upto

@@ -730,6 +730,126 @@ int sem_schedule_cost(const uint8_t* priority, const int32_t* prompt, const int3
   return finish(ws, st);
 }
 
+static_assert(SEM_SELECT_CAP == kSelectCap && SEM_EVICT_CAP == kEvictCap,
+              "the header's caps are the kernels'");
+
+int check_select(const uint8_t* p, const int32_t* l, const uint8_t* stage, int64_t n_ids,
+                 const int32_t* heap, int64_t n_heap, const int32_t* buffer, int64_t n_buffer,
+                 const int32_t* ongoing, int64_t n_ongoing, int64_t b, int32_t* batch,
+                 int32_t* pushed, int64_t* counts) {
+  if (n_ids < 0 || n_ids > INT32_MAX || n_heap < 0 || n_buffer < 0 || n_ongoing < 0 || b < 0)
+    return SEM_EINVAL;
+  if (b > kSelectCap || n_buffer > kSelectCap || n_ongoing > kSelectCap) return SEM_ENOTIMPL;
+  if (!counts) return SEM_EINVAL;
+  const bool any = std::min(b, n_heap) + n_buffer + n_ongoing > 0;
+  if (any && (!p || !l || !stage)) return SEM_EINVAL;
+  if ((std::min(b, n_heap) > 0 && !heap) || (n_buffer > 0 && !buffer) ||
+      (n_ongoing > 0 && !ongoing) || (b > 0 && !batch) || (any && !pushed))
+    return SEM_EINVAL;
+  return SEM_OK;
+}
+
+int enqueue_select(const uint8_t* p, const int32_t* l, const uint8_t* stage, int64_t n_ids,
+                   const int32_t* heap, int64_t n_heap, const int32_t* buffer, int64_t n_buffer,
+                   const int32_t* ongoing, int64_t n_ongoing, int64_t b, int32_t* batch,
+                   int32_t* pushed, int64_t* counts, void* ws, hipStream_t st) {
+  SelArgs a = {p, l, stage, n_ids, heap, n_heap, buffer, n_buffer, ongoing, n_ongoing, b,
+               batch, pushed, counts, static_cast<uint32_t*>(ws)};
+  if (launch_fill_zero(a.flags, 1, st) != hipSuccess || launch_select(a, st) != hipSuccess)
+    return SEM_EDEVICE;
+  return SEM_OK;
+}
+
+int sem_select_batch_async(const uint8_t* priority, const int32_t* length, const uint8_t* stage,
+                           int64_t n_ids, const int32_t* heap_order, int64_t n_heap,
+                           const int32_t* buffer, int64_t n_buffer, const int32_t* ongoing,
+                           int64_t n_ongoing, int64_t b, int32_t* batch_out, int32_t* pushed_out,
+                           int64_t* counts_out, void* workspace, size_t ws_bytes, void* stream) {
+  const int rc = check_select(priority, length, stage, n_ids, heap_order, n_heap, buffer,
+                              n_buffer, ongoing, n_ongoing, b, batch_out, pushed_out, counts_out);
+  if (rc != SEM_OK) return rc;
+  if (!workspace || ws_bytes < kHeaderBytes ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return SEM_EINVAL;
+  return enqueue_select(priority, length, stage, n_ids, heap_order, n_heap, buffer, n_buffer,
+                        ongoing, n_ongoing, b, batch_out, pushed_out, counts_out, workspace,
+                        static_cast<hipStream_t>(stream));
+}
+
+int sem_select_batch(const uint8_t* priority, const int32_t* length, const uint8_t* stage,
+                     int64_t n_ids, const int32_t* heap_order, int64_t n_heap,
+                     const int32_t* buffer, int64_t n_buffer, const int32_t* ongoing,
+                     int64_t n_ongoing, int64_t b, int32_t* batch_out, int32_t* pushed_out,
+                     int64_t* counts_out) {
+  int rc = check_select(priority, length, stage, n_ids, heap_order, n_heap, buffer, n_buffer,
+                        ongoing, n_ongoing, b, batch_out, pushed_out, counts_out);
+  if (rc != SEM_OK) return rc;
+  std::lock_guard<std::mutex> g(state().mu);
+  void* ws = nullptr;
+  rc = cached_workspace(kHeaderBytes, &ws);
+  if (rc != SEM_OK) return rc;
+  const hipStream_t st = state().stream;
+  rc = enqueue_select(priority, length, stage, n_ids, heap_order, n_heap, buffer, n_buffer,
+                      ongoing, n_ongoing, b, batch_out, pushed_out, counts_out, ws, st);
+  if (rc != SEM_OK) return rc;
+  return finish(ws, st);
+}
+
+int check_evict(const uint8_t* p, const int32_t* l, int64_t n_ids, const int32_t* cached,
+                const int64_t* kv, int64_t n_cached, const int64_t* demands, int64_t n_demands,
+                int32_t* victims, int64_t* upto) {
+  if (n_ids < 0 || n_ids > INT32_MAX || n_cached < 0 || n_demands < 0) return SEM_EINVAL;
+  if (n_cached > kEvictCap) return SEM_ENOTIMPL;
+  if (n_cached > 0 && (!p || !l || !cached || !kv || !victims)) return SEM_EINVAL;
+  if (n_demands > 0 && (!demands || !upto)) return SEM_EINVAL;
+  return SEM_OK;
+}
+
+int enqueue_evict(const uint8_t* p, const int32_t* l, int64_t n_ids, const int32_t* cached,
+                  const int64_t* kv, int64_t n_cached, int64_t usage, int64_t capacity,
+                  const int64_t* demands, int64_t n_demands, int32_t* victims, int64_t* upto,
+                  void* ws, hipStream_t st) {
+  EvictArgs a = {p, l, n_ids, cached, kv, n_cached, usage, capacity, demands, n_demands,
+                 victims, upto, static_cast<uint32_t*>(ws)};
+  if (launch_fill_zero(a.flags, 1, st) != hipSuccess) return SEM_EDEVICE;
+  if (n_cached + n_demands == 0) return SEM_OK;
+  return launch_evict_victims(a, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
+}
+
+int sem_evict_async(const uint8_t* priority, const int32_t* length, int64_t n_ids,
+                    const int32_t* cached, const int64_t* kv, int64_t n_cached, int64_t usage,
+                    int64_t capacity, const int64_t* demands, int64_t n_demands,
+                    int32_t* victims_out, int64_t* upto_out, void* workspace, size_t ws_bytes,
+                    void* stream) {
+  const int rc = check_evict(priority, length, n_ids, cached, kv, n_cached, demands, n_demands,
+                             victims_out, upto_out);
+  if (rc != SEM_OK) return rc;
+  if (!workspace || ws_bytes < kHeaderBytes ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return SEM_EINVAL;
+  return enqueue_evict(priority, length, n_ids, cached, kv, n_cached, usage, capacity, demands,
+                       n_demands, victims_out, upto_out, workspace,
+                       static_cast<hipStream_t>(stream));
+}
+
+int sem_evict(const uint8_t* priority, const int32_t* length, int64_t n_ids,
+              const int32_t* cached, const int64_t* kv, int64_t n_cached, int64_t usage,
+              int64_t capacity, const int64_t* demands, int64_t n_demands, int32_t* victims_out,
+              int64_t* upto_out) {
+  int rc = check_evict(priority, length, n_ids, cached, kv, n_cached, demands, n_demands,
+                       victims_out, upto_out);
+  if (rc != SEM_OK) return rc;
+  std::lock_guard<std::mutex> g(state().mu);
+  void* ws = nullptr;
+  rc = cached_workspace(kHeaderBytes, &ws);
+  if (rc != SEM_OK) return rc;
+  const hipStream_t st = state().stream;
+  rc = enqueue_evict(priority, length, n_ids, cached, kv, n_cached, usage, capacity, demands,
+                     n_demands, victims_out, upto_out, ws, st);
+  if (rc != SEM_OK) return rc;
+  return finish(ws, st);
+}
+
 int sem_schedule(const uint8_t* priority, const int32_t* length, int64_t n, int32_t* order_out,
                  int64_t* wait_out, sem_i128* totals_out) {
   int rc = check_queue_args(priority, length, n, order_out, wait_out, totals_out);

@@ -218,4 +218,45 @@ hipError_t launch_service(const CostArgs& a, hipStream_t st, hipEvent_t before, 
 hipError_t launch_evict(const CostArgs& a, hipStream_t st);
 hipError_t launch_merge_flags(uint32_t* dst, const uint32_t* src, hipStream_t st);
 
+// ---------------------------------------------------------------------------
+// Batch selection and eviction (batch.hip), one workgroup each.
+constexpr int kSelectCap = 4096;  // largest batch, buffer and ongoing set
+constexpr int kEvictCap = 8192;   // most cached requests
+
+struct SelArgs {
+  const uint8_t* priority;  // [n_ids]
+  const int32_t* length;    // [n_ids]
+  const uint8_t* stage;     // [n_ids] 0 = prefill, 1 = decoding
+  int64_t n_ids;
+  const int32_t* heap_order;  // [n_heap] the waiting requests' schedule (first b read)
+  int64_t n_heap;
+  const int32_t* buffer;    // [n_buffer] arrivals not yet in the schedule
+  int64_t n_buffer;
+  const int32_t* ongoing;   // [n_ongoing]
+  int64_t n_ongoing;
+  int64_t b;
+  int32_t* batch;           // [b]
+  int32_t* pushed;          // [b + n_ongoing]
+  int64_t* counts;          // [2] batch size, pushed-back count
+  uint32_t* flags;
+};
+
+struct EvictArgs {
+  const uint8_t* priority;
+  const int32_t* length;
+  int64_t n_ids;
+  const int32_t* cached;    // [n_cached]
+  const int64_t* kv;        // [n_cached] KV size of each cached request
+  int64_t n_cached;
+  int64_t usage, capacity;
+  const int64_t* demands;   // [n_demands] KV demand of each incoming request
+  int64_t n_demands;
+  int32_t* victims;         // [n_cached] eviction order, first upto[last] written
+  int64_t* upto;            // [n_demands] victims after each incoming request
+  uint32_t* flags;
+};
+
+hipError_t launch_select(const SelArgs& a, hipStream_t st);
+hipError_t launch_evict_victims(const EvictArgs& a, hipStream_t st);
+
 }  // namespace semsched

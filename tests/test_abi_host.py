@@ -154,3 +154,27 @@ def test_cost_argument_errors(ss):
     assert L.sem_cost_workspace_bytes(1 << 20) >= ss.workspace_bytes(1 << 20) + 4 * (1 << 20)
     assert L.sem_schedule_cost_async(fake, fake, fake, nul, 1 << 20, ref, fake, fake, fake, nul,
                                      fake, 256, nul) == ss.SEM_EINVAL
+
+
+def test_select_and_evict_argument_errors(ss):
+    L = ss.lib
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 40)  # never dereferenced: the call fails first
+    S = L.sem_select_batch
+    assert S(fake, fake, fake, -1, fake, 5, nul, 0, nul, 0, 2, fake, fake, fake) == ss.SEM_EINVAL
+    assert S(fake, fake, fake, 10, fake, 5, nul, 0, nul, 0, -1, fake, fake, fake) == ss.SEM_EINVAL
+    assert S(fake, fake, fake, 10, fake, 5, nul, 0, nul, 0, ss.SELECT_CAP + 1, fake, fake,
+             fake) == ss.SEM_ENOTIMPL
+    assert S(fake, fake, fake, 10, fake, 5, fake, ss.SELECT_CAP + 1, nul, 0, 2, fake, fake,
+             fake) == ss.SEM_ENOTIMPL
+    assert S(fake, fake, nul, 10, fake, 5, nul, 0, nul, 0, 2, fake, fake, fake) == ss.SEM_EINVAL
+    assert S(fake, fake, fake, 10, nul, 5, nul, 0, nul, 0, 2, fake, fake, fake) == ss.SEM_EINVAL
+    assert S(fake, fake, fake, 10, fake, 5, nul, 0, nul, 0, 2, fake, fake, nul) == ss.SEM_EINVAL
+    E = L.sem_evict
+    assert E(fake, fake, 10, fake, fake, -1, 0, 0, fake, 1, fake, fake) == ss.SEM_EINVAL
+    assert E(fake, fake, 10, fake, fake, ss.EVICT_CAP + 1, 0, 0, fake, 1, fake,
+             fake) == ss.SEM_ENOTIMPL
+    assert E(fake, fake, 10, fake, nul, 5, 0, 0, fake, 1, fake, fake) == ss.SEM_EINVAL
+    assert E(fake, fake, 10, fake, fake, 5, 0, 0, nul, 1, fake, fake) == ss.SEM_EINVAL
+    assert L.sem_evict_async(fake, fake, 10, fake, fake, 5, 0, 0, fake, 1, fake, fake, nul, 256,
+                             nul) == ss.SEM_EINVAL

@@ -1,0 +1,117 @@
+"""GPU parity of stage-aware batch selection (sem_select_batch, Algorithm 2)
+and priority-based eviction (sem_evict, Algorithms 3-4) against the oracle's
+heap simulations (oracle/batch_oracle.py, pinned in
+tests/test_oracle_batch.py). Ids and counts: exact comparisons.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import evict, select_batch
+from tests._lib import ensure_built, gpu_available
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    ensure_built()
+
+
+def dev(a, dt):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=dt)).cuda()
+
+
+def instance(seed, n_ids, nh, nu, no, classes=5, max_len=4000, decode_frac=0.5):
+    rng = np.random.default_rng(seed)
+    p = rng.integers(0, classes, n_ids).astype(np.uint8)
+    l = rng.integers(0, max_len, n_ids).astype(np.int32)
+    stage = (rng.random(n_ids) < decode_frac).astype(np.uint8)
+    ids = rng.permutation(n_ids)
+    waiting = ids[:nh]
+    heap = waiting[np.lexsort((waiting, l[waiting], p[waiting]))]
+    buf = ids[nh:nh + nu]
+    ong = ids[nh + nu:nh + nu + no]
+    return p, l, stage, heap, buf, ong
+
+
+def run_select(p, l, stage, heap, buf, ong, b):
+    import paper_2506_12204_amd as ss
+    bt, pu = ss.select_batch(dev(p, np.uint8), dev(l, np.int32), dev(stage, np.uint8),
+                             dev(heap, np.int32), dev(buf, np.int32), dev(ong, np.int32), b)
+    return bt.cpu().numpy().tolist(), pu.cpu().numpy().tolist()
+
+
+@pytest.mark.parametrize("case", [
+    (1, 0, 0, 0, 1), (10, 5, 2, 3, 4), (1000, 500, 100, 50, 64), (1 << 20, 200000, 3000, 256, 256),
+    (1 << 20, 100000, 4096, 4096, 4096), (50000, 3, 4096, 10, 4096), (50000, 20000, 0, 4096, 1),
+    (50000, 20000, 0, 0, 0), (50000, 0, 0, 300, 128), (9000, 4000, 4096, 0, 4096)])
+@pytest.mark.parametrize("decode_frac", [0.0, 0.5, 1.0])
+def test_select_batch(case, decode_frac):
+    n_ids, nh, nu, no, b = case
+    print(f"[gpu] select n_ids={n_ids} heap={nh} buffer={nu} ongoing={no} b={b}", flush=True)
+    p, l, stage, heap, buf, ong = instance(sum(case) + int(10 * decode_frac), n_ids, nh, nu, no,
+                                           decode_frac=decode_frac)
+    want = select_batch(p.tolist(), l.tolist(), stage.tolist(), heap.tolist(), buf.tolist(),
+                        ong.tolist(), b)
+    assert run_select(p, l, stage, heap, buf, ong, b) == want
+
+
+def test_select_batch_ties_and_inversion():
+    # many equal keys (ties go to the lower id) and an urgent decoding request
+    n = 20000
+    rng = np.random.default_rng(5)
+    p = rng.integers(0, 2, n).astype(np.uint8)
+    l = rng.integers(0, 3, n).astype(np.int32)
+    stage = (rng.random(n) < 0.5).astype(np.uint8)
+    ids = rng.permutation(n)
+    heap = ids[:9000][np.lexsort((ids[:9000], l[ids[:9000]], p[ids[:9000]]))]
+    buf, ong = ids[9000:12000], ids[12000:12100]
+    p[ong[0]], l[ong[0]], stage[ong[0]] = 0, 0, 1  # the most urgent request is decoding
+    want = select_batch(p.tolist(), l.tolist(), stage.tolist(), heap.tolist(), buf.tolist(),
+                        ong.tolist(), 2000)
+    assert run_select(p, l, stage, heap, buf, ong, 2000) == want
+
+
+@pytest.mark.parametrize("n_cached,n_dem", [(0, 0), (0, 3), (1, 1), (100, 7), (5000, 300),
+                                            (8192, 4000), (8192, 0), (3000, 2500)])
+def test_evict(n_cached, n_dem):
+    import paper_2506_12204_amd as ss
+    rng = np.random.default_rng(n_cached * 31 + n_dem)
+    n_ids = 1 << 18
+    p = rng.integers(0, 5, n_ids).astype(np.uint8)
+    l = rng.integers(0, 100, n_ids).astype(np.int32)  # small range: many ties
+    cached = rng.permutation(n_ids)[:n_cached].astype(np.int32)
+    kv = rng.integers(0, 1 << 30, n_cached).astype(np.int64)
+    kv[: n_cached // 10] = 0
+    demands = rng.integers(0, 1 << 31, n_dem).astype(np.int64)
+    usage = int(kv.sum()) + 12345
+    for capacity in (usage + int(demands.sum()) + 1, usage, usage // 2, 0):
+        print(f"[gpu] evict cached={n_cached} demands={n_dem} capacity={capacity}", flush=True)
+        want_v, want_u = evict(p.tolist(), l.tolist(), cached.tolist(), kv.tolist(), usage,
+                               capacity, demands.tolist())
+        v, u = ss.evict(dev(p, np.uint8), dev(l, np.int32), dev(cached, np.int32),
+                        dev(kv, np.int64), usage, capacity, dev(demands, np.int64))
+        assert v.cpu().numpy().tolist() == want_v
+        assert u.cpu().numpy().tolist() == want_u
+
+
+def test_errors():
+    import paper_2506_12204_amd as ss
+    p = dev(np.zeros(10, np.uint8), np.uint8)
+    l = dev(np.ones(10, np.int32), np.int32)
+    st = dev(np.zeros(10, np.uint8), np.uint8)
+    with pytest.raises(ss.SemschedError):
+        ss.select_batch(p, l, st, dev(np.array([1, 12]), np.int32), None, None, 2)
+    with pytest.raises(ss.SemschedRangeError):
+        ss.evict(p, l, dev(np.array([1, 2]), np.int32), dev(np.array([3, -1]), np.int64), 5, 1,
+                 dev(np.array([1]), np.int64))
+    with pytest.raises(ss.SemschedError):
+        ss.evict(p, l, dev(np.array([1, 99]), np.int32), dev(np.array([3, 1]), np.int64), 5, 1,
+                 dev(np.array([1]), np.int64))
+    # a later good call is not affected
+    v, u = ss.evict(p, l, dev(np.array([1, 2]), np.int32), dev(np.array([3, 4]), np.int64), 7, 7,
+                    dev(np.array([1]), np.int64))
+    assert u.cpu().tolist() == [1]
