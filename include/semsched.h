@@ -293,6 +293,7 @@ int sem_schedule_cost_async(const uint8_t *priority, const int32_t *prompt,
  *     sem_schedule / sem_insert return them; only the first b are read);
  *   buffer [n_buffer] DEVICE: waiting requests not yet in that schedule;
  *   ongoing [n_ongoing] DEVICE: the requests of the running batch.
+ * The three lists hold distinct ids (a request is in one place only).
  * C = the b smallest keys among heap and buffer. If the smallest key of C
  * and the ongoing requests is in the prefill stage, M = C and the ongoing
  * requests merged by key; otherwise M = C's decoding members and the ongoing
@@ -328,8 +329,8 @@ int sem_select_batch_async(const uint8_t *priority, const int32_t *length,
  * evicts until its demand fits: victims are the shortest prefix of that
  * order whose KV sizes cover usage + (demands 0..j) - capacity (all cached
  * requests if they do not). Incoming requests are not victims of each other.
- *   priority, length [n_ids] DEVICE; cached [n_cached] int32 ids and
- *   kv [n_cached] int64 sizes DEVICE; demands [n_demands] int64 DEVICE;
+ *   priority, length [n_ids] DEVICE; cached [n_cached] int32 ids (distinct)
+ *   and kv [n_cached] int64 sizes DEVICE; demands [n_demands] int64 DEVICE;
  *   victims_out [n_cached] DEVICE: the first upto_out[n_demands-1] entries
  *     receive the victims in eviction order;
  *   upto_out [n_demands] int64 DEVICE: victims after each incoming request.
