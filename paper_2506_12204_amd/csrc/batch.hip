@@ -33,41 +33,111 @@ __device__ __forceinline__ bool less(uint64_t ka, uint32_t ia, uint64_t kb, uint
   return ka < kb || (ka == kb && ia < ib);
 }
 
-__device__ __forceinline__ uint32_t pow2_at_least(uint32_t n) {
-  uint32_t p = 1;
-  while (p < n) p <<= 1;
-  return p;
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m) {
+  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m, kWave);
+  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m, kWave);
+  return (uint64_t)hi << 32 | lo;
 }
 
-// Ascending bitonic sort of N (a power of two) (key, id) pairs with an
-// optional u32 payload that moves with them. Every thread of the block
-// must call it.
-template <bool PAYLOAD>
-__device__ void bitonic(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t N) {
+// Ascending bitonic sort of BT * E (key, id) pairs in LDS, with an optional
+// u32 payload that moves with them. Thread t holds elements t*E .. t*E+E-1 in
+// registers throughout: compare-exchange distances below E stay inside a
+// thread, distances below 64 * E pair a lane with another lane of its wave
+// (shuffles, no barrier), and only the longer ones go through LDS with
+// workgroup barriers. Every thread of the block must call it.
+template <int E, bool PAYLOAD>
+__device__ void block_sort(uint64_t* key, uint32_t* id, uint32_t* pay) {
+  constexpr uint32_t N = BT * E;
+  const uint32_t t = threadIdx.x, lane = t & (kWave - 1);
+  uint64_t xk[E];
+  uint32_t xi[E], xp[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    xk[e] = key[t * E + e];
+    xi[e] = id[t * E + e];
+    xp[e] = PAYLOAD ? pay[t * E + e] : 0u;
+  }
+  // element (t*E + e) meets its partner; keep the smaller when take_min
+  auto keep = [&](int e, bool take_min, uint64_t pk, uint32_t pi, uint32_t pp) {
+    const bool pless = less(pk, pi, xk[e], xi[e]);
+    if (take_min == pless) {
+      xk[e] = pk;
+      xi[e] = pi;
+      xp[e] = pp;
+    }
+  };
   for (uint32_t k = 2; k <= N; k <<= 1) {
     for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-      for (uint32_t i = threadIdx.x; i < N; i += BT) {
-        const uint32_t x = i ^ j;
-        if (x > i) {
-          const bool up = (i & k) == 0;
-          const uint64_t ka = key[i], kb = key[x];
-          const uint32_t ia = id[i], ib = id[x];
-          if (less(kb, ib, ka, ia) == up) {
-            key[i] = kb;
-            key[x] = ka;
-            id[i] = ib;
-            id[x] = ia;
-            if (PAYLOAD) {
-              const uint32_t t = pay[i];
-              pay[i] = pay[x];
-              pay[x] = t;
+      if (j < (uint32_t)E) {
+#pragma unroll
+        for (int jj = E / 2; jj >= 1; jj >>= 1) {
+          if (j != (uint32_t)jj) continue;
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            if (e & jj) continue;
+            const int f = e | jj;
+            const bool up = ((t * E + e) & k) == 0;
+            if (less(xk[f], xi[f], xk[e], xi[e]) == up) {
+              const uint64_t tk = xk[e];
+              const uint32_t ti = xi[e], tp = xp[e];
+              xk[e] = xk[f];
+              xi[e] = xi[f];
+              xp[e] = xp[f];
+              xk[f] = tk;
+              xi[f] = ti;
+              xp[f] = tp;
             }
           }
         }
+      } else if (j < (uint32_t)(kWave * E)) {
+        const int m = (int)(j / E);  // partner lane = lane ^ m
+        const bool take_min = ((lane & m) == 0) == (((t * E) & k) == 0);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const uint64_t pk = shfl_xor64(xk[e], m);
+          const uint32_t pi = (uint32_t)__shfl_xor((int)xi[e], m, kWave);
+          const uint32_t pp = PAYLOAD ? (uint32_t)__shfl_xor((int)xp[e], m, kWave) : 0u;
+          keep(e, take_min, pk, pi, pp);
+        }
+      } else {
+        const uint32_t m = j / E;  // partner thread = t ^ m, another wave
+        const bool take_min = ((t & m) == 0) == (((t * E) & k) == 0);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          key[t * E + e] = xk[e];
+          id[t * E + e] = xi[e];
+          if (PAYLOAD) pay[t * E + e] = xp[e];
+        }
+        block_sync();
+        const uint32_t pt = t ^ m;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+          keep(e, take_min, key[pt * E + e], id[pt * E + e], PAYLOAD ? pay[pt * E + e] : 0u);
+        block_sync();
       }
-      block_sync();
     }
   }
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    key[t * E + e] = xk[e];
+    id[t * E + e] = xi[e];
+    if (PAYLOAD) pay[t * E + e] = xp[e];
+  }
+  block_sync();
+}
+
+// Sorts the first n entries (n <= 8 * BT; entries from n up to the sort
+// size must hold the sentinel key ~0).
+template <bool PAYLOAD>
+__device__ void sort_pairs(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t n) {
+  if (n <= (uint32_t)BT) block_sort<1, PAYLOAD>(key, id, pay);
+  else if (n <= 2u * BT) block_sort<2, PAYLOAD>(key, id, pay);
+  else if (n <= 4u * BT) block_sort<4, PAYLOAD>(key, id, pay);
+  else block_sort<8, PAYLOAD>(key, id, pay);
+}
+
+__device__ __forceinline__ uint32_t sort_size(uint32_t n) {
+  return n <= (uint32_t)BT ? BT : n <= 2u * BT ? 2 * BT : n <= 4u * BT ? 4 * BT : 8 * BT;
 }
 
 // Number of entries of a sorted list below (k, i).
@@ -101,7 +171,7 @@ __global__ __launch_bounds__(BT) void b_select(SelArgs a) {
   const uint32_t nh = (uint32_t)min(a.b, a.n_heap);
   const uint32_t nc_in = nh + (uint32_t)a.n_buffer;
   const uint32_t no = (uint32_t)a.n_ongoing;
-  const uint32_t NC = pow2_at_least(max(nc_in, 1u)), NO = pow2_at_least(max(no, 1u));
+  const uint32_t NC = sort_size(nc_in), NO = sort_size(no);
   if (t == 0) sh.bad = 0;
   block_sync();
   // gather the keys; ids outside [0, n_ids) are reported and sort last
@@ -143,8 +213,8 @@ __global__ __launch_bounds__(BT) void b_select(SelArgs a) {
     }
     return;
   }
-  bitonic<false>(sh.ckey, sh.cid, nullptr, NC);
-  bitonic<false>(sh.okey, sh.oid, nullptr, NO);
+  sort_pairs<false>(sh.ckey, sh.cid, nullptr, nc_in);
+  sort_pairs<false>(sh.okey, sh.oid, nullptr, no);
   const uint32_t nc = min((uint32_t)a.b, nc_in);  // C = the first nc candidates
   if (nc == 0 && no == 0) {
     if (t == 0) a.counts[0] = a.counts[1] = 0;
@@ -224,7 +294,7 @@ __global__ __launch_bounds__(BT) void b_evict(EvictArgs a) {
   __shared__ EvictShared sh;
   const uint32_t t = threadIdx.x;
   const uint32_t nr = (uint32_t)a.n_cached;
-  const uint32_t N = pow2_at_least(max(nr, 1u));
+  const uint32_t N = sort_size(nr);
   if (t == 0) sh.bad = 0;
   block_sync();
   for (uint32_t i = t; i < N; i += BT) {
@@ -248,7 +318,7 @@ __global__ __launch_bounds__(BT) void b_evict(EvictArgs a) {
     if (t == 0) atomicOr(a.flags, (sh.bad & 1u) ? kFlagInval : kFlagRange);
     return;
   }
-  bitonic<true>(sh.key, sh.id, sh.src, N);
+  sort_pairs<true>(sh.key, sh.id, sh.src, nr);
   // KV sizes in eviction order (the sorted order read backwards), inclusive
   // prefix sums over a contiguous chunk per thread, kept in sh.key
   constexpr uint32_t PER = (kEvictCap + BT - 1) / BT;
