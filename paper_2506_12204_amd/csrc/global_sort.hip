@@ -1068,9 +1068,153 @@ __global__ __launch_bounds__(HT) void g_histF(GArgs a) {
   count_block(a, (int)pl->nscatter - 1, row, a.fin, kHistRows, true, sh.generic, HT);
 }
 
+// ---- fast middle pass ---------------------------------------------------------
+// Packed u64 elements (key above W id bits) moved by a 10-bit digit of u2,
+// with the big tiles, wave counters, owner offsets and rotated loop of the
+// fast first pass: a big tile of 16384 items writes runs of about 16
+// consecutive elements per digit, against 4 on the 4096-item tiles of the
+// generic scatter, so most written lines are whole.
+struct MidFastShared {
+  uint64_t stage[T1];
+  uint16_t cnt[NW][kMaxBins];  // wave counters, then the waves' tile offsets
+  uint32_t base[kMaxBins];     // output position of the tile's first item of a digit
+  uint32_t part[NW + 1];
+};
+
+__device__ void mid_fast(const GArgs& a, int s, int g, MidFastShared& sh) {
+  constexpr int NBIN = kMaxBins;
+  constexpr uint32_t M = NBIN - 1;
+  constexpr int OWN = NBIN / NT;  // digits per owning thread (every thread owns)
+  static_assert(OWN * NT == NBIN, "every digit has an owner");
+  const int t = threadIdx.x;
+  const int lane = lane_id();
+  const int w = wave_id();
+  const int wb = w * kWave * R1;
+  const Plan* pl = a.plan;
+  KeyCodec kc;
+  kc.init(a, pl);
+  const uint32_t dshift = pl->shift[s];
+  const uint64_t* in = a.keys[(s - 1) & 1];
+  uint64_t* out = a.keys[s & 1];
+  uint16_t* mycnt = sh.cnt[w];
+  clear_wave_counters<NBIN>(mycnt);
+  auto digit = [&](uint64_t e) { return (kc.u2(e >> kc.W) >> dshift) & M; };
+
+  uint32_t carry[OWN];
+  {
+    uint32_t c[OWN];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      c[i] = a.hist_cnt[s * kMaxBins + t * OWN + i];
+      sum += c[i];
+    }
+    uint32_t tot;
+    uint32_t ex = block_excl_scan_u32<NT>(sum, sh.part, tot);
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      carry[i] = ex + a.block_hist[(size_t)g * kMaxBins + t * OWN + i];
+      ex += c[i];
+    }
+  }
+
+  const int64_t lo = (int64_t)g * a.mid.tpb * T;
+  const int64_t hi = min(a.n, lo + (int64_t)a.mid.tpb * T);
+  uint64_t ev[R1];  // this tile's elements (the digits are recomputed from them)
+  uint32_t rk[R1];
+  auto tile_items = [&](int64_t tb) { return (int)min((int64_t)T1, hi - tb); };
+  // buffer loads over this wave's share of the tile: one scalar base, the
+  // lane's offset plus an immediate per round; items past the end read 0
+  auto load = [&](int64_t tb, uint64_t (&dst)[R1]) {
+    const int lim = __builtin_amdgcn_readfirstlane(
+        (int)max((int64_t)0, min(hi - tb - wb, (int64_t)kWave * R1)));
+    const __amdgpu_buffer_rsrc_t rs = raw_rsrc(in + tb + wb, (uint32_t)lim * 8u);
+#pragma unroll
+    for (int r = 0; r < R1; ++r) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, (lane + r * kWave) * 8, 0, 0);
+      dst[r] = (uint64_t)v[0] | ((uint64_t)v[1] << 32);
+    }
+  };
+  // items past the end take the last digit and rank after every real one
+  auto digit_at = [&](int r, int cv) { return wb + r * kWave + lane < cv ? digit(ev[r]) : M; };
+  auto rank = [&](int cv) {
+#pragma unroll
+    for (int r = 0; r < R1; ++r) rk[r] = rank_round_c<10>(digit_at(r, cv), mycnt);
+  };
+
+  if (lo < hi) {
+    load(lo, ev);
+    rank(tile_items(lo));
+  }
+  for (int64_t tb = lo; tb < hi; tb += T1) {
+    const int cv = tile_items(tb);
+    const bool more = tb + T1 < hi;
+    uint64_t nx[R1];  // the next tile's elements load while this one is offset and written
+    if (more) load(tb + T1, nx);
+    block_sync();  // every wave's counters are complete
+
+    uint32_t cw[OWN][NW], tot[OWN];
+    uint32_t local = 0;
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      tot[i] = 0;
+#pragma unroll
+      for (int v = 0; v < NW; ++v) {
+        cw[i][v] = sh.cnt[v][t * OWN + i];
+        tot[i] += cw[i][v];
+      }
+      local += tot[i];
+    }
+    const uint32_t incl = wave_incl_scan_u32(local);
+    if (lane == kWave - 1) sh.part[w] = incl;
+    block_sync();
+    uint32_t ex = incl - local;
+    for (int v = 0; v < w; ++v) ex += sh.part[v];  // (w is uniform)
+#pragma unroll
+    for (int i = 0; i < OWN; ++i) {
+      const int b = t * OWN + i;
+      uint32_t run = ex;
+#pragma unroll
+      for (int v = 0; v < NW; ++v) {
+        sh.cnt[v][b] = (uint16_t)run;
+        run += cw[i][v];
+      }
+      sh.base[b] = carry[i] - ex;
+      carry[i] += tot[i];
+      ex += tot[i];
+    }
+    block_sync();  // tile offsets and bases are written
+
+#pragma unroll
+    for (int r = 0; r < R1; ++r) rk[r] += mycnt[opaque(digit_at(r, cv))];
+    clear_wave_counters<NBIN>(mycnt);  // only this wave reads them until the next ranking
+#pragma unroll
+    for (int r = 0; r < R1; ++r) sh.stage[rk[r]] = ev[r];
+    block_sync();  // the tile is staged in digit order
+
+    const bool full = cv == T1;
+#pragma unroll
+    for (int r = 0; r < R1; ++r) {
+      const int j = wb + r * kWave + lane;
+      const uint64_t e = sh.stage[j];
+      const uint32_t pos = sh.base[digit(e)] + (uint32_t)j;
+      const bool item = (full || j < cv) && pos < (uint64_t)a.n;  // (pos < n for consistent counts)
+      uint64_t* po = item ? out + pos : a.sink;
+      *po = e;
+      if (r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
+    }
+    if (more) {
+#pragma unroll
+      for (int r = 0; r < R1; ++r) ev[r] = nx[r];
+      rank(tile_items(tb + T1));
+    }
+  }
+}
+
 // ---- middle passes: one launch of co-resident workgroups, grid barriers ----
 union MidShared {
   ScatterShared scatter;
+  MidFastShared fast;
   CountShared count;
   struct {
     uint32_t scan32[NT / kWave + 1];
@@ -1118,7 +1262,12 @@ __global__ __launch_bounds__(NT) void g_mid(GArgs a) {
     for (int b = blockIdx.x; b < (int)pl->nbins[s]; b += gridDim.x)
       column_scan<NT>(a, s, b, false, G, sh.scan.scan32, sh.scan.scan64);
     if (!grid_barrier(a, ++gen)) return;
-    if ((int)blockIdx.x < G) scatter_block<false>(a, s, blockIdx.x, a.mid, sh.scatter);
+    if ((int)blockIdx.x < G) {
+      if (pl->packed)
+        mid_fast(a, s, blockIdx.x, sh.fast);
+      else
+        scatter_block<false>(a, s, blockIdx.x, a.mid, sh.scatter);
+    }
     if (!grid_barrier(a, ++gen)) return;
   }
 }
@@ -2180,7 +2329,7 @@ Split global_final_split(int64_t n) {
 
 Split global_mid_split(int64_t n) {
   static const int r = resident_blocks(reinterpret_cast<const void*>(g_mid), NT);
-  return make_split(n, r, 1);
+  return make_split(n, r, kFirstTiles);  // the fast middle pass walks big tiles
 }
 
 hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEvents* ev) {
