@@ -105,6 +105,36 @@ __device__ __forceinline__ uint32_t rank_round_c(uint32_t d, uint16_t* cnt) {
   return rank;
 }
 
+// Stable per-wave ranking of one round by digit through a table of 64-bit
+// lane masks in LDS, one per digit, private to the wave and zero on entry and
+// on return. Every lane ORs its bit into its digit's mask, reads the mask
+// back (its peers: a wave's LDS operations complete in program order, so all
+// of the round's bits are in) and clears it again. Three LDS operations and
+// a few VALU ones, where matching the digit bit by bit with ballots takes
+// four VALU operations per bit. Returns, as rank_round_c, the number of
+// earlier items of the wave with the same digit and advances the counter.
+__device__ __forceinline__ uint32_t rank_round_mask(uint32_t d, u64_alias* masks,
+                                                    uint16_t* cnt) {
+  atomicOr(reinterpret_cast<unsigned long long*>(masks + d), 1ull << lane_id());
+  const uint64_t peers = masks[d];
+  masks[d] = 0;
+  const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+      (uint32_t)(peers >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
+  const uint32_t base = cnt[d];
+  cnt[d] = (uint16_t)(base + (uint32_t)__popcll(peers));
+  uint32_t rank = base + below;
+  asm volatile("" : "+v"(rank));
+  return rank;
+}
+
+// Zeroes NBIN u64 entries (a wave's mask table) with this wave's lanes.
+template <int NBIN>
+__device__ __forceinline__ void clear_wave_masks(u64_alias* masks) {
+  static_assert(NBIN % kWave == 0, "whole rounds of lanes");
+#pragma unroll
+  for (int i = 0; i < NBIN / kWave; ++i) masks[i * kWave + lane_id()] = 0;
+}
+
 // Hides a value's origin from the optimiser, so that an address derived from
 // it is recomputed after a barrier instead of being kept in a register.
 __device__ __forceinline__ uint32_t opaque(uint32_t v) {

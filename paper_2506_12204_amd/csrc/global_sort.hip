@@ -681,7 +681,11 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
   // key = (p - pmin) << (wh + d0) | ((l >> d0) - hmin) << d0 | (l & M0), or
   // for COMPACT u2 << d0 | (l & M0) with u2 = (p - pmin) * H + (l >> d0) - hmin;
   // either way its low D0 bits are the digit
+  // the ranking's lane masks live in this wave's slice of the stage, which
+  // only this wave reads after staging and is done with when it ranks
+  u64_alias* masks = reinterpret_cast<u64_alias*>(sh.stage + wb);
   auto rank_tile = [&](int cv) {
+    clear_wave_masks<NBIN>(masks);
 #pragma unroll
     for (int r = 0; r < R1; ++r)
       key[r] = (COMPACT ? (__umul24(pv[r] - pmin, H) << D0) : ((pv[r] - pmin) << psh)) +
@@ -694,7 +698,7 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
         if (wb + r * kWave + lane >= cv) key[r] |= M0;
     }
 #pragma unroll
-    for (int r = 0; r < R1; ++r) rk[r] = rank_round_c<D0>(key[r] & M0, mycnt);
+    for (int r = 0; r < R1; ++r) rk[r] = rank_round_mask(key[r] & M0, masks, mycnt);
   };
 
   load_first(a, lo, tile_items(lo), pv, lv);
@@ -798,6 +802,9 @@ struct CountShared {
   uint64_t w[kMaxBins];
 };
 
+// FEW: digits of at most 8 values are counted in registers (final-digit
+// histograms; the middle passes always have 1024 digits).
+template <bool FEW>
 __device__ void count_block(const GArgs& a, int s, int g, Split sp, int rows, bool weights,
                             CountShared& sh, int threads) {
   const Plan* pl = a.plan;
@@ -825,6 +832,29 @@ __device__ void count_block(const GArgs& a, int s, int g, Split sp, int rows, bo
     atomicAdd(&sh.cnt[d], 1u);
     if (weights) atomicAdd((unsigned long long*)&sh.w[d], (unsigned long long)kc.len(key));
   };
+  // With few digits every element would hit the same few LDS words: each
+  // lane then keeps its own counts and length sums in registers and the wave
+  // adds them up once at the end.
+  constexpr int kFew = 8;
+  uint32_t fc[kFew];
+  uint64_t fw[kFew];
+  const bool few = FEW && nb <= kFew;
+#pragma unroll
+  for (int b = 0; b < kFew; ++b) {
+    fc[b] = 0;
+    fw[b] = 0;
+  }
+  auto add_few = [&](uint64_t e) {
+    const uint64_t key = packed ? (e >> kc.W) : e;
+    const uint32_t d = (kc.u2(key) >> dshift) & dmask;
+    const uint64_t l = weights ? (uint64_t)kc.len(key) : 0;
+#pragma unroll
+    for (int b = 0; b < kFew; ++b) {
+      const bool on = d == (uint32_t)b;
+      fc[b] += on ? 1u : 0u;
+      fw[b] += on ? l : 0;
+    }
+  };
   for (int64_t q = q0 + t; q < q1; q += (int64_t)threads * HU) {
     ulonglong2 v[HU];
 #pragma unroll
@@ -832,8 +862,27 @@ __device__ void count_block(const GArgs& a, int s, int g, Split sp, int rows, bo
 #pragma unroll
     for (int u = 0; u < HU; ++u) {
       if (q + (int64_t)u * threads < q1) {
-        add(v[u].x);
-        add(v[u].y);
+        if (few) {
+          add_few(v[u].x);
+          add_few(v[u].y);
+        } else {
+          add(v[u].x);
+          add(v[u].y);
+        }
+      }
+    }
+  }
+  if (few) {
+#pragma unroll
+    for (int b = 0; b < kFew; ++b) {
+      if (b < nb) {  // (nb is uniform)
+        const uint32_t tc = (uint32_t)__builtin_amdgcn_readlane(
+            (int)wave_incl_scan_u32(fc[b]), kWave - 1);
+        const uint64_t tw = weights ? last_lane_u64(wave_incl_scan_u64(fw[b])) : 0;
+        if (lane_id() == 0) {
+          if (tc) atomicAdd(&sh.cnt[b], tc);
+          if (tw) atomicAdd((unsigned long long*)&sh.w[b], (unsigned long long)tw);
+        }
       }
     }
   }
@@ -1065,7 +1114,7 @@ __global__ __launch_bounds__(HT) void g_histF(GArgs a) {
       return;
     }
   }
-  count_block(a, (int)pl->nscatter - 1, row, a.fin, kHistRows, true, sh.generic, HT);
+  count_block<true>(a, (int)pl->nscatter - 1, row, a.fin, kHistRows, true, sh.generic, HT);
 }
 
 // ---- fast middle pass ---------------------------------------------------------
@@ -1257,7 +1306,7 @@ __global__ __launch_bounds__(NT) void g_mid(GArgs a) {
   const int G = a.mid.blocks;
   uint32_t gen = 0;
   for (int s = 1; s < S - 1; ++s) {
-    if ((int)blockIdx.x < G) count_block(a, s, blockIdx.x, a.mid, 1, false, sh.count, NT);
+    if ((int)blockIdx.x < G) count_block<false>(a, s, blockIdx.x, a.mid, 1, false, sh.count, NT);
     if (!grid_barrier(a, ++gen)) return;
     for (int b = blockIdx.x; b < (int)pl->nbins[s]; b += gridDim.x)
       column_scan<NT>(a, s, b, false, G, sh.scan.scan32, sh.scan.scan64);
@@ -2079,6 +2128,9 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
                                                    : (e[r] >> kChunkBits) & (MAXB - 1);
   };
   // ---- phase 1: decode, tile length sums per digit, ranks --------------
+  // (Ballot matching here: with at most 256 final digits many lanes of a
+  // round share a digit, and the lane-mask ranking of the first pass then
+  // serialises on its LDS atomics.)
   auto phase1 = [&](int64_t tb) {
     const int cv = tile_items(tb);
     // the sub-buckets this tile's positions lie in, then those of this wave's
