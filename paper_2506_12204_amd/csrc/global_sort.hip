@@ -1186,9 +1186,13 @@ __device__ void mid_fast(const GArgs& a, int s, int g, MidFastShared& sh) {
   };
   // items past the end take the last digit and rank after every real one
   auto digit_at = [&](int r, int cv) { return wb + r * kWave + lane < cv ? digit(ev[r]) : M; };
+  // lane-mask ranking, the masks in this wave's slice of the stage (as in the
+  // first pass)
+  u64_alias* masks = reinterpret_cast<u64_alias*>(sh.stage + wb);
   auto rank = [&](int cv) {
+    clear_wave_masks<NBIN>(masks);
 #pragma unroll
-    for (int r = 0; r < R1; ++r) rk[r] = rank_round_c<10>(digit_at(r, cv), mycnt);
+    for (int r = 0; r < R1; ++r) rk[r] = rank_round_mask(digit_at(r, cv), masks, mycnt);
   };
 
   if (lo < hi) {
