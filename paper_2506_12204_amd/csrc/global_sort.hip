@@ -588,6 +588,8 @@ __device__ __forceinline__ int wave_id() {
   return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
 }
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
 // Buffer resource over `bytes` bytes at `base` (raw, untyped). Loads through
 // it return 0 past the end instead of touching memory there.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, uint32_t bytes) {
@@ -2021,10 +2023,16 @@ struct FinalCompactShared {
   uint64_t clo[256], chi[256]; // class totals, low and high words
   uint32_t bstart[kMaxBins + 1];
   uint32_t win[kWinCap];       // absolute sub-bucket starts of this block's buckets
+  uint32_t lbase[MAXB];        // length of a digit's requests without the first digit
+  int32_t wd[NWB];             // a wave's one first digit in the tile, or -1
   uint32_t part_c[NWB + 1];
   uint64_t part_w[NWB + 1];
   uint64_t chunk[NWB];
 };
+
+// Requests below this count store through buffer resources (byte offsets of
+// the waits stay below 2^31); larger queues take the global-window kernel.
+constexpr int64_t kBufferStoreItems = 1ll << 28;
 
 __device__ __forceinline__ void load_final_compact(const uint32_t* keys, int64_t tb, int cnt,
                                                    uint32_t (&e)[KB]) {
@@ -2037,8 +2045,9 @@ __device__ __forceinline__ void load_final_compact(const uint32_t* keys, int64_t
     e[r] = __builtin_amdgcn_raw_buffer_load_b32(rk, (lane + r * kWave) * 4, 0, 0);
 }
 
-// WIN_LDS: the block's sub-bucket starts fit the LDS window; else they are
-// read from global memory (separate kernels, see g_final_cglb).
+// WIN_LDS: the block's sub-bucket starts fit the LDS window and n is below
+// kBufferStoreItems; else the starts are read from global memory and the
+// outputs stored through plain pointers (separate kernels, see g_final_cglb).
 template <bool WIN_LDS>
 __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   const int t = threadIdx.x;
@@ -2061,7 +2070,10 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   };
 
   clear_wave_counters<MAXB>(mycnt);
-  if (t < MAXB) sh.wsum[t] = 0;
+  if (t < MAXB) {
+    sh.wsum[t] = 0;
+    sh.lbase[t] = t < nb ? len_of((uint32_t)t, 0u) : 0u;
+  }
   if (t < 256) sh.clo[t] = sh.chi[t] = 0;
   bucket_starts<NTB>(a, sh.bstart, sh.part_c);
   uint32_t carry_c;
@@ -2098,7 +2110,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   const int d_hi = hi > lo ? bucket_of(sh.bstart, nd, (uint32_t)(hi - 1)) : 0;
   const int win0 = d_lo << kpb;
   const int wn = (d_hi - d_lo + 1) << kpb;
-  if (WIN_LDS != (wn <= kWinCap)) return;  // the other kernel's block
+  if (WIN_LDS != (wn <= kWinCap && a.n < kBufferStoreItems)) return;  // the other kernel's block
   if (WIN_LDS) {
     for (int j = t; j < wn; j += NTB)
       sh.win[j] = sh.bstart[(win0 + j) >> kpb] + a.sub_start[win0 + j];
@@ -2126,6 +2138,9 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   // only for the loads: the stores drain while the next tile is ranked.
   uint32_t e[KB];   // elements of the tile being ranked
   uint32_t rw[KB];  // per item: rank (below 2^14) | window index << 14 (below 2^18)
+  // output resources (used when n < kBufferStoreItems: byte offsets below 2^31)
+  const __amdgpu_buffer_rsrc_t rs_order = raw_rsrc(a.order, (uint32_t)a.n * 4u);
+  const __amdgpu_buffer_rsrc_t rs_wait = raw_rsrc(a.wait, (uint32_t)a.n * 8u);
   auto tile_items = [&](int64_t tb) { return (int)min((int64_t)TB, hi - tb); };
   auto digit_of = [&](int r, int cv) {  // past the end: the last digit
     return (cv < TB && wb + r * kWave + lane >= cv) ? (uint32_t)nb - 1
@@ -2135,6 +2150,11 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   // (Ballot matching here: with at most 256 final digits many lanes of a
   // round share a digit, and the lane-mask ranking of the first pass then
   // serialises on its LDS atomics.)
+  // A wave whose full share of the tile lies in one first-digit bucket d
+  // (nearly all: a bucket spans about n / 2^d0 positions) adds no lengths
+  // here: its requests of digit u2 contribute count * (lbase[u2] + d), which
+  // the digit's owner forms from the wave's counter. The other waves add each
+  // length to the digit's LDS sum.
   auto phase1 = [&](int64_t tb) {
     const int cv = tile_items(tb);
     // the sub-buckets this tile's positions lie in, then those of this wave's
@@ -2147,17 +2167,27 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
         find(min((uint32_t)(tb + wb), wlast), ja, jb));
     const int wjb = __builtin_amdgcn_readfirstlane(
         find(min((uint32_t)(tb + wb + kWave * KB - 1), wlast), wja, jb));
+    const int wda = (win0 + wja) >> kpb;
+    const bool one_digit = wda == ((win0 + wjb) >> kpb) && wb + kWave * KB <= cv;  // uniform
+    if (lane == 0) sh.wd[w] = one_digit ? wda : -1;
+    auto rank_items = [&](auto add_lengths) {
 #pragma unroll
-    for (int r = 0; r < KB; ++r) {
-      const int j = wb + r * kWave + lane;
-      const bool past = j >= cv;
-      const uint32_t jj = (uint32_t)find((uint32_t)(tb + j), wja, wjb);
-      const uint32_t d = (uint32_t)((win0 + (int)jj) >> kpb);
-      const uint32_t dg = digit_of(r, cv);
-      const uint32_t ls = past ? 0u : len_of(dg, d);
-      atomicAdd((unsigned long long*)&sh.wsum[dg], (unsigned long long)ls);
-      rw[r] = rank_round_c<8>(dg, mycnt) | (jj << 14);
-    }
+      for (int r = 0; r < KB; ++r) {
+        const int j = wb + r * kWave + lane;
+        const uint32_t jj = (uint32_t)find((uint32_t)(tb + j), wja, wjb);
+        const uint32_t dg = digit_of(r, cv);
+        if constexpr (decltype(add_lengths)::value) {
+          const uint32_t d = (uint32_t)((win0 + (int)jj) >> kpb);
+          const uint32_t ls = j >= cv ? 0u : sh.lbase[dg] + d;
+          atomicAdd((unsigned long long*)&sh.wsum[dg], (unsigned long long)ls);
+        }
+        rw[r] = rank_round_c<8>(dg, mycnt) | (jj << 14);
+      }
+    };
+    if (one_digit)
+      rank_items(std::false_type{});
+    else
+      rank_items(std::true_type{});
   };
 
   load_final_compact(keys_in, lo, tile_items(lo), e);
@@ -2171,9 +2201,15 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     uint32_t tot = 0;
     uint64_t ws = 0;
     if (owner) {
+      const uint32_t lb = sh.lbase[t];
 #pragma unroll
-      for (int v = 0; v < NWB; ++v) tot += sh.cnt[v][t];
-      ws = sh.wsum[t];
+      for (int v = 0; v < NWB; ++v) {
+        const uint32_t c = sh.cnt[v][t];
+        const int dv = sh.wd[v];
+        tot += c;
+        if (dv >= 0) ws += (uint64_t)c * (lb + (uint32_t)dv);
+      }
+      ws += sh.wsum[t];
       sh.wsum[t] = 0;
     }
     const uint32_t inc_c = wave_incl_scan_u32(tot);
@@ -2230,7 +2266,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
       uint32_t ls = 0;
       if (full || j < cv) {
         const uint32_t hw = (uint32_t)(sh.stage[j] >> 32);
-        ls = len_of(hw >> 10, hw & 1023u);
+        ls = sh.lbase[hw >> 10] + (hw & 1023u);
       }
       const uint32_t inc = wave_incl_scan_u32(ls);  // below 2^32: 64 lengths < 2^26
       exc[r] = inc - ls;
@@ -2242,8 +2278,9 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     uint64_t run = 0;
     for (int v = 0; v < w; ++v) run += sh.chunk[v];  // (w is uniform)
     // Stores are unconditional, so that the compiler counts them exactly:
-    // lanes without an item (past the end of the last, partial tile) write to
-    // the sink.
+    // lanes without an item (past the end of the last, partial tile) store
+    // at the end of the buffer resource, where the range check drops the
+    // store, or write to the sink (plain pointers).
 #pragma unroll
     for (int r = 0; r < KB; ++r) {
       const int j = wb + r * kWave + lane;
@@ -2253,10 +2290,17 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
       const uint32_t pos = sh.base_c[u2] + (uint32_t)j;
       const bool in_tile = full || j < cv;
       const bool item = in_tile && pos < (uint64_t)a.n;  // (pos < n for consistent counts)
-      int32_t* po = item ? a.order + pos : reinterpret_cast<int32_t*>(a.sink);
-      int64_t* pw = item ? a.wait + pos : reinterpret_cast<int64_t*>(a.sink + 1);
-      *po = (int32_t)(uint32_t)x;
-      *pw = (int64_t)wt;
+      if constexpr (WIN_LDS) {
+        const uint32_t slot = item ? pos : (uint32_t)a.n;
+        __builtin_amdgcn_raw_buffer_store_b32((uint32_t)x, rs_order, slot * 4u, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{(uint32_t)wt, (uint32_t)(wt >> 32)}, rs_wait,
+                                              slot * 8u, 0, 0);
+      } else {
+        int32_t* po = item ? a.order + pos : reinterpret_cast<int32_t*>(a.sink);
+        int64_t* pw = item ? a.wait + pos : reinterpret_cast<int64_t*>(a.sink + 1);
+        *po = (int32_t)(uint32_t)x;
+        *pw = (int64_t)wt;
+      }
       if (in_tile) {
         if (u2 >= cur_end) {  // a new class for this lane
           if (cur != ~0u) flush_class();
