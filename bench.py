@@ -56,13 +56,16 @@ WORKLOAD_TEXT = {
 }
 POLICY_COUNTERS = os.path.join(ROOT, "profiles", "policy_c3_counters.md")
 POLICY_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "policy.hip")
-# algorithmic bytes per request of the pass each policy's roofline is taken on
-# (FCFS and HPJF: rank and length read, order and wait written; SJF's class
-# pass: order and wait read, the rank gathered through the id)
+# The pass each policy's roofline is taken on: its name, the algorithmic
+# bytes per request (FCFS and HPJF: rank and length read, order and wait
+# written; SJF's final sort pass: its compact element read, order and wait
+# written), the stage whose events bracket it, the source file its counters
+# belong to.
 POLICY_PASS = {
-    "fcfs": ("f_write: identity order and waits", 17),
-    "hpjf": ("h_scatter: stable scatter by rank", 17),
-    "sjf": ("s_classes: per-class sums of the waits", 13),
+    "fcfs": ("f_write: identity order and waits", 17, "policy", POLICY_SOURCE),
+    "hpjf": ("h_scatter: stable scatter by rank", 17, "policy", POLICY_SOURCE),
+    "sjf": ("g_final_pay: final pass of the sort by (length, id), ranks carried "
+            "(order, waits, class totals)", 16, "final", FINAL_SOURCE),
 }
 
 
@@ -121,7 +124,8 @@ def counter_traffic(n: int, counters: str = COUNTERS, source: str = FINAL_SOURCE
             if ":" in line and not line.startswith(("|", "#", " ")):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip().strip("`")
-    if kv.get("code_sha256") != code_sha(source) or kv.get("n") != str(n):
+    sha = kv.get(prefix + "code_sha256", kv.get("code_sha256"))  # (a kernel may have its own)
+    if sha != code_sha(source) or kv.get("n") != str(n):
         return None
     key = prefix + "hbm_bytes_per_launch"
     return float(kv[key]) if key in kv else None
@@ -291,8 +295,9 @@ def bench_policy(args) -> int:
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record()
+    kernel, per_req, stage, source = POLICY_PASS[args.policy]
     for k in range(args.steps):
-        ss.trace_stage(ss.STAGE_POLICY, *pairs[k])
+        ss.trace_stage(ss.STAGE_FINAL if stage == "final" else ss.STAGE_POLICY, *pairs[k])
         sched.run(p, l)
     t1.record()
     torch.cuda.synchronize()
@@ -302,7 +307,6 @@ def bench_policy(args) -> int:
     for a, b in pairs:
         hip.destroy(a)
         hip.destroy(b)
-    kernel, per_req = POLICY_PASS[args.policy]
     print(f"[bench] {args.steps} schedules: {ms_step:.4f} ms each; {kernel}: {pass_ms:.4f} ms",
           file=sys.stderr, flush=True)
     pass_bytes = per_req * n
@@ -325,7 +329,7 @@ def bench_policy(args) -> int:
         "roofline": {
             "bound": "hbm", "kernel": kernel, "achieved": achieved,
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": counter_traffic(n, POLICY_COUNTERS, POLICY_SOURCE, args.policy + "."),
+            "traffic": counter_traffic(n, POLICY_COUNTERS, source, args.policy + "."),
             "bytes_per_launch": pass_bytes, "avg_launch_ms": pass_ms,
         },
     }

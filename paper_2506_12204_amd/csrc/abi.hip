@@ -157,8 +157,11 @@ int finish(void* ws, hipStream_t st) {
 }
 
 // Enqueue one queue (any n >= 0). Arguments already checked.
+// payload / pay_pmax (optional, SJF): ranks carried through the long-queue
+// path and their largest value; see GArgs.
 int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_classes,
-                  int32_t* order, int64_t* wait, sem_i128* totals, void* ws, hipStream_t st) {
+                  int32_t* order, int64_t* wait, sem_i128* totals, void* ws, hipStream_t st,
+                  const uint8_t* payload = nullptr, const uint32_t* pay_pmax = nullptr) {
   char* base = static_cast<char*>(ws);
   uint32_t* flags = reinterpret_cast<uint32_t*>(base);
   uint64_t* tot = reinterpret_cast<uint64_t*>(totals);
@@ -226,6 +229,8 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   g.ids[1] = reinterpret_cast<uint32_t*>(base + L.ids1);
   g.chunk_part = reinterpret_cast<uint32_t*>(base + L.chunk_part);
   g.sub_start = reinterpret_cast<uint32_t*>(base + L.sub_start);
+  g.payload = payload;
+  g.pay_pmax = pay_pmax;
   StageEvents ev = {};
   bool armed = false;
   {
@@ -469,18 +474,24 @@ int enqueue_policy(int policy, const uint8_t* p, const int32_t* l, int64_t n, in
   a.part = reinterpret_cast<uint64_t*>(base + L.part);
   a.sink = reinterpret_cast<uint64_t*>(base + L.sink);
   if (policy == SEM_POLICY_SJF) {
-    // the order by (length, id): the queue kernels with every rank read as 0
+    // The order by (length, id): the queue kernels with every rank read as
+    // 0. The largest rank comes first, so that a long queue's compact
+    // elements can carry the ranks to its final pass (then that pass splits
+    // the totals; else s_classes does, after it).
     uint32_t* zeros = reinterpret_cast<uint32_t*>(base + L.zeros);
-    if (launch_fill_zero(zeros, ((size_t)n + 3) / 4, st) != hipSuccess) return SEM_EDEVICE;
+    if (launch_fill_zero(zeros, ((size_t)n + 3) / 4, st) != hipSuccess ||
+        launch_fill_zero(a.pmax, 1, st) != hipSuccess ||
+        launch_policy_range(a, st) != hipSuccess)
+      return SEM_EDEVICE;
     const int rc = enqueue_queue(reinterpret_cast<const uint8_t*>(zeros), l, n, SEM_MAX_CLASSES,
-                                 order, wait, totals, ws, st);
+                                 order, wait, totals, ws, st, p, a.pmax);
     if (rc != SEM_OK) return rc;
-  } else if (launch_fill_zero(flags, 1, st) != hipSuccess) {
+    if (needs_global(n)) a.pay = &reinterpret_cast<const Plan*>(base + layout_for(n).plan)->pay;
+  } else if (launch_fill_zero(flags, 1, st) != hipSuccess ||
+             launch_fill_zero(a.pmax, 1, st) != hipSuccess ||
+             launch_fill_zero(tot32, tot_words, st) != hipSuccess) {
     return SEM_EDEVICE;
   }
-  if (launch_fill_zero(a.pmax, 1, st) != hipSuccess ||
-      launch_fill_zero(tot32, tot_words, st) != hipSuccess)
-    return SEM_EDEVICE;
   hipEvent_t before = nullptr, after = nullptr;
   {
     std::lock_guard<std::mutex> guard(trace_mu());

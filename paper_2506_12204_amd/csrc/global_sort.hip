@@ -56,6 +56,8 @@ __global__ __launch_bounds__(1024) void g_reset(GArgs a) {
     a.flags[0] = 0;
     a.barrier[0] = 0;
     a.plan->ok = 0;
+    a.plan->pay = 0;
+    a.plan->pay_shift = 32;
   }
   for (int i = t; i < kMaxScatter * kMaxBins; i += 1024) a.hist_cnt[i] = 0;
   for (int i = t; i < kMaxBins; i += 1024) a.hist_w[i] = 0;
@@ -173,6 +175,16 @@ __device__ void write_plan(const GArgs& a, int G) {
   // compact layout: two passes, at most 256 final digits (the big-tile final
   // pass), lengths below 2^26, and the sub-bucket starts were counted
   pl->compact = (a.chunked && !a.force_wide && mids == 0 && fb <= 256 && pl->small) ? 1u : 0u;
+  // carried ranks: above the final digit's bits, if they fit the u32 element
+  pl->pay = 0;
+  pl->pay_shift = 32;
+  if (pl->compact && a.payload) {
+    const uint32_t at = kChunkBits + bit_width32(fb - 1);
+    if (at + bit_width32(*a.pay_pmax) <= 32) {
+      pl->pay = 1;
+      pl->pay_shift = at;
+    }
+  }
   pl->ok = 1;
 }
 
@@ -600,12 +612,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, uin
 // Inputs of one big tile of `cnt` items starting at item tb, round-major per
 // wave (round r of wave w holds items w*64*R1 + r*64 + lane). Items past the
 // tile's end read as zero.
-__device__ __forceinline__ void load_first(const GArgs& a, int64_t tb, int cnt,
+__device__ __forceinline__ void load_first(const GArgs& a, const uint8_t* pri, int64_t tb, int cnt,
                                            uint32_t (&pv)[R1], uint32_t (&lv)[R1]) {
   const int wb = wave_id() * kWave * R1;
   // items of this wave's share (uniform; stated so the descriptor stays scalar)
   const int lim = __builtin_amdgcn_readfirstlane(max(0, min(cnt - wb, kWave * R1)));
-  const __amdgpu_buffer_rsrc_t rp = raw_rsrc(a.priority + tb + wb, (uint32_t)lim);
+  const __amdgpu_buffer_rsrc_t rp = raw_rsrc(pri + tb + wb, (uint32_t)lim);
   const __amdgpu_buffer_rsrc_t rl = raw_rsrc(a.length + tb + wb, (uint32_t)lim * 4u);
   const int lane = lane_id();
 #pragma unroll
@@ -629,7 +641,10 @@ __device__ __forceinline__ void clear_wave_counters(uint16_t* cnt) {
 // COMPACT: the element written is the compact u32 (final digit u2 above the
 // low kChunkBits bits of the id); the key ranked and staged is then
 // u2 << D0 | first digit instead of the packed key.
-template <int D0, bool COMPACT>
+// PAY (compact only): the ordering ranks are all zero (u2 = h) and the
+// caller's ranks (GArgs::payload) ride along: bits 24 and up of the staged
+// key, then bits pay_shift and up of the element.
+template <int D0, bool COMPACT, bool PAY>
 __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
   constexpr int NBIN = 1 << D0;
   constexpr uint32_t M0 = NBIN - 1;
@@ -645,6 +660,8 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
   const uint32_t psh = pl->wh + D0;
   const uint32_t hoff = pl->hmin << D0;
   const uint32_t H = pl->H;
+  const uint32_t pay_shift = pl->pay_shift;
+  const uint8_t* pri = PAY ? a.payload : a.priority;
   uint64_t* out = a.keys[0];
   uint32_t* out32 = reinterpret_cast<uint32_t*>(a.keys[0]);
   uint16_t* mycnt = sh.cnt[w];
@@ -690,8 +707,9 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
     clear_wave_masks<NBIN>(masks);
 #pragma unroll
     for (int r = 0; r < R1; ++r)
-      key[r] = (COMPACT ? (__umul24(pv[r] - pmin, H) << D0) : ((pv[r] - pmin) << psh)) +
-               (lv[r] - hoff);
+      key[r] = PAY ? ((pv[r] << 24) | (lv[r] - hoff))  // (u2 << D0 < 2^18)
+                   : (COMPACT ? (__umul24(pv[r] - pmin, H) << D0) : ((pv[r] - pmin) << psh)) +
+                         (lv[r] - hoff);
     if (cv < T1) {
       // items past the end take the last digit: they rank after every real
       // item of it, i.e. at the tile positions >= cv, which are not written
@@ -703,13 +721,13 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
     for (int r = 0; r < R1; ++r) rk[r] = rank_round_mask(key[r] & M0, masks, mycnt);
   };
 
-  load_first(a, lo, tile_items(lo), pv, lv);
+  load_first(a, pri, lo, tile_items(lo), pv, lv);
   rank_tile(tile_items(lo));
   for (int64_t tb = lo; tb < hi; tb += T1) {
     const int cv = tile_items(tb);
     const bool more = tb + T1 < hi;
     // the next tile's inputs load while this one is offset, staged and written
-    if (more) load_first(a, tb + T1, tile_items(tb + T1), pv, lv);
+    if (more) load_first(a, pri, tb + T1, tile_items(tb + T1), pv, lv);
     block_sync();  // every wave's counters are complete
 
     uint32_t cw[OWN][NW], tot[OWN];
@@ -762,9 +780,12 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
       const uint64_t e = sh.stage[j];
       const uint32_t pos = sh.base[(uint32_t)(e >> 32) & M0] + (uint32_t)j;
       const bool item = (full || j < cv) && pos < (uint64_t)a.n;  // (pos < n for consistent counts)
-      if (COMPACT) {  // u2 above the id's low bits
+      if (COMPACT) {  // u2 above the id's low bits (and the carried rank above u2)
         uint32_t* po = item ? out32 + pos : reinterpret_cast<uint32_t*>(a.sink);
-        *po = (((uint32_t)(e >> 32) >> D0) << kChunkBits) | ((uint32_t)e & ((1u << kChunkBits) - 1));
+        const uint32_t hi = (uint32_t)(e >> 32);
+        const uint32_t u2 = PAY ? (hi & 0xffffffu) >> D0 : hi >> D0;
+        const uint32_t rank_bits = PAY ? (hi >> 24) << pay_shift : 0u;
+        *po = rank_bits | (u2 << kChunkBits) | ((uint32_t)e & ((1u << kChunkBits) - 1));
       } else {
         uint64_t* po = item ? out + pos : a.sink;
         *po = e;
@@ -790,10 +811,12 @@ __global__ __launch_bounds__(NT, 2) void g_first(GArgs a) {
   } sh;
   const Plan* pl = a.plan;
   if (!pl->ok) return;
-  if (pl->compact)
-    first_fast<D0, true>(a, blockIdx.x, sh.fast);
+  if (pl->compact && pl->pay)
+    first_fast<D0, true, true>(a, blockIdx.x, sh.fast);
+  else if (pl->compact)
+    first_fast<D0, true, false>(a, blockIdx.x, sh.fast);
   else if (pl->packed && pl->W == 32)
-    first_fast<D0, false>(a, blockIdx.x, sh.fast);
+    first_fast<D0, false, false>(a, blockIdx.x, sh.fast);
   else
     scatter_block<true>(a, 0, blockIdx.x, a.main, sh.generic);
 }
@@ -1045,9 +1068,10 @@ __device__ void histF_compact(const GArgs& a, int row, int64_t lo, int64_t hi,
     d = bucket_of(sh.bstart, nd, (uint32_t)(4 * (q0 + t)));
     nxt = sh.bstart[d + 1];
   }
+  const uint32_t dbits = pl->pay_shift - kChunkBits;  // digit bits (carried ranks above)
   auto add = [&](uint32_t e, uint32_t pos) {
     while (pos >= nxt) nxt = sh.bstart[++d + 1];
-    atomicAdd((unsigned long long*)&bins[(e >> kChunkBits) & (kHistFBins - 1)],
+    atomicAdd((unsigned long long*)&bins[__builtin_amdgcn_ubfe(e, kChunkBits, dbits)],
               (unsigned long long)((1ull << CSH) | (uint32_t)d));
   };
   for (int64_t q = q0 + t; q < q1; q += (int64_t)HT * HU) {
@@ -2048,7 +2072,9 @@ __device__ __forceinline__ void load_final_compact(const uint32_t* keys, int64_t
 // WIN_LDS: the block's sub-bucket starts fit the LDS window and n is below
 // kBufferStoreItems; else the starts are read from global memory and the
 // outputs stored through plain pointers (separate kernels, see g_final_cglb).
-template <bool WIN_LDS>
+// PAY: the elements carry the caller's ranks (Plan::pay); the totals are
+// split by those instead of by the ordering classes.
+template <bool WIN_LDS, bool PAY>
 __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   const int t = threadIdx.x;
   const int lane = lane_id();
@@ -2063,6 +2089,8 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   const uint32_t hmin = pl->hmin;
   const uint32_t magic = div_magic(H);
   const int kpb = a.kpb;
+  const uint32_t pay_shift = pl->pay_shift;
+  const uint32_t dbits = pay_shift - kChunkBits;  // digit bits (carried ranks above)
   const uint32_t* keys_in = reinterpret_cast<const uint32_t*>(a.keys[0]);
   uint16_t* mycnt = sh.cnt[w];
   auto len_of = [&](uint32_t u2, uint32_t d) {
@@ -2144,7 +2172,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   auto tile_items = [&](int64_t tb) { return (int)min((int64_t)TB, hi - tb); };
   auto digit_of = [&](int r, int cv) {  // past the end: the last digit
     return (cv < TB && wb + r * kWave + lane >= cv) ? (uint32_t)nb - 1
-                                                   : (e[r] >> kChunkBits) & (MAXB - 1);
+                                                   : __builtin_amdgcn_ubfe(e[r], kChunkBits, dbits);
   };
   // ---- phase 1: decode, tile length sums per digit, ranks --------------
   // (Ballot matching here: with at most 256 final digits many lanes of a
@@ -2251,7 +2279,8 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
       const uint32_t d = (uint32_t)(idx >> kpb);
       const uint32_t id = ((uint32_t)(idx & ((1 << kpb) - 1)) << kChunkBits) |
                           (e[r] & ((1u << kChunkBits) - 1));
-      sh.stage[rk[r]] = ((uint64_t)((digit_of(r, cv) << 10) | d) << 32) | id;
+      const uint32_t rank_bits = PAY ? (e[r] >> pay_shift) << 18 : 0u;
+      sh.stage[rk[r]] = ((uint64_t)(rank_bits | (digit_of(r, cv) << 10) | d) << 32) | id;
     }
     const bool more = tb + TB < hi;
     if (more) load_final_compact(keys_in, tb + TB, tile_items(tb + TB), e);
@@ -2266,7 +2295,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
       uint32_t ls = 0;
       if (full || j < cv) {
         const uint32_t hw = (uint32_t)(sh.stage[j] >> 32);
-        ls = sh.lbase[hw >> 10] + (hw & 1023u);
+        ls = sh.lbase[PAY ? (hw >> 10) & (MAXB - 1) : hw >> 10] + (hw & 1023u);
       }
       const uint32_t inc = wave_incl_scan_u32(ls);  // below 2^32: 64 lengths < 2^26
       exc[r] = inc - ls;
@@ -2285,7 +2314,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     for (int r = 0; r < KB; ++r) {
       const int j = wb + r * kWave + lane;
       const uint64_t x = sh.stage[j];
-      const uint32_t u2 = (uint32_t)(x >> 42);
+      const uint32_t u2 = PAY ? (uint32_t)(x >> 42) & (MAXB - 1) : (uint32_t)(x >> 42);
       const uint64_t wt = sh.base_w[u2] + run + exc[r];
       const uint32_t pos = sh.base_c[u2] + (uint32_t)j;
       const bool in_tile = full || j < cv;
@@ -2302,7 +2331,13 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
         *pw = (int64_t)wt;
       }
       if (in_tile) {
-        if (u2 >= cur_end) {  // a new class for this lane
+        if constexpr (PAY) {  // the carried rank, in no particular order
+          const uint32_t c = (uint32_t)(x >> 50);
+          if (c != cur) {
+            if (cur != ~0u) flush_class();
+            cur = c;
+          }
+        } else if (u2 >= cur_end) {  // a new class for this lane
           if (cur != ~0u) flush_class();
           cur = class_of(u2, magic);  // class - pmin
           cur_end = __umul24(cur + 1, H);
@@ -2317,10 +2352,11 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     if (more) phase1(tb + TB);
   }
   block_sync();  // every lane's total is in
-  const int P = (int)pl->P;
+  // (carried ranks are the caller's ranks themselves)
+  const int P = PAY ? (int)*a.pay_pmax + 1 : (int)pl->P;
   for (int c = t; c < P; c += NTB) {
     U128 v = {sh.clo[c], sh.chi[c]};
-    const int cls = c + (int)pl->pmin;
+    const int cls = c + (PAY ? 0 : (int)pl->pmin);
     if (v.lo | v.hi) atomic_add128(a.totals + 2 * (1 + cls), a.totals + 2 * (1 + cls) + 1, v);
   }
   if (t == 0) {
@@ -2341,7 +2377,7 @@ __global__ __launch_bounds__(NTB) void g_final_big(GArgs a) {
   const Plan* pl = a.plan;
   if (!pl->ok) return;
   if (pl->compact) {
-    final_compact<true>(a, blockIdx.x, sh.compact);
+    if (!pl->pay) final_compact<true, false>(a, blockIdx.x, sh.compact);
     return;
   }
   if (!use_big_final(pl)) return;
@@ -2356,8 +2392,25 @@ __global__ __launch_bounds__(NTB) void g_final_big(GArgs a) {
 __global__ __launch_bounds__(NTB) void g_final_cglb(GArgs a) {
   __shared__ FinalCompactShared sh;
   const Plan* pl = a.plan;
-  if (!pl->ok || !pl->compact) return;
-  final_compact<false>(a, blockIdx.x, sh);
+  if (!pl->ok || !pl->compact || pl->pay) return;
+  final_compact<false, false>(a, blockIdx.x, sh);
+}
+
+// The compact final pass with carried ranks, in kernels of their own (one
+// kernel holding both forms would spill registers), launched only when the
+// caller passed ranks to carry.
+__global__ __launch_bounds__(NTB) void g_final_pay(GArgs a) {
+  __shared__ FinalCompactShared sh;
+  const Plan* pl = a.plan;
+  if (!pl->ok || !pl->compact || !pl->pay) return;
+  final_compact<true, true>(a, blockIdx.x, sh);
+}
+
+__global__ __launch_bounds__(NTB) void g_final_pay_cglb(GArgs a) {
+  __shared__ FinalCompactShared sh;
+  const Plan* pl = a.plan;
+  if (!pl->ok || !pl->compact || !pl->pay) return;
+  final_compact<false, true>(a, blockIdx.x, sh);
 }
 
 template <typename unused = void>
@@ -2459,6 +2512,10 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   // exactly one of the two does the work; the plan on the device decides
   hipLaunchKernelGGL(g_final_big, gf, dim3(NTB), 0, st, a);
   if (a.chunked) hipLaunchKernelGGL(g_final_cglb, gf, dim3(NTB), 0, st, a);
+  if (a.chunked && a.payload) {
+    hipLaunchKernelGGL(g_final_pay, gf, dim3(NTB), 0, st, a);
+    hipLaunchKernelGGL(g_final_pay_cglb, gf, dim3(NTB), 0, st, a);
+  }
   hipLaunchKernelGGL(g_final<>, gf, dim3(NT), 0, st, a);
   mark(ev, 2, true, st);
   return hipGetLastError();

@@ -76,6 +76,9 @@ struct Plan {
   uint32_t small;     // 1: every length < 2^26 (64-lane length sums fit 32 bits)
   uint32_t nscatter;  // number of scatter passes (>= 2)
   uint32_t compact;   // 1: the compact two-pass layout (u32 elements) is used
+  uint32_t pay;       // 1: compact elements also carry the caller's rank above the
+                      // final digit (the rank takes no part in the order)
+  uint32_t pay_shift; // bit of a compact element where that rank starts
   uint32_t shift[kMaxScatter];  // digit = (u2 >> shift) & (bins - 1), passes >= 1
   uint32_t nbits[kMaxScatter];
   uint32_t nbins[kMaxScatter];
@@ -122,6 +125,12 @@ struct GArgs {
                         // chunk boundary k's block that lie below the boundary
   uint32_t* sub_start;  // [kMaxBins][Kp] start of sub-bucket (digit d, chunk k)
                         // relative to bucket d's start; k >= K hold the bucket size
+  // Optional (SJF): ranks carried through the sort but not ordered by, and
+  // their largest value (written by an earlier kernel). When the compact
+  // layout has room for them, the final pass splits the totals by these
+  // ranks instead of by `priority`.
+  const uint8_t* payload;
+  const uint32_t* pay_pmax;
 };
 
 // Optional events recorded around one stage's kernel (null: not armed).
@@ -179,7 +188,7 @@ struct PolArgs {
   int64_t n;
   int32_t* order;           // [n] (SJF: the schedule already computed)
   int64_t* wait;            // [n]
-  uint64_t* totals;         // (lo, hi) pairs, 1 + 256, zeroed by the caller
+  uint64_t* totals;         // (lo, hi) pairs, 1 + 256, zeroed by the caller (FCFS, HPJF)
   uint32_t* flags;          // device error bits
   uint32_t* pmax;           // largest rank, zeroed by the caller
   uint64_t* rsum;           // [ranges] FCFS: length sum per range, then range offsets
@@ -189,6 +198,8 @@ struct PolArgs {
   uint64_t* ctot_len;       // [256] HPJF: class length totals
   uint64_t* part;           // [blocks * P] (lo, hi) per-block class sums
   uint64_t* sink;           // 16 bytes for the stores of lanes without an element
+  const uint32_t* pay;      // SJF: nonzero once the sort split the totals by rank itself
+                            // (the plan's flag; null when the sort has no plan)
 };
 
 int64_t policy_ranges(int64_t n);
@@ -197,6 +208,9 @@ int64_t policy_blocks(int64_t n);
 // the schedule (FCFS, HPJF) or sums the classes (SJF).
 hipError_t launch_fcfs(const PolArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after);
 hipError_t launch_hpjf(const PolArgs& a, hipStream_t st, hipEvent_t before, hipEvent_t after);
+// Largest rank of a.priority into a.pmax (zeroed by the caller).
+hipError_t launch_policy_range(const PolArgs& a, hipStream_t st);
+// SJF's class sums after the sort; the caller ran launch_policy_range.
 hipError_t launch_class_totals(const PolArgs& a, hipStream_t st, hipEvent_t before,
                                hipEvent_t after);
 

@@ -25,8 +25,11 @@
 //              (class start + range offset + rank among its class in the
 //              range) with wait = the same prefix of lengths
 //   SJF        the semantic kernels with every rank read as 0 (the order by
-//              (length, id)), then s_classes: per-class sums of the waits
-//              with each position's rank gathered through its id
+//              (length, id)); where their compact layout has room, the
+//              elements carry the caller's ranks and the final pass splits
+//              the totals by them (s_classes and p_total then return at
+//              once); else s_classes: per-class sums of the waits with each
+//              position's rank gathered through its id
 //   p_total    adds the per-block class sums of the last pass: totals
 #include <algorithm>
 
@@ -696,6 +699,10 @@ __device__ __forceinline__ void class_sums(const PolArgs& a, int64_t ranges, Par
 template <bool REG>
 __global__ __launch_bounds__(PT) void s_classes(PolArgs a, int64_t ranges) {
   __shared__ PartShared sh;
+  if (a.pay && *a.pay) return;  // the sort split the totals already
+  // The sort left its own grand total; p_total adds the class sums to a
+  // zero one (no other kernel touches it until p_total).
+  if (REG && blockIdx.x == 0 && threadIdx.x < 2) a.totals[threadIdx.x] = 0;
   const uint32_t P = class_count(a);
   if (REG != (P <= kRegClasses)) return;
   zero_partials(sh);
@@ -703,10 +710,11 @@ __global__ __launch_bounds__(PT) void s_classes(PolArgs a, int64_t ranges) {
   else class_sums<0, 4>(a, ranges, sh, P);
 }
 
-// Block c: class c's total from the blocks' partial sums; added to the grand
-// total as well. totals were zeroed before.
+// Block c: class c's total from the blocks' partial sums (written over the
+// entry); added to the grand total as well, which was zeroed before.
 __global__ __launch_bounds__(PT) void p_total(PolArgs a, int64_t blocks) {
   __shared__ U128 ws[kWaves];
+  if (a.pay && *a.pay) return;
   const uint32_t P = class_count(a);
   const uint32_t c = blockIdx.x;
   if (c >= P) return;
@@ -771,10 +779,11 @@ hipError_t launch_hpjf(const PolArgs& a, hipStream_t st, hipEvent_t before, hipE
   return hipGetLastError();
 }
 
+hipError_t launch_policy_range(const PolArgs& a, hipStream_t st) { return launch_p_range(a, st); }
+
 hipError_t launch_class_totals(const PolArgs& a, hipStream_t st, hipEvent_t before,
                                hipEvent_t after) {
   const int64_t ranges = ranges_of(a.n), blocks = blocks_of(a.n);
-  if (launch_p_range(a, st) != hipSuccess) return hipGetLastError();
   mark(before, st);
   hipLaunchKernelGGL(s_classes<true>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);
   hipLaunchKernelGGL(s_classes<false>, dim3((unsigned)blocks), dim3(PT), 0, st, a, ranges);

@@ -101,3 +101,22 @@ def test_policy_empty_and_errors():
 def test_semantic_policy_is_sem_schedule():
     p, l = fuzz_queue(50000, seed=3, classes=5, max_len=900, tie_frac=0.2)
     check(p, l, POLICY_SEMANTIC, "semantic")
+
+
+@pytest.mark.parametrize("classes,max_len", [(4, 2**18 - 1), (5, 2**18 - 1), (8, 2**17 - 1),
+                                             (9, 2**17 - 1), (256, 4095), (256, 4096)])
+def test_sjf_carried_ranks_either_side_of_the_fit(classes, max_len):
+    # A long SJF queue in the compact layout carries the ranks through the
+    # sort when final-digit bits + rank bits fit above the 22 id bits
+    # (4 ranks with 256 final digits fit, 5 do not; 8 ranks with 128 digits
+    # fit, 9 do not; 256 ranks fit with 4 digits, lengths below 4096, not
+    # with 5); otherwise
+    # the class sums gather every position's rank. Both sides must agree
+    # with the oracle.
+    rng = np.random.default_rng(classes * 7 + max_len % 97)
+    n = 70000
+    p = rng.integers(0, classes, n).astype(np.uint8)
+    p[0] = classes - 1  # the largest rank is present
+    l = rng.integers(0, max_len + 1, n).astype(np.int32)
+    l[1], l[2] = 0, max_len  # the full length range is present
+    check(p, l, POLICY_SJF, f"classes={classes} max_len={max_len}")
