@@ -509,10 +509,12 @@ __global__ __launch_bounds__(ST) void h_scan(PolArgs a, int64_t ranges) {
 // One range of the stable scatter by rank. Every lane's element goes to
 // (running position of its class) + (rank among the round's lanes of that
 // class) with wait = (running wait of its class) + (lengths of those lanes
-// before it). PB > 0: at most PB classes, walked in an unrolled loop with
-// their running position and wait in scalar registers, class sums of the
+// before it). PB > 0: at most PB classes with their running position and
+// wait in scalar registers; a round's lanes are permuted into (class, lane)
+// order, one wave scan of the permuted lengths gives every lane its prefix,
+// and the prefix at the start of its class is subtracted; class sums of the
 // waits in lane registers. PB = 0: the class loop over the ranks present,
-// running values and sums in lane tables.
+// one masked scan per rank, running values and sums in lane tables.
 template <int PB, int SETS>
 __device__ __forceinline__ void hpjf_range(const PolArgs& a, int64_t w, int64_t ranges,
                                            uint32_t P, PartShared& sh) {
@@ -586,11 +588,58 @@ __device__ __forceinline__ void hpjf_range(const PolArgs& a, int64_t w, int64_t 
       };
       const uint64_t lmask = __ballot(live);
       if constexpr (PB > 0) {
+        // this lane's class: its live lanes, the live lanes of lower
+        // classes, its running position and wait (lanes without an element
+        // rank after every live lane, among themselves)
+        uint64_t mine = ~lmask;
+        uint32_t below = (uint32_t)__popcll(lmask);
+        uint32_t pbase = 0;
+        uint64_t wbase = 0;
+        uint32_t first[PB + 1];  // (uniform) slot of each class's first lane
+        uint32_t seen = 0;
+#pragma unroll
+        for (int c = 0; c < PB; ++c) {
+          first[c] = seen;
+          if (c < (int)P) {
+            const bool on = live && cls == (uint32_t)c;
+            const uint64_t peers = __ballot(on);
+            mine = on ? peers : mine;
+            below = on ? seen : below;
+            pbase = on ? spos[c] : pbase;
+            wbase = on ? swb[c] : wbase;
+            seen += (uint32_t)__popcll(peers);
+          }
+        }
+        first[PB] = seen;
+        const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
+            (uint32_t)(mine >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mine, 0u));
+        const uint32_t slot = below + rank;  // a permutation of the 64 lanes
+        // lengths in (class, lane) order, their inclusive scan, read back at
+        // this lane's slot and at the slot before its class
+        const uint32_t sl = (uint32_t)__builtin_amdgcn_ds_permute((int)(slot * 4), (int)lv);
+        const uint64_t incl = wave_incl_scan_len(sl);
+        auto pull = [&](uint32_t from) {
+          const uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(from * 4),
+                                                                     (int)(uint32_t)incl);
+          const uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(
+              (int)(from * 4), (int)(uint32_t)(incl >> 32));
+          return (uint64_t)hi << 32 | lo;
+        };
+        const uint64_t at = pull(slot);
+        const uint64_t before = pull(below > 0 ? below - 1 : 0);
+        const uint64_t ahead = below > 0 ? before : 0;  // lengths of the lower classes
+        q = pbase + rank;
+        wt = wbase + (at - lv - ahead);
+        // running positions and waits: each class's count and length sum
+        uint64_t lp = 0;  // (uniform) scan value before class c's first slot
 #pragma unroll
         for (int c = 0; c < PB; ++c) {
           if (c < (int)P) {
-            const uint64_t peers = __ballot(cls == (uint32_t)c) & lmask;
-            if (peers) place(peers, spos[c], swb[c], spos[c], swb[c]);
+            const uint32_t e = first[c + 1];
+            const uint64_t le = e > 0 ? readlane_u64(incl, (int)e - 1) : 0;
+            spos[c] += e - first[c];
+            swb[c] += le - lp;
+            lp = le;
           }
         }
         rs.add(cls, live ? wt : 0, P);
