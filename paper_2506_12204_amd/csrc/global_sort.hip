@@ -420,14 +420,16 @@ struct KeyCodec {
 
 // Stable rank of the tile's K rounds by digit: on return rk[r] is the position
 // of item (wave, round r, lane) in the tile's digit-sorted order and excl[b]
-// the number of the tile's items with digit < b.
+// the number of the tile's items with digit < b. NB: bits matched (every
+// digit is below 2^NB).
+template <int NB = 10>
 __device__ __forceinline__ void rank_tile(const uint32_t (&dg)[K], uint32_t (&rk)[K],
                                           int nb, int nbits, uint16_t* cnt, uint32_t* excl,
                                           uint32_t* scan32) {
   const int w = threadIdx.x / kWave;
   for (int b = lane_id(); b < nb; b += kWave) cnt[w * kMaxBins + b] = 0;
 #pragma unroll
-  for (int r = 0; r < K; ++r) rk[r] = rank_round_c<10>(dg[r], cnt + w * kMaxBins);
+  for (int r = 0; r < K; ++r) rk[r] = rank_round_c<NB>(dg[r], cnt + w * kMaxBins);
   block_sync();
   block_digit_offsets<NT>(cnt, kMaxBins, nb, excl, scan32);
 #pragma unroll
@@ -1291,14 +1293,115 @@ __device__ void mid_fast(const GArgs& a, int s, int g, MidFastShared& sh) {
 }
 
 // ---- middle passes: one launch of co-resident workgroups, grid barriers ----
+// Digit counts of one block of a middle pass: every wave counts into a table
+// of its own (no LDS atomics between waves), summed at the end.
+struct CountMidShared {
+  uint32_t cnt[NW][kMaxBins];
+};
+
+__device__ void count_mid(const GArgs& a, int s, int g, CountMidShared& sh) {
+  const Plan* pl = a.plan;
+  const int t = threadIdx.x;
+  const int w = t / kWave;
+  const uint32_t dshift = pl->shift[s];
+  constexpr uint32_t M = kMaxBins - 1;  // middle passes have 1024 digits
+  KeyCodec kc;
+  kc.init(a, pl);
+  const bool packed = pl->packed != 0;
+  const uint64_t* keys_in = a.keys[(s - 1) & 1];
+  uint32_t* flat = &sh.cnt[0][0];
+  for (int i = t; i < NW * kMaxBins; i += NT) flat[i] = 0;
+  block_sync();
+  int64_t lo, hi;
+  row_range(a, a.mid, g, 1, lo, hi);
+  uint32_t* mine = sh.cnt[w];
+  auto add = [&](uint64_t e) {
+    const uint64_t key = packed ? (e >> kc.W) : e;
+    atomicAdd(&mine[(kc.u2(key) >> dshift) & M], 1u);
+  };
+  // lo is even (a multiple of the tile), so pairs of elements stay aligned
+  const int64_t q0 = lo >> 1, q1 = hi >> 1;
+  const ulonglong2* k2 = reinterpret_cast<const ulonglong2*>(keys_in);
+  for (int64_t q = q0 + t; q < q1; q += (int64_t)NT * HU) {
+    ulonglong2 v[HU];
+#pragma unroll
+    for (int u = 0; u < HU; ++u) v[u] = k2[min(q + (int64_t)u * NT, q1 - 1)];
+#pragma unroll
+    for (int u = 0; u < HU; ++u) {
+      if (q + (int64_t)u * NT < q1) {
+        add(v[u].x);
+        add(v[u].y);
+      }
+    }
+  }
+  if ((hi & 1) && t == 0 && hi > lo) add(keys_in[hi - 1]);
+  block_sync();
+  for (int b = t; b < kMaxBins; b += NT) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) c += sh.cnt[v][b];
+    a.block_hist[(size_t)g * kMaxBins + b] = c;
+  }
+}
+
+// Column scans of four adjacent digits b0 .. b0+3 of a middle pass at once
+// (one 16-byte load per block row), as column_scan does for one digit.
+__device__ void column_scan4(const GArgs& a, int s, int b0, int G, uint32_t (*part)[4]) {
+  constexpr int PER = kMaxBlocks / NT;
+  const int per = (G + NT - 1) / NT;
+  const int t = threadIdx.x;
+  const int lane = lane_id();
+  const int w = t / kWave;
+  const int g0 = t * per;
+  uint4 v[PER];
+  uint32_t loc[4] = {0, 0, 0, 0};
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    v[i] = make_uint4(0, 0, 0, 0);
+    if (i < per && g0 + i < G)
+      v[i] = *reinterpret_cast<const uint4*>(a.block_hist + (size_t)(g0 + i) * kMaxBins + b0);
+    loc[0] += v[i].x;
+    loc[1] += v[i].y;
+    loc[2] += v[i].z;
+    loc[3] += v[i].w;
+  }
+  uint32_t run[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t inc = wave_incl_scan_u32(loc[k]);
+    run[k] = inc - loc[k];
+    if (lane == kWave - 1) part[w][k] = inc;
+  }
+  block_sync();
+  uint32_t total[4] = {0, 0, 0, 0};
+#pragma unroll
+  for (int u = 0; u < NT / kWave; ++u) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      run[k] += u < w ? part[u][k] : 0u;
+      total[k] += part[u][k];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    if (i < per && g0 + i < G) {
+      *reinterpret_cast<uint4*>(a.block_hist + (size_t)(g0 + i) * kMaxBins + b0) =
+          make_uint4(run[0], run[1], run[2], run[3]);
+      run[0] += v[i].x;
+      run[1] += v[i].y;
+      run[2] += v[i].z;
+      run[3] += v[i].w;
+    }
+  }
+  if (t < 4) a.hist_cnt[s * kMaxBins + b0 + t] = total[t];
+  block_sync();  // part is reused by the next call
+}
+
 union MidShared {
   ScatterShared scatter;
   MidFastShared fast;
-  CountShared count;
-  struct {
-    uint32_t scan32[NT / kWave + 1];
-    uint64_t scan64[NT / kWave + 1];
-  } scan;
+  CountMidShared count;
+  uint32_t part4[NT / kWave][4];
 };
 
 // Grid barrier for a launch whose workgroups are all resident (the grid is
@@ -1336,10 +1439,9 @@ __global__ __launch_bounds__(NT) void g_mid(GArgs a) {
   const int G = a.mid.blocks;
   uint32_t gen = 0;
   for (int s = 1; s < S - 1; ++s) {
-    if ((int)blockIdx.x < G) count_block<false>(a, s, blockIdx.x, a.mid, 1, false, sh.count, NT);
+    if ((int)blockIdx.x < G) count_mid(a, s, blockIdx.x, sh.count);
     if (!grid_barrier(a, ++gen)) return;
-    for (int b = blockIdx.x; b < (int)pl->nbins[s]; b += gridDim.x)
-      column_scan<NT>(a, s, b, false, G, sh.scan.scan32, sh.scan.scan64);
+    for (int b = blockIdx.x; b < kMaxBins / 4; b += gridDim.x) column_scan4(a, s, 4 * b, G, sh.part4);
     if (!grid_barrier(a, ++gen)) return;
     if ((int)blockIdx.x < G) {
       if (pl->packed)
@@ -1439,7 +1541,13 @@ __device__ void final_generic(const GArgs& a, int g, FinalShared& sh) {
           atomicAdd((unsigned long long*)&sh.wsum[dg[r]], (unsigned long long)kc.len(key[r]));
         }
       }
-      rank_tile(dg, rk, nb, nbits, cnt, sh.excl, sh.scan32);
+      // (few final digits, e.g. after middle passes: match only their bits)
+      if (nbits <= 2)
+        rank_tile<2>(dg, rk, nb, nbits, cnt, sh.excl, sh.scan32);
+      else if (nbits <= 5)
+        rank_tile<5>(dg, rk, nb, nbits, cnt, sh.excl, sh.scan32);
+      else
+        rank_tile<10>(dg, rk, nb, nbits, cnt, sh.excl, sh.scan32);
       block_sync();  // counters read before the stage is reused
       if (!packed) {
         u32_alias* sid = reinterpret_cast<u32_alias*>(sh.stage);
