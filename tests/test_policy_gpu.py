@@ -120,3 +120,17 @@ def test_sjf_carried_ranks_either_side_of_the_fit(classes, max_len):
     l = rng.integers(0, max_len + 1, n).astype(np.int32)
     l[1], l[2] = 0, max_len  # the full length range is present
     check(p, l, POLICY_SJF, f"classes={classes} max_len={max_len}")
+
+
+def test_sjf_carried_ranks_window_in_global_memory():
+    # As the queue test of the same name: 99 % of the lengths are multiples
+    # of 1024, so the last blocks span more sub-bucket starts than the LDS
+    # window holds; the final pass with carried ranks then takes its
+    # global-window kernel.
+    rng = np.random.default_rng(32)
+    n = 12_000_000
+    p = rng.integers(0, 4, n).astype(np.uint8)
+    l = (rng.integers(1, 8, n) * 1024).astype(np.int32)
+    sprinkle = rng.random(n) < 0.01
+    l[sprinkle] = rng.integers(1, 8192, int(sprinkle.sum()))
+    check(p, l, POLICY_SJF, "window-global")
