@@ -829,9 +829,8 @@ struct CountShared {
   uint64_t w[kMaxBins];
 };
 
-// FEW: digits of at most 8 values are counted in registers (final-digit
-// histograms; the middle passes always have 1024 digits).
-template <bool FEW>
+// (Used for the final digit of the generic layouts; the middle passes count
+// with count_mid.) Digits of at most 8 values are counted in registers.
 __device__ void count_block(const GArgs& a, int s, int g, Split sp, int rows, bool weights,
                             CountShared& sh, int threads) {
   const Plan* pl = a.plan;
@@ -865,7 +864,7 @@ __device__ void count_block(const GArgs& a, int s, int g, Split sp, int rows, bo
   constexpr int kFew = 8;
   uint32_t fc[kFew];
   uint64_t fw[kFew];
-  const bool few = FEW && nb <= kFew;
+  const bool few = nb <= kFew;
 #pragma unroll
   for (int b = 0; b < kFew; ++b) {
     fc[b] = 0;
@@ -1142,7 +1141,7 @@ __global__ __launch_bounds__(HT) void g_histF(GArgs a) {
       return;
     }
   }
-  count_block<true>(a, (int)pl->nscatter - 1, row, a.fin, kHistRows, true, sh.generic, HT);
+  count_block(a, (int)pl->nscatter - 1, row, a.fin, kHistRows, true, sh.generic, HT);
 }
 
 // ---- fast middle pass ---------------------------------------------------------
