@@ -33,10 +33,29 @@ __device__ __forceinline__ bool less(uint64_t ka, uint32_t ia, uint64_t kb, uint
   return ka < kb || (ka == kb && ia < ib);
 }
 
-__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m) {
-  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m, kWave);
-  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m, kWave);
-  return (uint64_t)hi << 32 | lo;
+// The value of lane (this lane ^ M). Distances 1, 2 and 8 are one DPP move
+// (quad permutes; a rotation of the 16-lane row by 8), 4 is two row shifts
+// and a select: no LDS traffic. 16 and 32 cross rows: a bpermute.
+template <int M>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
+  if constexpr (M == 1) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xb1, 0xf, 0xf, false);  // quad_perm [1,0,3,2]
+  } else if constexpr (M == 2) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4e, 0xf, 0xf, false);  // quad_perm [2,3,0,1]
+  } else if constexpr (M == 4) {
+    const uint32_t up = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x104, 0xf, 0xf, false);
+    const uint32_t dn = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);
+    return (lane_id() & 4) ? dn : up;  // row_shl:4 (lane + 4), row_shr:4 (lane - 4)
+  } else if constexpr (M == 8) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xf, 0xf, false);  // row_ror:8
+  } else {
+    return (uint32_t)__shfl_xor((int)v, M, kWave);
+  }
+}
+
+template <int M>
+__device__ __forceinline__ uint64_t xor_lane64(uint64_t v) {
+  return (uint64_t)xor_lane<M>((uint32_t)(v >> 32)) << 32 | xor_lane<M>((uint32_t)v);
 }
 
 // Ascending bitonic sort of BT * E (key, id) pairs in LDS, with an optional
@@ -92,12 +111,23 @@ __device__ void block_sort(uint64_t* key, uint32_t* id, uint32_t* pay) {
       } else if (j < (uint32_t)(kWave * E)) {
         const int m = (int)(j / E);  // partner lane = lane ^ m
         const bool take_min = ((lane & m) == 0) == (((t * E) & k) == 0);
+        auto stage = [&](auto mc) {
+          constexpr int M = decltype(mc)::value;
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const uint64_t pk = shfl_xor64(xk[e], m);
-          const uint32_t pi = (uint32_t)__shfl_xor((int)xi[e], m, kWave);
-          const uint32_t pp = PAYLOAD ? (uint32_t)__shfl_xor((int)xp[e], m, kWave) : 0u;
-          keep(e, take_min, pk, pi, pp);
+          for (int e = 0; e < E; ++e) {
+            const uint64_t pk = xor_lane64<M>(xk[e]);
+            const uint32_t pi = xor_lane<M>(xi[e]);
+            const uint32_t pp = PAYLOAD ? xor_lane<M>(xp[e]) : 0u;
+            keep(e, take_min, pk, pi, pp);
+          }
+        };
+        switch (m) {  // (uniform)
+          case 1: stage(std::integral_constant<int, 1>{}); break;
+          case 2: stage(std::integral_constant<int, 2>{}); break;
+          case 4: stage(std::integral_constant<int, 4>{}); break;
+          case 8: stage(std::integral_constant<int, 8>{}); break;
+          case 16: stage(std::integral_constant<int, 16>{}); break;
+          default: stage(std::integral_constant<int, 32>{}); break;
         }
       } else {
         const uint32_t m = j / E;  // partner thread = t ^ m, another wave
