@@ -7,10 +7,10 @@
 // Algorithm 1; the smallest key is the most urgent request.
 //
 //   b_select  sorts the candidates (the heap's first b entries and the
-//             unsorted buffer) and the ongoing requests with a bitonic
-//             network; the candidates C are the first b. The most urgent of
-//             C and O decides the stage filter; every element's place in
-//             the merged list M (C's surviving members and O) and in the
+//             unsorted buffer) and the ongoing requests (an LDS radix sort
+//             over the key bits that vary); the candidates C are the first
+//             b. The most urgent of C and O decides the stage filter; every
+//             element's place in the merged list M (C's surviving members and O) and in the
 //             pushed-back list (C's filtered members and M beyond b) comes
 //             from binary searches in the other sorted lists.
 //   b_evict   sorts the cached requests; the eviction order is that order
@@ -33,137 +33,136 @@ __device__ __forceinline__ bool less(uint64_t ka, uint32_t ia, uint64_t kb, uint
   return ka < kb || (ka == kb && ia < ib);
 }
 
-// The value of lane (this lane ^ M). Distances 1, 2 and 8 are one DPP move
-// (quad permutes; a rotation of the 16-lane row by 8), 4 is two row shifts
-// and a select: no LDS traffic. 16 and 32 cross rows: a bpermute.
-template <int M>
-__device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
-  if constexpr (M == 1) {
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xb1, 0xf, 0xf, false);  // quad_perm [1,0,3,2]
-  } else if constexpr (M == 2) {
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4e, 0xf, 0xf, false);  // quad_perm [2,3,0,1]
-  } else if constexpr (M == 4) {
-    const uint32_t up = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x104, 0xf, 0xf, false);
-    const uint32_t dn = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);
-    return (lane_id() & 4) ? dn : up;  // row_shl:4 (lane + 4), row_shr:4 (lane - 4)
-  } else if constexpr (M == 8) {
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xf, 0xf, false);  // row_ror:8
-  } else {
-    return (uint32_t)__shfl_xor((int)v, M, kWave);
-  }
-}
+// Scratch of the block radix sort: per-wave digit counters (then the waves'
+// offsets) and the wave partials of the key range reduction and the scans.
+constexpr int kSortWaves = BT / kWave;
+struct SortScratch {
+  uint16_t cnt[kSortWaves][256];
+  uint32_t red[kSortWaves * 6];
+};
 
-template <int M>
-__device__ __forceinline__ uint64_t xor_lane64(uint64_t v) {
-  return (uint64_t)xor_lane<M>((uint32_t)(v >> 32)) << 32 | xor_lane<M>((uint32_t)v);
-}
-
-// Ascending bitonic sort of BT * E (key, id) pairs in LDS, with an optional
-// u32 payload that moves with them. Thread t holds elements t*E .. t*E+E-1 in
-// registers throughout: compare-exchange distances below E stay inside a
-// thread, distances below 64 * E pair a lane with another lane of its wave
-// (shuffles, no barrier), and only the longer ones go through LDS with
-// workgroup barriers. Every thread of the block must call it.
+// Stable LSD radix sort by (key, id) of the first n of the BT * E entries of
+// key / id (and a u32 payload that moves with them) in LDS, 8 bits at a time,
+// the id's digits first, then the key's; digits that are the same for all n
+// entries are skipped (the bitwise AND and OR of all keys and ids tell which
+// vary). Every pass ranks the rounds of each wave by ballot matching
+// (entries (wave, round, lane) in index order, so ranks follow the current
+// order: stable), turns the waves' counts into digit-major offsets and
+// scatters through LDS. Entries n .. BT*E-1 take (OR of the keys, OR of the
+// ids): no real entry sorts after them. Every thread of the block must call
+// it.
 template <int E, bool PAYLOAD>
-__device__ void block_sort(uint64_t* key, uint32_t* id, uint32_t* pay) {
-  constexpr uint32_t N = BT * E;
-  const uint32_t t = threadIdx.x, lane = t & (kWave - 1);
+__device__ void block_sort(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t n,
+                           SortScratch& sc) {
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  auto at = [&](int r) { return (uint32_t)(w * kWave * E + r * kWave + lane); };
   uint64_t xk[E];
   uint32_t xi[E], xp[E];
+  uint32_t kand_lo = ~0u, kand_hi = ~0u, kor_lo = 0, kor_hi = 0, iand = ~0u, ior = 0;
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    xk[e] = key[t * E + e];
-    xi[e] = id[t * E + e];
-    xp[e] = PAYLOAD ? pay[t * E + e] : 0u;
-  }
-  // element (t*E + e) meets its partner; keep the smaller when take_min
-  auto keep = [&](int e, bool take_min, uint64_t pk, uint32_t pi, uint32_t pp) {
-    const bool pless = less(pk, pi, xk[e], xi[e]);
-    if (take_min == pless) {
-      xk[e] = pk;
-      xi[e] = pi;
-      xp[e] = pp;
-    }
-  };
-  for (uint32_t k = 2; k <= N; k <<= 1) {
-    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-      if (j < (uint32_t)E) {
-#pragma unroll
-        for (int jj = E / 2; jj >= 1; jj >>= 1) {
-          if (j != (uint32_t)jj) continue;
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            if (e & jj) continue;
-            const int f = e | jj;
-            const bool up = ((t * E + e) & k) == 0;
-            if (less(xk[f], xi[f], xk[e], xi[e]) == up) {
-              const uint64_t tk = xk[e];
-              const uint32_t ti = xi[e], tp = xp[e];
-              xk[e] = xk[f];
-              xi[e] = xi[f];
-              xp[e] = xp[f];
-              xk[f] = tk;
-              xi[f] = ti;
-              xp[f] = tp;
-            }
-          }
-        }
-      } else if (j < (uint32_t)(kWave * E)) {
-        const int m = (int)(j / E);  // partner lane = lane ^ m
-        const bool take_min = ((lane & m) == 0) == (((t * E) & k) == 0);
-        auto stage = [&](auto mc) {
-          constexpr int M = decltype(mc)::value;
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            const uint64_t pk = xor_lane64<M>(xk[e]);
-            const uint32_t pi = xor_lane<M>(xi[e]);
-            const uint32_t pp = PAYLOAD ? xor_lane<M>(xp[e]) : 0u;
-            keep(e, take_min, pk, pi, pp);
-          }
-        };
-        switch (m) {  // (uniform)
-          case 1: stage(std::integral_constant<int, 1>{}); break;
-          case 2: stage(std::integral_constant<int, 2>{}); break;
-          case 4: stage(std::integral_constant<int, 4>{}); break;
-          case 8: stage(std::integral_constant<int, 8>{}); break;
-          case 16: stage(std::integral_constant<int, 16>{}); break;
-          default: stage(std::integral_constant<int, 32>{}); break;
-        }
-      } else {
-        const uint32_t m = j / E;  // partner thread = t ^ m, another wave
-        const bool take_min = ((t & m) == 0) == (((t * E) & k) == 0);
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          key[t * E + e] = xk[e];
-          id[t * E + e] = xi[e];
-          if (PAYLOAD) pay[t * E + e] = xp[e];
-        }
-        block_sync();
-        const uint32_t pt = t ^ m;
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-          keep(e, take_min, key[pt * E + e], id[pt * E + e], PAYLOAD ? pay[pt * E + e] : 0u);
-        block_sync();
-      }
+  for (int r = 0; r < E; ++r) {
+    const uint32_t i = at(r);
+    xk[r] = key[i];
+    xi[r] = id[i];
+    xp[r] = PAYLOAD ? pay[i] : 0u;
+    if (i < n) {
+      kand_lo &= (uint32_t)xk[r];
+      kand_hi &= (uint32_t)(xk[r] >> 32);
+      kor_lo |= (uint32_t)xk[r];
+      kor_hi |= (uint32_t)(xk[r] >> 32);
+      iand &= xi[r];
+      ior |= xi[r];
     }
   }
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    key[t * E + e] = xk[e];
-    id[t * E + e] = xi[e];
-    if (PAYLOAD) pay[t * E + e] = xp[e];
+  for (int off = kWave / 2; off >= 1; off >>= 1) {
+    kand_lo &= (uint32_t)__shfl_xor((int)kand_lo, off, kWave);
+    kand_hi &= (uint32_t)__shfl_xor((int)kand_hi, off, kWave);
+    kor_lo |= (uint32_t)__shfl_xor((int)kor_lo, off, kWave);
+    kor_hi |= (uint32_t)__shfl_xor((int)kor_hi, off, kWave);
+    iand &= (uint32_t)__shfl_xor((int)iand, off, kWave);
+    ior |= (uint32_t)__shfl_xor((int)ior, off, kWave);
+  }
+  if (lane == 0) {
+    uint32_t* r6 = sc.red + 6 * w;
+    r6[0] = kand_lo, r6[1] = kand_hi, r6[2] = kor_lo, r6[3] = kor_hi, r6[4] = iand, r6[5] = ior;
   }
   block_sync();
+#pragma unroll
+  for (int v = 0; v < kSortWaves; ++v) {
+    const uint32_t* r6 = sc.red + 6 * v;
+    kand_lo &= r6[0], kand_hi &= r6[1], kor_lo |= r6[2], kor_hi |= r6[3];
+    iand &= r6[4], ior |= r6[5];
+  }
+  block_sync();  // (the partials' words are the scans' scratch below)
+  const uint64_t kor = (uint64_t)kor_hi << 32 | kor_lo;
+  const uint64_t kvary = kor ^ ((uint64_t)kand_hi << 32 | kand_lo);
+  const uint32_t ivary = ior ^ iand;
+#pragma unroll
+  for (int r = 0; r < E; ++r) {
+    if (at(r) >= n) {
+      xk[r] = kor;
+      xi[r] = ior;
+    }
+  }
+  uint16_t* mycnt = sc.cnt[w];
+  for (int pass = 0; pass < 12; ++pass) {
+    const bool on_id = pass < 4;
+    const int sh = 8 * (on_id ? pass : pass - 4);
+    const uint32_t vary = on_id ? (ivary >> sh) & 0xffu : (uint32_t)(kvary >> sh) & 0xffu;
+    if (vary == 0) continue;  // (uniform)
+    for (int b = lane; b < 256; b += kWave) mycnt[b] = 0;
+    uint32_t dg[E], rk[E];
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+      dg[r] = on_id ? (xi[r] >> sh) & 0xffu : (uint32_t)(xk[r] >> sh) & 0xffu;
+      rk[r] = rank_round_c<8>(dg[r], mycnt);
+    }
+    block_sync();  // every wave's counts are in
+    // digit-major offsets: thread d < 256 owns digit d
+    uint32_t c[kSortWaves], tot = 0;
+#pragma unroll
+    for (int v = 0; v < kSortWaves; ++v) {
+      c[v] = t < 256 ? sc.cnt[v][t] : 0u;
+      tot += c[v];
+    }
+    uint32_t all;
+    uint32_t run = block_excl_scan_u32<BT>(tot, sc.red, all);
+    if (t < 256) {
+#pragma unroll
+      for (int v = 0; v < kSortWaves; ++v) {
+        sc.cnt[v][t] = (uint16_t)run;
+        run += c[v];
+      }
+    }
+    block_sync();  // offsets are written
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+      const uint32_t q = rk[r] + mycnt[dg[r]];
+      key[q] = xk[r];
+      id[q] = xi[r];
+      if (PAYLOAD) pay[q] = xp[r];
+    }
+    block_sync();  // the pass is scattered
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+      const uint32_t i = at(r);
+      xk[r] = key[i];
+      xi[r] = id[i];
+      if (PAYLOAD) xp[r] = pay[i];
+    }
+  }
+  block_sync();  // (the last pass's reads are done before callers write)
 }
 
-// Sorts the first n entries (n <= 8 * BT; entries from n up to the sort
-// size must hold the sentinel key ~0).
+// Sorts the first n entries (n <= 8 * BT) of key / id (and pay).
 template <bool PAYLOAD>
-__device__ void sort_pairs(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t n) {
-  if (n <= (uint32_t)BT) block_sort<1, PAYLOAD>(key, id, pay);
-  else if (n <= 2u * BT) block_sort<2, PAYLOAD>(key, id, pay);
-  else if (n <= 4u * BT) block_sort<4, PAYLOAD>(key, id, pay);
-  else block_sort<8, PAYLOAD>(key, id, pay);
+__device__ void sort_pairs(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t n,
+                           SortScratch& sc) {
+  if (n <= (uint32_t)BT) block_sort<1, PAYLOAD>(key, id, pay, n, sc);
+  else if (n <= 2u * BT) block_sort<2, PAYLOAD>(key, id, pay, n, sc);
+  else if (n <= 4u * BT) block_sort<4, PAYLOAD>(key, id, pay, n, sc);
+  else block_sort<8, PAYLOAD>(key, id, pay, n, sc);
 }
 
 __device__ __forceinline__ uint32_t sort_size(uint32_t n) {
@@ -190,7 +189,10 @@ struct SelectShared {
   uint32_t cid[kCandCap];
   uint64_t okey[kSelectCap];
   uint32_t oid[kSelectCap];
-  uint16_t dec_excl[kSelectCap + 1];  // kept members of C before each index (<= 4096)
+  union {  // (the sorts are done before dec_excl is written)
+    uint16_t dec_excl[kSelectCap + 1];  // kept members of C before each index (<= 4096)
+    SortScratch sort;
+  };
   uint32_t scan32[BT / kWave + 1];
   uint32_t bad;
 };
@@ -243,8 +245,8 @@ __global__ __launch_bounds__(BT) void b_select(SelArgs a) {
     }
     return;
   }
-  sort_pairs<false>(sh.ckey, sh.cid, nullptr, nc_in);
-  sort_pairs<false>(sh.okey, sh.oid, nullptr, no);
+  sort_pairs<false>(sh.ckey, sh.cid, nullptr, nc_in, sh.sort);
+  sort_pairs<false>(sh.okey, sh.oid, nullptr, no, sh.sort);
   const uint32_t nc = min((uint32_t)a.b, nc_in);  // C = the first nc candidates
   if (nc == 0 && no == 0) {
     if (t == 0) a.counts[0] = a.counts[1] = 0;
@@ -317,6 +319,7 @@ struct EvictShared {
   uint32_t id[kEvictCap];
   uint32_t src[kEvictCap];    // index into the caller's cached / kv arrays
   uint64_t scan64[BT / kWave + 1];
+  SortScratch sort;
   uint32_t bad;
 };
 
@@ -348,7 +351,7 @@ __global__ __launch_bounds__(BT) void b_evict(EvictArgs a) {
     if (t == 0) atomicOr(a.flags, (sh.bad & 1u) ? kFlagInval : kFlagRange);
     return;
   }
-  sort_pairs<true>(sh.key, sh.id, sh.src, nr);
+  sort_pairs<true>(sh.key, sh.id, sh.src, nr, sh.sort);
   // KV sizes in eviction order (the sorted order read backwards), inclusive
   // prefix sums over a contiguous chunk per thread, kept in sh.key
   constexpr uint32_t PER = (kEvictCap + BT - 1) / BT;
