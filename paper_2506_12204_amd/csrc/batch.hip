@@ -54,6 +54,7 @@ struct SortScratch {
 template <int E, bool PAYLOAD>
 __device__ void block_sort(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t n,
                            SortScratch& sc) {
+  if (n <= 1) return;  // (uniform) nothing to order
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
   auto at = [&](int r) { return (uint32_t)(w * kWave * E + r * kWave + lane); };
   uint64_t xk[E];
