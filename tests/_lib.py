@@ -52,3 +52,42 @@ def assert_same(got, want, label=""):
     bad = np.flatnonzero(gw.astype(np.int64) != ww)
     assert bad.size == 0, f"{label}: wait differs at {bad[:8]} ({bad.size} positions)"
     assert list(gt) == list(wt), f"{label}: totals differ"
+
+
+def check_queue_by_definition(p, l, order, wait, totals):
+    """The schedule's definition checked directly, for queues the oracle would
+    take minutes on: order is a permutation of the ids and strictly
+    increasing in the unique key (rank, length, id), so it is the one sorted
+    order; every wait is the sum of the lengths before it; the totals are the
+    exact sums of the waits, overall and per rank (Eq. 1)."""
+    n = p.shape[0]
+    assert order.shape == (n,) and wait.shape == (n,)
+    if n == 0:
+        assert all(t == 0 for t in totals)
+        return
+    assert order.min() >= 0 and order.max() < n
+    seen = np.zeros(n, np.bool_)
+    seen[order] = True
+    assert seen.all(), "order is not a permutation"
+    del seen
+    po = p[order]
+    lo = l[order]
+    dp = np.diff(po.astype(np.int16))
+    dl = np.diff(lo.astype(np.int64))
+    di = np.diff(order.astype(np.int64))
+    assert (dp >= 0).all(), "ranks decrease"
+    assert (dl[dp == 0] >= 0).all(), "lengths decrease within a rank"
+    assert (di[(dp == 0) & (dl == 0)] > 0).all(), "ids decrease within a key"
+    del dp, dl, di
+    assert wait[0] == 0
+    assert np.array_equal(np.diff(wait), lo[:-1].astype(np.int64)), "waits"
+
+    def exact_sum(v):  # int64 values >= 0, summed exactly in two 32-bit halves
+        u = v.astype(np.uint64)
+        return (int((u >> np.uint64(32)).sum()) << 32) + int((u & np.uint64(0xffffffff)).sum())
+
+    assert totals[0] == exact_sum(wait), "grand total"
+    present = np.bincount(po, minlength=256)
+    for c in range(256):
+        want = exact_sum(wait[po == c]) if present[c] else 0
+        assert totals[1 + c] == want, f"class {c} total"

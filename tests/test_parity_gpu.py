@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 from oracle import c_oracle_batched, c_oracle_queue
-from tests._lib import assert_same, ensure_built, gpu_available, gpu_batched, gpu_queue
+from tests._lib import check_queue_by_definition, assert_same, ensure_built, gpu_available, gpu_batched, gpu_queue
 from workloads import fuzz_queue, fuzz_segments, generate
 
 pytestmark = [pytest.mark.gpu,
@@ -110,6 +110,20 @@ def test_compact_window_in_global_memory():
     sprinkle = rng.random(n) < 0.01
     l[sprinkle] = rng.integers(1, 8192, int(sprinkle.sum()))
     check_queue(p, l, "window-global")
+
+
+def test_compact_beyond_buffer_store_range():
+    # 2^28 + 12,345 requests: past the size up to which the compact passes
+    # store through buffer resources (2^28), so every block of the final pass
+    # takes the kernel with plain stores; the largest queue tested (checked
+    # against the definition: the oracle's merge sort takes minutes here)
+    rng = np.random.default_rng(35)
+    n = (1 << 28) + 12_345
+    p = rng.integers(0, 5, n, dtype=np.uint8)
+    l = rng.integers(1, 32769, n, dtype=np.int32)
+    say(f"[gpu] queue 2^28+: n={n}")
+    order, wait, totals = gpu_queue(p, l)
+    check_queue_by_definition(p, l, order, wait, totals)
 
 
 @pytest.mark.parametrize("n", [100_003, 5_000_000])
