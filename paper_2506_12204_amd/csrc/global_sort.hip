@@ -926,6 +926,14 @@ __device__ __forceinline__ bool use_big_final(const Plan* pl) {
   return pl->packed && pl->W == 32 && pl->nscatter == 2 && pl->small && pl->nbins[1] <= 256;
 }
 
+// Its wide form (in the kernel g_final_cglb, which is launched when the
+// queue is chunked) takes the other keys in the high word with at most 256
+// final digits: after middle passes or with lengths of 2^26 and more.
+__device__ __forceinline__ bool use_wide_big_final(const GArgs& a, const Plan* pl) {
+  return a.chunked && pl->packed && pl->W == 32 && !pl->compact && !use_big_final(pl) &&
+         pl->nbins[pl->nscatter - 1] <= 256;
+}
+
 // Final-digit histogram of one row when the big final pass runs (keys in the
 // high word, two passes, at most 256 final digits). Every wave counts into
 // bins of its own, so lanes of different waves never meet on an LDS address
@@ -1952,13 +1960,19 @@ __device__ __forceinline__ void load_final_big(const uint64_t* keys, int64_t tb,
   }
 }
 
+// WIDE: after middle passes (the final digit is u2 >> shift of the last
+// pass) or with lengths of 2^26 and more (64 lengths may pass 2^32: the
+// round scans are 64-bit and taken again in the store loop instead of being
+// held in registers).
+template <bool WIDE>
 __device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
   const int t = threadIdx.x;
   const int lane = lane_id();
   const int w = wave_id();
   const int wb = w * kWave * KB;
   const Plan* pl = a.plan;
-  const int nb = (int)pl->nbins[1];
+  const int s_last = WIDE ? (int)pl->nscatter - 1 : 1;  // the final pass
+  const int nb = (int)pl->nbins[s_last];
   const bool owner = t < nb;
   const uint32_t d0 = (uint32_t)a.d0;
   const uint32_t psh = pl->wh + d0;
@@ -1966,9 +1980,12 @@ __device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
   const uint32_t mh = (1u << pl->wh) - 1;
   const uint32_t lenmask = (1u << psh) - 1;
   const uint32_t hoff = pl->hmin << d0;
-  const uint64_t* keys_in = a.keys[0];
+  const uint32_t sf = WIDE ? pl->shift[s_last] : 0u;
+  const uint64_t* keys_in = a.keys[(s_last - 1) & 1];
   uint16_t* mycnt = sh.cnt[w];
-  auto digit = [&](uint32_t key) { return __umul24(key >> psh, H) + ((key >> d0) & mh); };
+  auto digit = [&](uint32_t key) {
+    return (__umul24(key >> psh, H) + ((key >> d0) & mh)) >> sf;
+  };
   auto len = [&](uint32_t key) { return (key & lenmask) + hoff; };
 
   clear_wave_counters<MAXB>(mycnt);
@@ -1979,7 +1996,7 @@ __device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
   uint32_t carry_c;
   uint64_t carry_w;
   {
-    const uint32_t c = owner ? a.hist_cnt[kMaxBins + t] : 0u;
+    const uint32_t c = owner ? a.hist_cnt[s_last * kMaxBins + t] : 0u;
     const uint64_t wv = owner ? a.hist_w[t] : 0ull;
     uint32_t tc;
     uint64_t tw;
@@ -2029,7 +2046,8 @@ __device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
       sh.wsum[t] = 0;
     }
     const uint32_t inc_c = wave_incl_scan_u32(tot);
-    const uint64_t inc_w = wave_incl_scan_u40(ws);  // a tile's lengths add up to < 2^40
+    // a tile's lengths add up to < 2^40 (lengths below 2^26), else < 2^45
+    const uint64_t inc_w = WIDE ? wave_incl_scan_u64(ws) : wave_incl_scan_u40(ws);
     if (lane == kWave - 1) {
       sh.part_c[w] = inc_c;
       sh.part_w[w] = inc_w;
@@ -2067,6 +2085,49 @@ __device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
     block_sync();  // the tile is staged
 
     // ---- phase 2: tile length prefix, order, waits, class totals -----------
+    auto place = [&](int j, uint64_t wt_in_tile) {
+      const uint64_t x = sh.stage[j];
+      const uint32_t key = (uint32_t)(x >> 32);
+      const uint32_t c = key >> psh;  // class - pmin
+      const uint32_t d = digit(key);
+      const uint64_t wt = sh.base_w[d] + wt_in_tile;
+      const uint32_t pos = sh.base_c[d] + (uint32_t)j;
+      if (pos < (uint64_t)a.n) {  // always true for consistent counts
+        a.order[pos] = (int32_t)(uint32_t)x;
+        a.wait[pos] = (int64_t)wt;
+      }
+      if (c != cur) {
+        if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
+        cur = c;
+        acc = {0, 0};
+      }
+      add128(acc, wt);
+    };
+    if constexpr (WIDE) {
+      uint64_t rt[KB];  // round totals (the scans are taken again below)
+      uint64_t chunk = 0;
+#pragma unroll
+      for (int r = 0; r < KB; ++r) {
+        const int j = wb + r * kWave + lane;
+        const uint32_t ls = (full || j < cv) ? len((uint32_t)(sh.stage[j] >> 32)) : 0u;
+        rt[r] = last_lane_u64(wave_incl_scan_len(ls));
+        chunk += rt[r];
+      }
+      if (lane == 0) sh.chunk[w] = chunk;
+      block_sync();
+      uint64_t run = 0;
+#pragma unroll
+      for (int v = 0; v < NWB; ++v) run += v < w ? sh.chunk[v] : 0ull;
+#pragma unroll
+      for (int r = 0; r < KB; ++r) {
+        const int j = wb + r * kWave + lane;
+        const bool in_tile = full || j < cv;
+        const uint32_t ls = in_tile ? len((uint32_t)(sh.stage[j] >> 32)) : 0u;
+        const uint64_t inc = wave_incl_scan_len(ls);
+        if (in_tile) place(j, run + (inc - ls));
+        run += rt[r];
+      }
+    } else {
     uint32_t lsr[KB], inc[KB], rt[KB];
     uint64_t chunk = 0;
 #pragma unroll
@@ -2106,6 +2167,7 @@ __device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
         add128(acc, wt);
       }
       run += rt[r];
+    }
     }
   }
   if (acc.lo | acc.hi) atomic_add128(sh.clo + cur, sh.chi + cur, acc);
@@ -2488,7 +2550,7 @@ __global__ __launch_bounds__(NTB) void g_final_big(GArgs a) {
     return;
   }
   if (!use_big_final(pl)) return;
-  final_big(a, blockIdx.x, sh.big);
+  final_big<false>(a, blockIdx.x, sh.big);
 }
 
 // The compact final pass for the blocks whose sub-bucket starts do not fit
@@ -2497,10 +2559,18 @@ __global__ __launch_bounds__(NTB) void g_final_big(GArgs a) {
 // kind's loop holds no global loads besides the element prefetch and the
 // compiler's wait counts stay exact there. Returns at once for other blocks.
 __global__ __launch_bounds__(NTB) void g_final_cglb(GArgs a) {
-  __shared__ FinalCompactShared sh;
+  __shared__ union {
+    FinalCompactShared compact;
+    FinalBigShared big;
+  } sh;
   const Plan* pl = a.plan;
-  if (!pl->ok || !pl->compact || pl->pay) return;
-  final_compact<false, false>(a, blockIdx.x, sh);
+  if (!pl->ok) return;
+  if (use_wide_big_final(a, pl)) {
+    final_big<true>(a, blockIdx.x, sh.big);
+    return;
+  }
+  if (!pl->compact || pl->pay) return;
+  final_compact<false, false>(a, blockIdx.x, sh.compact);
 }
 
 // The compact final pass with carried ranks, in kernels of their own (one
@@ -2527,7 +2597,7 @@ __global__ __launch_bounds__(NT, kScatterWavesPerSimd) void g_final(GArgs a) {
     FinalFastShared fast;
   } sh;
   const Plan* pl = a.plan;
-  if (!pl->ok || pl->compact || use_big_final(pl)) return;
+  if (!pl->ok || pl->compact || use_big_final(pl) || use_wide_big_final(a, pl)) return;
   if (pl->packed && pl->W == 32 && pl->nscatter == 2 && pl->small) {
     if (pl->nbits[1] <= 8)
       final_fast<8>(a, blockIdx.x, sh.fast);

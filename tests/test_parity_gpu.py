@@ -154,6 +154,26 @@ def test_one_class_and_zero_lengths(n):
     check_queue(np.zeros(n, np.uint8), l, "one-class-zeros")
 
 
+@pytest.mark.parametrize("classes,lo,hi,label", [
+    (5, 0, 1 << 20, "one middle pass, 5 final digits"),
+    (1, 0, 1 << 27, "one middle pass, lengths past 2^26, 128 final digits"),
+    (5, 0, 1 << 29, "two middle passes, 3 final digits (the cost-model shape)"),
+    (2, 1 << 26, (1 << 26) + (1 << 19), "two passes, lengths past 2^26"),
+    (5, 0, 1 << 31, "34-bit keys: generic final pass"),
+])
+def test_wide_keys_with_few_final_digits(classes, lo, hi, label):
+    # Keys of at most 32 bits (in the high word) with at most 256 final
+    # digits but more than two passes or lengths of 2^26 and more: the wide
+    # form of the big-tile final pass, reading the buffer of the pass before
+    # it (either of the two)
+    rng = np.random.default_rng(len(label))
+    n = 300_000
+    p = rng.integers(0, classes, n).astype(np.uint8)
+    l = rng.integers(lo, hi, n, dtype=np.int64).astype(np.int32)
+    l[:1000] = l[1000:2000]  # ties on (rank, length)
+    check_queue(p, l, label)
+
+
 @pytest.mark.parametrize("n", [2000, 50000])
 def test_all_256_classes_full_length_range(n):
     # 256 classes x lengths up to 2^31-1: the widest keys; on the global path
