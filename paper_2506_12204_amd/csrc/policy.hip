@@ -269,6 +269,49 @@ __global__ __launch_bounds__(PT) void p_range(PolArgs a) {
   if (lane_id() == 0 && m) atomicMax(a.pmax, m);
 }
 
+// Calls f(length, rank, live) for every element of the range starting at k0
+// (kPolRange elements, in no particular order). With vec (lengths 16-byte
+// and ranks 4-byte aligned) every lane loads four consecutive elements at a
+// time; elements past n come with live = false. All lanes call f together.
+template <typename F>
+__device__ __forceinline__ void range_elements(const PolArgs& a, int64_t k0, bool vec, F&& f) {
+  if (vec) {
+#pragma unroll 4
+    for (int r = 0; r < kRounds / 4; ++r) {
+      const int64_t k = k0 + 4 * ((int64_t)r * kWave + lane_id());
+      int32_t l[4];
+      uint32_t p[4];
+      if (k + 3 < a.n) {
+        const int4 lv = *reinterpret_cast<const int4*>(a.length + k);
+        const uint32_t pv = *reinterpret_cast<const uint32_t*>(a.priority + k);
+        l[0] = lv.x, l[1] = lv.y, l[2] = lv.z, l[3] = lv.w;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[i] = (pv >> (8 * i)) & 0xffu;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t ki = min(k + i, a.n - 1);
+          l[i] = a.length[ki];
+          p[i] = a.priority[ki];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) f(l[i], p[i], k + i < a.n);
+    }
+  } else {
+#pragma unroll 16
+    for (int r = 0; r < kRounds; ++r) {
+      const int64_t k = k0 + r * kWave + lane_id();
+      const int64_t kc = min(k, a.n - 1);
+      f(a.length[kc], (uint32_t)a.priority[kc], k < a.n);
+    }
+  }
+}
+
+__device__ __forceinline__ bool vec_ok(const PolArgs& a) {
+  return ((reinterpret_cast<uintptr_t>(a.length) & 15) | (reinterpret_cast<uintptr_t>(a.priority) & 3)) == 0;
+}
+
 // FCFS: length sum of every range and the largest rank; negative lengths
 // are flagged.
 __global__ __launch_bounds__(PT) void f_sums(PolArgs a, int64_t ranges) {
@@ -278,6 +321,9 @@ __global__ __launch_bounds__(PT) void f_sums(PolArgs a, int64_t ranges) {
   uint64_t s = 0;
   uint32_t m = 0;
   bool bad = false;
+  // (one element per lane: this first kernel of a schedule runs while the
+  // caches write back the previous schedule's output, and loading four per
+  // lane did not help it)
 #pragma unroll 16
   for (int r = 0; r < kRounds; ++r) {
     const int64_t k = k0 + r * kWave + lane_id();
@@ -434,13 +480,7 @@ __device__ __forceinline__ void hpjf_count(const PolArgs& a, int64_t w, int64_t 
   lsum.zero();
   const int64_t k0 = w * kPolRange;
   bool bad = false;
-#pragma unroll 16
-  for (int r = 0; r < kRounds; ++r) {
-    const int64_t k = k0 + r * kWave + lane_id();
-    const bool live = k < a.n;
-    const int64_t kc = min(k, a.n - 1);
-    const int32_t l = a.length[kc];
-    const uint32_t p = a.priority[kc];
+  range_elements(a, k0, vec_ok(a), [&](int32_t l, uint32_t p, bool live) {
     bad |= live && l < 0;
     const uint32_t lv = live ? (uint32_t)l : 0u;
     if constexpr (PB > 0) {
@@ -451,7 +491,7 @@ __device__ __forceinline__ void hpjf_count(const PolArgs& a, int64_t w, int64_t 
         lsum.add(c, readlane_u64(wave_incl_scan_len(in_mask(peers) ? lv : 0u), 63));
       });
     }
-  }
+  });
   if (__ballot(bad)) {
     if (lane_id() == 0) atomicOr(a.flags, kFlagRange);
   }

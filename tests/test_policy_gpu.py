@@ -134,3 +134,22 @@ def test_sjf_carried_ranks_window_in_global_memory():
     sprinkle = rng.random(n) < 0.01
     l[sprinkle] = rng.integers(1, 8192, int(sprinkle.sum()))
     check(p, l, POLICY_SJF, "window-global")
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+def test_policy_unaligned_inputs(policy):
+    # inputs that start one element into their allocations: lengths not
+    # 16-byte aligned, ranks not 4-byte aligned (the range kernels then load
+    # one element per lane instead of four)
+    import torch
+
+    import paper_2506_12204_amd as ss
+    p, l = fuzz_queue(100_001, seed=41 + policy, classes=6, max_len=5000, tie_frac=0.2)
+    dev = torch.device("cuda")
+    tp = torch.from_numpy(np.concatenate([[0], p]).astype(np.uint8)).to(dev)[1:]
+    tl = torch.from_numpy(np.concatenate([[0], l]).astype(np.int32)).to(dev)[1:]
+    assert tl.data_ptr() % 16 != 0 and tp.data_ptr() % 4 != 0
+    print(f"[gpu] policy {NAMES[policy]} unaligned: n={len(p)}", flush=True)
+    order, wait, totals = ss.schedule_policy(tp, tl, policy)
+    assert_same((order.cpu().numpy(), wait.cpu().numpy(), totals),
+                c_oracle_policy(p, l, policy), f"{NAMES[policy]} unaligned")
