@@ -214,6 +214,41 @@ def test_repeatable_bit_for_bit():
         assert_same(gpu_queue(p, l), first, "repeat")
 
 
+def _shifted(a, dtype):
+    # a device copy that starts one element into its allocation
+    import torch
+    buf = np.concatenate([np.zeros(1, dtype), np.asarray(a, dtype)])
+    return torch.from_numpy(buf).to("cuda")[1:]
+
+
+@pytest.mark.parametrize("n", [5000, 100_003, 5_000_001])
+def test_queue_unaligned_inputs(n):
+    # lengths not 16-byte aligned, ranks not 4-byte aligned: the first
+    # histogram pass then loads one request per lane instead of four (at 5M,
+    # with the chunk counts of the compact layout); 5000 takes the LDS path
+    import paper_2506_12204_amd as ss
+    p, l = fuzz_queue(n, seed=51, classes=5, max_len=32768, tie_frac=0.2)
+    tp, tl = _shifted(p, np.uint8), _shifted(l, np.int32)
+    assert tl.data_ptr() % 16 != 0 and tp.data_ptr() % 4 != 0
+    say(f"[gpu] queue unaligned: n={n}")
+    order, wait, totals = ss.schedule(tp, tl)
+    assert_same((order.cpu().numpy(), wait.cpu().numpy(), totals),
+                c_oracle_queue(p, l), f"unaligned{n}")
+
+
+def test_batched_unaligned_inputs():
+    import paper_2506_12204_amd as ss
+    sizes = [0, 7, 300, 4097, 16385, 70000, 1]
+    p, l, off = fuzz_segments(sizes, seed=52, classes=6, max_len=3000)
+    tp, tl = _shifted(p, np.uint8), _shifted(l, np.int32)
+    to = _shifted(off, np.int64)
+    assert tl.data_ptr() % 16 != 0 and tp.data_ptr() % 4 != 0
+    say(f"[gpu] batched unaligned: n={len(p)}")
+    order, wait, totals = ss.schedule_batched(tp, tl, to, 6, None)
+    assert_same((order.cpu().numpy(), wait.cpu().numpy(), totals),
+                c_oracle_batched(p, l, off, 6), "batched-unaligned")
+
+
 # ---- batched inputs ------------------------------------------------------------
 
 def test_batched_mixed_sizes_and_empty_queues():
