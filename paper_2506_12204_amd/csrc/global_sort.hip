@@ -13,8 +13,9 @@
 // ever waits for another inside a kernel, and consecutive tiles of a digit
 // land next to each other in memory, written by the same workgroup.
 //
-//   g_reset      clear the small per-call state and the totals.
-//   g_hist0      read (priority, length) once: validate, find the ranges and
+//   g_hist0      (its first workgroup also clears the small per-call state
+//                and the totals)
+//                read (priority, length) once: validate, find the ranges and
 //                count the low `d0` bits of every length per block. That
 //                digit does not depend on the ranges, so no separate min/max
 //                pass is needed.
@@ -50,7 +51,11 @@ static_assert(BPT * NT == kMaxBins, "every bin has a thread");
 static_assert(NW * kMaxBins * 2 <= T * 8, "wave counters must fit in the stage");
 
 // ------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void g_reset(GArgs a) {
+// Run by one workgroup of the first histogram pass: no other workgroup of
+// that pass touches this state (a block's range error goes into its block
+// ranges, and the plan writer raises the flag).
+template <int THREADS>
+__device__ void reset_call_state(const GArgs& a) {
   const int t = threadIdx.x;
   if (t == 0) {
     a.flags[0] = 0;
@@ -59,9 +64,9 @@ __global__ __launch_bounds__(1024) void g_reset(GArgs a) {
     a.plan->pay = 0;
     a.plan->pay_shift = 32;
   }
-  for (int i = t; i < kMaxScatter * kMaxBins; i += 1024) a.hist_cnt[i] = 0;
-  for (int i = t; i < kMaxBins; i += 1024) a.hist_w[i] = 0;
-  for (int i = t; i < 2 * (1 + a.num_classes); i += 1024) a.totals[i] = 0;
+  for (int i = t; i < kMaxScatter * kMaxBins; i += THREADS) a.hist_cnt[i] = 0;
+  for (int i = t; i < kMaxBins; i += THREADS) a.hist_w[i] = 0;
+  for (int i = t; i < 2 * (1 + a.num_classes); i += THREADS) a.totals[i] = 0;
 }
 
 // ------------------------------------------------------------------------
@@ -104,7 +109,7 @@ __device__ void write_plan(const GArgs& a, int G) {
   for (int g = threadIdx.x; g < G; g += SCT) {
     const uint32_t* r = a.block_ranges + 4 * (size_t)g;
     pl_ = min(pl_, r[0]);
-    ph = max(ph, r[1]);
+    ph = max(ph, r[1]);  // bit 31: the block found a range error
     ll = min(ll, r[2]);
     lh = max(lh, r[3]);
   }
@@ -129,7 +134,8 @@ __device__ void write_plan(const GArgs& a, int G) {
     glmax = max(glmax, s_red[3][i]);
   }
   Plan* pl = a.plan;
-  if (load_agent(a.flags) != 0) {
+  if (gpmax >> 31) atomicOr(a.flags, kFlagRange);
+  if ((gpmax >> 31) || load_agent(a.flags) != 0) {
     pl->ok = 0;
     return;
   }
@@ -198,6 +204,7 @@ __global__ __launch_bounds__(HT) void g_hist0(GArgs a, int vec_ok) {
   const int nb = 1 << a.d0;
   const uint32_t mask = (uint32_t)nb - 1;
 
+  if (g == 0) reset_call_state<HT>(a);
   int64_t lo, hi;
   row_range(a, a.main, g, kHistRows, lo, hi);
   // The first chunk boundary at or after lo, if it lies in this row: the
@@ -275,10 +282,9 @@ __global__ __launch_bounds__(HT) void g_hist0(GArgs a, int vec_ok) {
       ph = max(ph, s_red[3][i] & 0xffu);
       bb |= s_red[3][i] >> 31;
     }
-    if (bb) atomicOr(a.flags, kFlagRange);
     uint32_t* r = a.block_ranges + 4 * (size_t)g;
     r[0] = pl;  // an empty block leaves the neutral values
-    r[1] = ph;
+    r[1] = ph | (bb << 31);
     r[2] = bl;
     r[3] = bh;
   }
@@ -2663,7 +2669,6 @@ Split global_mid_split(int64_t n) {
 }
 
 hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEvents* ev) {
-  hipLaunchKernelGGL(g_reset, dim3(1), dim3(1024), 0, st, a);
   const int vec_ok = ((uintptr_t)a.priority % 4 == 0) && ((uintptr_t)a.length % 16 == 0);
   const dim3 gm(a.main.blocks);
   const dim3 gmh(a.main.blocks * kHistRows);
