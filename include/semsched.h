@@ -352,6 +352,32 @@ int sem_evict_async(const uint8_t *priority, const int32_t *length, int64_t n_id
                     int32_t *victims_out, int64_t *upto_out, void *workspace, size_t ws_bytes,
                     void *stream);
 
+/*
+ * Allocation-free single-queue schedule, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc. Same computation, arguments and outputs as
+ * sem_schedule_async, but the workspace is a scratch array that the library
+ * holds in static device memory (SEM_STATIC_SCRATCH_BYTES on every device it
+ * runs on, until the process ends), so nothing is allocated or freed and the
+ * call does not synchronise.
+ *   status_out [1] int32 DEVICE: receives, on the stream after the schedule,
+ *             SEM_OK or the device-detected error (SEM_ERANGE for a negative
+ *             length).
+ *   stream    the stream to enqueue on (NULL = null stream).
+ * Errors returned at once: as sem_schedule_async (SEM_EINVAL also for a null
+ * status_out), and SEM_ENOMEM for n > SEM_STATIC_MAX_N (the scratch holds the
+ * workspace of at most that many requests).
+ * All calls on one device share its scratch array: calls whose work overlaps
+ * on that device (on different streams, or from different threads without
+ * ordering) race and give unspecified results. Calls enqueued on one stream
+ * are ordered and safe; each call clears what it needs.
+ */
+#define SEM_STATIC_MAX_N 1048576
+#define SEM_STATIC_SCRATCH_BYTES 33554432
+int sem_schedule_static(const uint8_t *priority, const int32_t *length, int64_t n,
+                        int32_t *order_out, int64_t *wait_out, sem_i128 *totals_out,
+                        int32_t *status_out, void *stream);
+
 /* Stream used by the blocking calls (NULL = null stream). */
 int sem_set_stream(void *stream);
 

@@ -58,7 +58,10 @@ SYMBOLS = (
     "sem_select_batch_async",
     "sem_evict",
     "sem_evict_async",
+    "sem_schedule_static",
 )
+STATIC_MAX_N = 1048576
+STATIC_SCRATCH_BYTES = 33554432
 SELECT_CAP = 4096
 EVICT_CAP = 8192
 PREFILL, DECODE = 0, 1
@@ -130,6 +133,7 @@ def _load() -> ctypes.CDLL:
     lib.sem_evict.argtypes = [vp, vp, i64, vp, vp, i64, i64, i64, vp, i64, vp, vp]
     lib.sem_evict_async.argtypes = [vp, vp, i64, vp, vp, i64, i64, i64, vp, i64, vp, vp, vp, sz,
                                     vp]
+    lib.sem_schedule_static.argtypes = [vp, vp, i64, vp, vp, vp, vp, vp]
     lib.sem_strerror.argtypes = [ctypes.c_int]
     lib.sem_strerror.restype = ctypes.c_char_p
     for name in ("sem_schedule", "sem_schedule_batched", "sem_schedule_async",
@@ -137,7 +141,7 @@ def _load() -> ctypes.CDLL:
                  "sem_insert_async", "sem_schedule_policy", "sem_schedule_policy_async",
                  "sem_service_times", "sem_evict_plan", "sem_schedule_cost",
                  "sem_schedule_cost_async", "sem_select_batch", "sem_select_batch_async",
-                 "sem_evict", "sem_evict_async"):
+                 "sem_evict", "sem_evict_async", "sem_schedule_static"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -230,6 +234,33 @@ def schedule(priority: torch.Tensor, length: torch.Tensor
     s.run(priority, length)
     s.check()
     return s.order, s.wait, totals_to_ints(s.totals)
+
+
+def schedule_static(priority: torch.Tensor, length: torch.Tensor,
+                    out: Optional[Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]]
+                    = None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Schedule one queue through the allocation-free entry point (the library's
+    static scratch stands in for the workspace; n <= STATIC_MAX_N).
+
+    ``out`` = (order int32[n], wait int64[n], totals int64[257, 2], status
+    int32[1]) preallocated by the caller; without it they are allocated here.
+    Enqueues on the current stream without synchronising and returns the four
+    tensors; status[0] holds SEM_OK or the device-detected error once the
+    stream reaches it.
+    """
+    _check_inputs(priority, length)
+    n = priority.numel()
+    dev = priority.device
+    if out is None:
+        out = (torch.empty(n, dtype=torch.int32, device=dev),
+               torch.empty(n, dtype=torch.int64, device=dev),
+               torch.empty((1 + MAX_CLASSES, 2), dtype=torch.int64, device=dev),
+               torch.empty(1, dtype=torch.int32, device=dev))
+    order, wait, totals, status = out
+    rc = lib.sem_schedule_static(_ptr(priority), _ptr(length), n, _ptr(order), _ptr(wait),
+                                 _ptr(totals), _ptr(status), _stream_handle(dev))
+    _raise(rc, "sem_schedule_static")
+    return order, wait, totals, status
 
 
 def schedule_batched(priority: torch.Tensor, length: torch.Tensor, offsets: torch.Tensor,

@@ -538,9 +538,66 @@ int enqueue_segments(SegArgs a, int64_t seg_max, const int64_t* counts, hipStrea
   return SEM_OK;
 }
 
+// ---- allocation-free single-queue schedule ---------------------------------
+// `scratch` stands in for the workspace of sem_schedule_async when the caller
+// cannot allocate one. Every device the library runs on holds its own copy
+// until the process ends. In host code the array's name is not a device
+// address: each device's address is taken once with hipGetSymbolAddress and
+// only that address is handed to kernels.
+static __device__ __align__(256) uint8_t scratch[SEM_STATIC_SCRATCH_BYTES];
+
+// Device-side status of the call: the error bits of the flags word mapped to
+// the library's codes, written to the caller's status word.
+__global__ void g_write_status(const uint32_t* flags, int32_t* status) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    const uint32_t f = *flags;
+    *status = (f & kFlagDevice)  ? SEM_EDEVICE
+              : (f & kFlagInval) ? SEM_EINVAL
+              : (f & kFlagRange) ? SEM_ERANGE
+                                 : SEM_OK;
+  }
+}
+
+// This device's address of `scratch`, looked up once per device.
+int scratch_address(void** out) {
+  static std::mutex mu;
+  static std::map<int, void*> addr;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> guard(mu);
+  auto it = addr.find(dev);
+  if (it == addr.end()) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SEM_EDEVICE;
+    it = addr.emplace(dev, p).first;
+  }
+  *out = it->second;
+  return SEM_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+int sem_schedule_static(const uint8_t* priority, const int32_t* length, int64_t n,
+                        int32_t* order_out, int64_t* wait_out, sem_i128* totals_out,
+                        int32_t* status_out, void* stream) {
+  int rc = check_queue_args(priority, length, n, order_out, wait_out, totals_out);
+  if (rc != SEM_OK) return rc;
+  if (!status_out) return SEM_EINVAL;
+  if (n > SEM_STATIC_MAX_N) return SEM_ENOMEM;
+  if (sem_workspace_bytes(n, 1) > SEM_STATIC_SCRATCH_BYTES) return SEM_ENOMEM;
+  void* ws = nullptr;
+  rc = scratch_address(&ws);
+  if (rc != SEM_OK) return rc;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  rc = enqueue_queue(priority, length, n, SEM_MAX_CLASSES, order_out, wait_out, totals_out, ws,
+                     st);
+  if (rc != SEM_OK) return rc;
+  hipLaunchKernelGGL(g_write_status, dim3(1), dim3(64), 0, st,
+                     static_cast<const uint32_t*>(ws), status_out);
+  return hipGetLastError() == hipSuccess ? SEM_OK : SEM_EDEVICE;
+}
 
 const char* sem_strerror(int code) {
   switch (code) {

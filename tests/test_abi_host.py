@@ -178,3 +178,16 @@ def test_select_and_evict_argument_errors(ss):
     assert E(fake, fake, 10, fake, fake, 5, 0, 0, nul, 1, fake, fake) == ss.SEM_EINVAL
     assert L.sem_evict_async(fake, fake, 10, fake, fake, 5, 0, 0, fake, 1, fake, fake, nul, 256,
                              nul) == ss.SEM_EINVAL
+
+
+def test_static_entry_point_host_checks(ss):
+    L = ss.lib
+    nul = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 40)  # never dereferenced: the call fails first
+    # the scratch holds the workspace of the largest size it accepts
+    assert ss.workspace_bytes(ss.STATIC_MAX_N, 1) <= ss.STATIC_SCRATCH_BYTES
+    assert L.sem_schedule_static(fake, fake, ss.STATIC_MAX_N + 1, fake, fake, fake, fake,
+                                 nul) == ss.SEM_ENOMEM
+    assert L.sem_schedule_static(fake, fake, 5, fake, fake, fake, nul, nul) == ss.SEM_EINVAL
+    assert L.sem_schedule_static(fake, fake, -1, fake, fake, fake, fake, nul) == ss.SEM_EINVAL
+    assert L.sem_schedule_static(nul, fake, 5, fake, fake, fake, fake, nul) == ss.SEM_EINVAL
