@@ -40,8 +40,8 @@
  *                the single-queue calls). Detected on the device.
  *   SEM_ENOMEM   the library could not allocate its internal workspace.
  *   SEM_EDEVICE  a HIP runtime call failed.
- *   SEM_ENOTIMPL the asynchronous batched call was given a queue longer than
- *                SEM_SEGMENT_CAP (the blocking call handles any length).
+ *   SEM_ENOTIMPL a size beyond what an entry point implements (noted at the
+ *                entry points that can return it).
  */
 #ifndef SEMSCHED_H
 #define SEMSCHED_H
@@ -87,16 +87,23 @@ int sem_schedule(const uint8_t *priority, const int32_t *length, int64_t n,
 
 /*
  * Schedule num_segments independent queues laid out back to back (blocking).
+ * Each queue is scheduled exactly as sem_schedule schedules a single queue
+ * (Section 3.2 per queue; the paper puts no bound on a queue's length).
  *   offsets   [num_segments + 1] int64, DEVICE pointer; queue s holds
  *             requests offsets[s] .. offsets[s+1]-1. Empty queues are valid.
+ *             offsets[0] must be 0 and the offsets non-decreasing; the batch
+ *             holds N = offsets[num_segments] requests.
+ *   num_classes in [1, 256]: every priority must be below it.
  *   order_out [N] int32, ids LOCAL to each queue (0-based arrival index),
  *             queue s's schedule written at offsets[s] + k.
  *   wait_out  [N] int64, same layout; waits restart at 0 in every queue.
  *   totals_out[num_segments * (1 + num_classes)] sem_i128, queue-major:
  *             queue s's total at s*(1+num_classes), class c at +1+c.
- * Queues up to SEM_SEGMENT_CAP requests are scheduled one per workgroup in
- * LDS; longer queues go through the multi-pass global path one at a time.
- * The call copies offsets to the host once to plan the launches.
+ * Queues of any length are accepted. Queues of up to SEM_SEGMENT_CAP
+ * requests are scheduled one per wave or workgroup inside LDS, longer ones by
+ * one segmented radix sort over all of them. The call copies the offsets to
+ * the host once, to size the workspace of the long queues, and synchronises
+ * once at the end.
  */
 int sem_schedule_batched(const uint8_t *priority, const int32_t *length,
                          const int64_t *offsets, int64_t num_segments,
@@ -104,8 +111,12 @@ int sem_schedule_batched(const uint8_t *priority, const int32_t *length,
                          int64_t *wait_out, sem_i128 *totals_out);
 
 /*
- * Workspace size in bytes needed by the asynchronous calls for n requests
- * in num_segments queues (num_segments = 1 for sem_schedule_async).
+ * Workspace size in bytes needed by the asynchronous calls.
+ *   sem_schedule_async: n requests, num_segments = 1.
+ *   sem_schedule_batched_async: num_segments queues, n = an upper bound on the
+ *     number of requests that lie in queues longer than SEM_SEGMENT_CAP (the
+ *     total N when unknown, 0 when every queue is known to be short).
+ * With num_segments = 1 the larger of the two sizes is returned.
  */
 size_t sem_workspace_bytes(int64_t n, int64_t num_segments);
 
@@ -124,15 +135,21 @@ int sem_schedule_async(const uint8_t *priority, const int32_t *length,
                        void *stream);
 
 /*
- * Asynchronous batched schedule. `max_segment` is a host-side upper bound on
- * the longest queue; it must be <= SEM_SEGMENT_CAP (else SEM_ENOTIMPL).
- * Offsets are validated on the device (SEM_EINVAL via sem_check), as is a
- * queue longer than max_segment.
+ * Asynchronous batched schedule: the arguments of sem_schedule_batched plus a
+ * caller-owned DEVICE workspace (256-byte aligned) of ws_bytes bytes and the
+ * stream. Allocates nothing, does not synchronise and never reads device
+ * memory on the host: the offsets are checked, the queues sorted into work
+ * lists by size and the long queues sized on the device. The workspace must
+ * hold at least sem_workspace_bytes(0, num_segments) bytes (else SEM_EINVAL
+ * at once); whatever it holds beyond that is room for the requests of queues
+ * longer than SEM_SEGMENT_CAP, and sem_workspace_bytes(L, num_segments) bytes
+ * give room for L of them. Device-detected errors, returned by sem_check:
+ * SEM_EINVAL for bad offsets or long queues that do not fit the workspace,
+ * SEM_ERANGE for a length < 0 or a priority >= num_classes.
  */
 int sem_schedule_batched_async(const uint8_t *priority, const int32_t *length,
                                const int64_t *offsets, int64_t num_segments,
-                               int32_t num_classes, int64_t n_total,
-                               int64_t max_segment, int32_t *order_out,
+                               int32_t num_classes, int32_t *order_out,
                                int64_t *wait_out, sem_i128 *totals_out,
                                void *workspace, size_t ws_bytes, void *stream);
 

@@ -106,8 +106,7 @@ def _load() -> ctypes.CDLL:
     lib.sem_workspace_bytes.argtypes = [i64, i64]
     lib.sem_workspace_bytes.restype = sz
     lib.sem_schedule_async.argtypes = [vp, vp, i64, vp, vp, vp, vp, sz, vp]
-    lib.sem_schedule_batched_async.argtypes = [vp, vp, vp, i64, i32, i64, i64, vp, vp, vp,
-                                               vp, sz, vp]
+    lib.sem_schedule_batched_async.argtypes = [vp, vp, vp, i64, i32, vp, vp, vp, vp, sz, vp]
     lib.sem_set_stream.argtypes = [vp]
     lib.sem_check.argtypes = [vp, vp]
     lib.sem_trace_stage.argtypes = [ctypes.c_int, vp, vp]
@@ -264,15 +263,17 @@ def schedule_static(priority: torch.Tensor, length: torch.Tensor,
 
 
 def schedule_batched(priority: torch.Tensor, length: torch.Tensor, offsets: torch.Tensor,
-                     num_classes: int, max_segment: Optional[int] = None
+                     num_classes: int, blocking: bool = False,
+                     long_requests: Optional[int] = None
                      ) -> Tuple[torch.Tensor, torch.Tensor, List[int]]:
     """Schedule independent queues laid out back to back.
 
     Returns (order int32 with queue-local ids, wait int64, totals as
-    num_segments*(1+num_classes) ints, queue-major). With ``max_segment``
-    (<= SEGMENT_CAP) the call stays asynchronous up to the final check;
-    without it the library reads the offsets once on the host, which also
-    allows queues longer than SEGMENT_CAP.
+    num_segments*(1+num_classes) ints, queue-major). By default the
+    asynchronous call runs on the current stream (queues of any length, no
+    host read of the offsets) and one check follows; ``long_requests`` bounds
+    the requests in queues longer than SEGMENT_CAP (default: all of them) and
+    sizes the workspace. ``blocking=True`` takes the blocking call instead.
     """
     _check_inputs(priority, length)
     if offsets.dtype != torch.int64 or offsets.device != priority.device or offsets.dim() != 1:
@@ -287,12 +288,13 @@ def schedule_batched(priority: torch.Tensor, length: torch.Tensor, offsets: torc
     wait = torch.empty(n, dtype=torch.int64, device=dev)
     totals = torch.empty((max(s, 1), 1 + num_classes, 2), dtype=torch.int64, device=dev)
     stream = _stream_handle(dev)
-    if max_segment is not None:
-        ws_bytes = workspace_bytes(n, max(s, 2))
+    if not blocking:
+        lr = n if long_requests is None else int(long_requests)
+        ws_bytes = int(lib.sem_workspace_bytes(lr, s))
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
         rc = lib.sem_schedule_batched_async(_ptr(priority), _ptr(length), _ptr(offsets), s,
-                                            num_classes, n, int(max_segment), _ptr(order),
-                                            _ptr(wait), _ptr(totals), _ptr(ws), ws_bytes, stream)
+                                            num_classes, _ptr(order), _ptr(wait), _ptr(totals),
+                                            _ptr(ws), ws_bytes, stream)
         _raise(rc, "sem_schedule_batched_async")
         _raise(lib.sem_check(_ptr(ws), stream), "sem_check")
     else:

@@ -20,7 +20,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libsemsched.so")
-SOURCES = ["abi.hip", "segment_sort.hip", "global_sort.hip", "insert.hip", "policy.hip",
+SOURCES = ["abi.hip", "batched.hip", "global_sort.hip", "insert.hip", "policy.hip",
            "cost.hip", "batch.hip"]
 ARCH = os.environ.get("SEMSCHED_ARCH", "gfx950")
 NOISE = "is not a recognized feature for this target"

@@ -174,23 +174,18 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   }
   if (!needs_global(n)) {
     if (launch_fill_zero(flags, 1, st) != hipSuccess) return SEM_EDEVICE;
-    SegArgs a = {};
+    BArgs a = {};
     a.priority = p;
     a.length = l;
     a.offsets = nullptr;
     a.num_segments = 1;
-    a.n_total = n;
-    a.max_segment = n;
+    a.n_single = n;
     a.num_classes = num_classes;
     a.order = order;
     a.wait = wait;
     a.totals = tot;
     a.flags = flags;
-    const SegSize sz = n <= kSegTinyCap     ? SegSize::kTiny
-                       : n <= kSegSmallCap  ? SegSize::kSmall
-                       : n <= kSegMediumCap ? SegSize::kMedium
-                                            : SegSize::kLarge;
-    return launch_segment_schedule(a, sz, 1, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
+    return launch_single_lds(a, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
   }
   const Layout L = layout_for(n);
   GArgs g = {};
@@ -516,26 +511,102 @@ int check_queue_args(const uint8_t* p, const int32_t* l, int64_t n, int32_t* ord
 int check_batched_args(const uint8_t* p, const int32_t* l, const int64_t* offsets,
                        int64_t num_segments, int32_t num_classes, int32_t* order,
                        int64_t* wait, sem_i128* totals) {
-  if (num_segments < 0 || num_classes < 1 || num_classes > SEM_MAX_CLASSES) return SEM_EINVAL;
+  if (num_segments < 0 || num_segments > INT32_MAX || num_classes < 1 ||
+      num_classes > SEM_MAX_CLASSES)
+    return SEM_EINVAL;
   if (!offsets) return SEM_EINVAL;
   if (num_segments > 0 && (!p || !l || !order || !wait || !totals)) return SEM_EINVAL;
   return SEM_OK;
 }
 
-// Launch the LDS kernels for every size class that can occur in (lo, hi].
-int enqueue_segments(SegArgs a, int64_t seg_max, const int64_t* counts, hipStream_t st) {
-  const SegSize sizes[4] = {SegSize::kTiny, SegSize::kSmall, SegSize::kMedium, SegSize::kLarge};
-  const int64_t lo[4] = {-1, kSegTinyCap, kSegSmallCap, kSegMediumCap};
-  const int per_cu[4] = {16, 4, 4, 1};
-  for (int k = 0; k < 4; ++k) {
-    if (seg_max <= lo[k] && k > 0) continue;
-    if (counts && counts[k] == 0) continue;
-    const int64_t want = counts ? counts[k] : a.num_segments;
-    const int64_t cap = (int64_t)num_cus() * per_cu[k];
-    const int grid = (int)std::max<int64_t>(1, std::min(want, cap));
-    if (launch_segment_schedule(a, sizes[k], grid, st) != hipSuccess) return SEM_EDEVICE;
+// Workspace of a batched call: the flags line, the control block, the work
+// lists, then the segmented sort's arrays for up to `long_cap` requests in
+// queues longer than kSegLargeCap.
+struct BLayout {
+  size_t ctl = 64, grab = 0, lists = 0, keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0, hist = 0, tsum = 0,
+         lbase = 0, tstart = 0, total = 0;
+  uint32_t max_tiles = 0;
+};
+
+static_assert(64 + sizeof(BCtl) <= kHeaderBytes, "control block must fit in the header");
+
+BLayout batched_layout(int64_t S, uint64_t long_cap) {
+  BLayout L;
+  size_t off = kHeaderBytes;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  L.grab = take(sizeof(GrabLine) * kLists * kSubLists);
+  L.lists = take(4 * (size_t)kLists * (size_t)S);
+  if (long_cap > 0) {
+    const uint64_t queues = std::min<uint64_t>((uint64_t)S, long_cap / (kSegLargeCap + 1));
+    L.max_tiles = long_max_tiles(long_cap, S);
+    L.keys0 = take(8 * long_cap);
+    L.keys1 = take(8 * long_cap);
+    L.ids0 = take(4 * long_cap);
+    L.ids1 = take(4 * long_cap);
+    L.hist = take(4 * 256 * (size_t)L.max_tiles);
+    L.tsum = take(8 * (size_t)L.max_tiles);
+    L.lbase = take(8 * (size_t)(queues + 1));
+    L.tstart = take(4 * (size_t)(queues + 1));
   }
-  return SEM_OK;
+  L.total = off;
+  return L;
+}
+
+// Largest long-queue capacity whose batched layout fits ws_bytes (0 if only
+// the fixed part does).
+uint64_t long_capacity(int64_t S, size_t ws_bytes) {
+  if (batched_layout(S, 1).total > ws_bytes) return 0;
+  uint64_t lo = 1, hi = ws_bytes / 24 + 1;  // more than 24 bytes per request
+  while (hi - lo > 1) {
+    const uint64_t mid = lo + (hi - lo) / 2;
+    if (batched_layout(S, mid).total <= ws_bytes) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+int enqueue_batched(const uint8_t* p, const int32_t* l, const int64_t* offsets,
+                    int64_t num_segments, int32_t num_classes, int32_t* order, int64_t* wait,
+                    sem_i128* totals, void* ws, size_t ws_bytes, hipStream_t st) {
+  char* base = static_cast<char*>(ws);
+  uint32_t* flags = reinterpret_cast<uint32_t*>(base);
+  const uint64_t cap = long_capacity(num_segments, ws_bytes);
+  const BLayout L = batched_layout(num_segments, cap);
+  // the flags line, the control block and the grab counters: one fill
+  if (launch_fill_zero(flags, (L.grab + sizeof(GrabLine) * kLists * kSubLists) / 4, st) !=
+      hipSuccess)
+    return SEM_EDEVICE;
+  if (num_segments == 0) return SEM_OK;
+  BArgs a = {};
+  a.priority = p;
+  a.length = l;
+  a.offsets = offsets;
+  a.num_segments = num_segments;
+  a.num_classes = num_classes;
+  a.order = order;
+  a.wait = wait;
+  a.totals = reinterpret_cast<uint64_t*>(totals);
+  a.flags = flags;
+  a.ctl = reinterpret_cast<BCtl*>(base + L.ctl);
+  a.grab = reinterpret_cast<GrabLine*>(base + L.grab);
+  a.lists = reinterpret_cast<uint32_t*>(base + L.lists);
+  a.long_cap = cap;
+  a.max_tiles = L.max_tiles;
+  if (cap > 0) {
+    a.keys[0] = reinterpret_cast<uint64_t*>(base + L.keys0);
+    a.keys[1] = reinterpret_cast<uint64_t*>(base + L.keys1);
+    a.ids[0] = reinterpret_cast<uint32_t*>(base + L.ids0);
+    a.ids[1] = reinterpret_cast<uint32_t*>(base + L.ids1);
+    a.hist = reinterpret_cast<uint32_t*>(base + L.hist);
+    a.tsum = reinterpret_cast<uint64_t*>(base + L.tsum);
+    a.lbase = reinterpret_cast<uint64_t*>(base + L.lbase);
+    a.tstart = reinterpret_cast<uint32_t*>(base + L.tstart);
+  }
+  return launch_batched(a, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
 }
 
 // ---- allocation-free single-queue schedule ---------------------------------
@@ -606,7 +677,7 @@ const char* sem_strerror(int code) {
     case SEM_ERANGE: return "length < 0 or priority >= num_classes";
     case SEM_ENOMEM: return "out of device memory";
     case SEM_EDEVICE: return "HIP runtime error";
-    case SEM_ENOTIMPL: return "queue longer than SEM_SEGMENT_CAP in the asynchronous batched call";
+    case SEM_ENOTIMPL: return "size beyond what this entry point implements";
     default: return "unknown error";
   }
 }
@@ -626,9 +697,10 @@ int sem_set_stream(void* stream) {
 }
 
 size_t sem_workspace_bytes(int64_t n, int64_t num_segments) {
-  if (n < 0) return 0;
-  if (num_segments == 1) return layout_for(n).total;
-  return kHeaderBytes;
+  if (n < 0 || num_segments < 0 || num_segments > INT32_MAX) return 0;
+  const size_t batched = batched_layout(num_segments, (uint64_t)n).total;
+  if (num_segments == 1) return std::max(layout_for(n).total, batched);
+  return batched;
 }
 
 int sem_check(const void* workspace, void* stream) {
@@ -935,34 +1007,18 @@ int sem_schedule(const uint8_t* priority, const int32_t* length, int64_t n, int3
 
 int sem_schedule_batched_async(const uint8_t* priority, const int32_t* length,
                                const int64_t* offsets, int64_t num_segments,
-                               int32_t num_classes, int64_t n_total, int64_t max_segment,
-                               int32_t* order_out, int64_t* wait_out, sem_i128* totals_out,
-                               void* workspace, size_t ws_bytes, void* stream) {
+                               int32_t num_classes, int32_t* order_out, int64_t* wait_out,
+                               sem_i128* totals_out, void* workspace, size_t ws_bytes,
+                               void* stream) {
   const int rc = check_batched_args(priority, length, offsets, num_segments, num_classes,
                                     order_out, wait_out, totals_out);
   if (rc != SEM_OK) return rc;
-  if (n_total < 0 || max_segment < 0) return SEM_EINVAL;
-  if (max_segment > SEM_SEGMENT_CAP) return SEM_ENOTIMPL;
-  if (!workspace || ws_bytes < kHeaderBytes ||
+  if (!workspace || ws_bytes < batched_layout(num_segments, 0).total ||
       (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
     return SEM_EINVAL;
-  const hipStream_t st = static_cast<hipStream_t>(stream);
-  uint32_t* flags = static_cast<uint32_t*>(workspace);
-  if (launch_fill_zero(flags, 1, st) != hipSuccess) return SEM_EDEVICE;
-  if (num_segments == 0) return SEM_OK;
-  SegArgs a = {};
-  a.priority = priority;
-  a.length = length;
-  a.offsets = offsets;
-  a.num_segments = num_segments;
-  a.n_total = n_total;
-  a.max_segment = max_segment;
-  a.num_classes = num_classes;
-  a.order = order_out;
-  a.wait = wait_out;
-  a.totals = reinterpret_cast<uint64_t*>(totals_out);
-  a.flags = flags;
-  return enqueue_segments(a, max_segment, nullptr, st);
+  return enqueue_batched(priority, length, offsets, num_segments, num_classes, order_out,
+                         wait_out, totals_out, workspace, ws_bytes,
+                         static_cast<hipStream_t>(stream));
 }
 
 int sem_schedule_batched(const uint8_t* priority, const int32_t* length,
@@ -971,59 +1027,28 @@ int sem_schedule_batched(const uint8_t* priority, const int32_t* length,
   int rc = check_batched_args(priority, length, offsets, num_segments, num_classes, order_out,
                               wait_out, totals_out);
   if (rc != SEM_OK) return rc;
-  if (num_segments == 0) return SEM_OK;
   std::lock_guard<std::mutex> g(state().mu);
   const hipStream_t st = state().stream;
+  // the offsets are read once, to size the workspace of the long queues
   std::vector<int64_t> off((size_t)num_segments + 1);
   HIP_TRY(hipMemcpyAsync(off.data(), offsets, off.size() * sizeof(int64_t),
                          hipMemcpyDeviceToHost, st));
   HIP_TRY(hipStreamSynchronize(st));
   if (off[0] != 0) return SEM_EINVAL;
-  int64_t counts[4] = {0, 0, 0, 0};
-  int64_t seg_max = 0;
-  std::vector<int64_t> big;
+  uint64_t long_elems = 0;
   for (int64_t s = 0; s < num_segments; ++s) {
     const int64_t m = off[s + 1] - off[s];
     if (m < 0 || m > INT32_MAX) return SEM_EINVAL;
-    seg_max = std::max(seg_max, m);
-    if (m <= kSegTinyCap) ++counts[0];
-    else if (m <= kSegSmallCap) ++counts[1];
-    else if (m <= kSegMediumCap) ++counts[2];
-    else if (m <= kSegLargeCap) ++counts[3];
-    else big.push_back(s);
+    if (m > kSegLargeCap) long_elems += (uint64_t)m;
   }
-  size_t need = kHeaderBytes;
-  for (int64_t s : big) need = std::max(need, layout_for(off[s + 1] - off[s]).total);
+  const size_t need = batched_layout(num_segments, long_elems).total;
   void* ws = nullptr;
   rc = cached_workspace(need, &ws);
   if (rc != SEM_OK) return rc;
-  uint32_t* flags = static_cast<uint32_t*>(ws);
-  if (launch_fill_zero(flags, 1, st) != hipSuccess) return SEM_EDEVICE;
-  SegArgs a = {};
-  a.priority = priority;
-  a.length = length;
-  a.offsets = offsets;
-  a.num_segments = num_segments;
-  a.n_total = off[num_segments];
-  a.max_segment = INT64_MAX;  // long queues are simply not routed to the LDS kernels
-  a.num_classes = num_classes;
-  a.order = order_out;
-  a.wait = wait_out;
-  a.totals = reinterpret_cast<uint64_t*>(totals_out);
-  a.flags = flags;
-  rc = enqueue_segments(a, std::min<int64_t>(seg_max, kSegLargeCap), counts, st);
+  rc = enqueue_batched(priority, length, offsets, num_segments, num_classes, order_out,
+                       wait_out, totals_out, ws, need, st);
   if (rc != SEM_OK) return rc;
-  rc = finish(ws, st);
-  if (rc != SEM_OK) return rc;
-  for (int64_t s : big) {
-    const int64_t b = off[s];
-    rc = enqueue_queue(priority + b, length + b, off[s + 1] - b, num_classes, order_out + b,
-                       wait_out + b, totals_out + s * (1 + (int64_t)num_classes), ws, st);
-    if (rc != SEM_OK) return rc;
-    rc = finish(ws, st);
-    if (rc != SEM_OK) return rc;
-  }
-  return SEM_OK;
+  return finish(ws, st);
 }
 
 }  // extern "C"

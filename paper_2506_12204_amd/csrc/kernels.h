@@ -11,29 +11,73 @@ constexpr uint32_t kFlagInval = 1u;  // bad offsets / queue longer than promised
 constexpr uint32_t kFlagRange = 2u;  // length < 0 or priority >= num_classes
 constexpr uint32_t kFlagDevice = 4u; // a grid barrier timed out (workgroups not co-resident)
 
-// Queue-size classes of the LDS path (one workgroup per queue).
-constexpr int kSegTinyCap = 256;      // 64 threads x 4 rounds
-constexpr int kSegSmallCap = 1024;    // 256 threads x 4 rounds
-constexpr int kSegMediumCap = 4096;   // 256 threads x 16 rounds
-constexpr int kSegLargeCap = 16384;   // 512 threads x 32 rounds
-enum class SegSize { kTiny, kSmall, kMedium, kLarge };
+// ---------------------------------------------------------------------------
+// Queues scheduled inside one workgroup's LDS (batched.hip).
+//
+// Size classes of the batched call. A queue of at most kSegTinyCap requests
+// is scheduled by one wave; up to kSegMediumCap by a 256-thread workgroup;
+// up to kSegLargeCap (and every shorter queue whose key does not fit a
+// 32-bit element) by a 512-thread workgroup on 64-bit elements; longer
+// queues by the multi-workgroup segmented sort.
+constexpr int kSegTinyCap = 256;
+constexpr int kSegMediumCap = 4096;
+constexpr int kSegLargeCap = 16384;
+constexpr int kLongTile = 8192;   // requests per tile of the segmented sort
 
-struct SegArgs {
-  const uint8_t* priority;
-  const int32_t* length;
-  const int64_t* offsets;  // null: one queue of n_total requests
-  int64_t num_segments;
-  int64_t n_total;
-  int64_t max_segment;     // longer queues are reported as kFlagInval
-  int32_t num_classes;     // validation bound and totals stride - 1
-  int32_t* order;
-  int64_t* wait;
-  uint64_t* totals;        // (lo, hi) pairs, num_segments * (1 + num_classes)
-  uint32_t* flags;
-  int64_t route_lo, route_hi;  // this launch handles route_lo < m <= route_hi
+// Work lists of the batched call, one per kernel.
+enum BList { kListTiny = 0, kListMedium = 1, kListWide = 2, kListLong = 3, kLists = 4 };
+constexpr int kSubLists = 8;      // per list: one grab counter per XCD
+
+// Per-call control block at the start of a batched workspace (after the
+// 64-byte flags line), followed by the grab counters.
+struct BCtl {
+  uint32_t count[kLists];             // entries of every list
+  uint32_t empty[kLists][kSubLists];  // 1 once a sub-list was found exhausted (a hint)
+  uint64_t long_elems;                // requests in the long list's queues
+  uint32_t ranges[4];                 // long queues: pmin, pmax, lmin, lmax
+};
+// Next batch index of one sub-list, alone in its 128-byte line: atomics on
+// one line are serialised wherever they come from, so counters that shared a
+// line would be one counter.
+struct alignas(128) GrabLine {
+  uint32_t next;
+  uint32_t pad[31];
 };
 
-hipError_t launch_segment_schedule(SegArgs a, SegSize size, int grid, hipStream_t st);
+struct BArgs {
+  const uint8_t* priority;
+  const int32_t* length;
+  const int64_t* offsets;   // [num_segments + 1]; null: one queue of n_single requests
+  int64_t num_segments;
+  int64_t n_single;
+  int32_t num_classes;      // validation bound and totals stride - 1
+  int32_t* order;
+  int64_t* wait;
+  uint64_t* totals;         // (lo, hi) pairs, num_segments * (1 + num_classes)
+  uint32_t* flags;
+  BCtl* ctl;
+  GrabLine* grab;           // [kLists][kSubLists]
+  uint32_t* lists;          // [kLists][num_segments] queue indices
+  // segmented sort of the long queues (capacity: requests in long queues)
+  uint64_t long_cap;
+  uint32_t max_tiles;
+  uint64_t* keys[2];        // [long_cap]
+  uint32_t* ids[2];         // [long_cap]
+  uint32_t* hist;           // [max_tiles][256] digit counts, then offsets
+  uint64_t* tsum;           // [max_tiles] length sums, then wait bases
+  uint64_t* lbase;          // [long list + 1] start of every long queue in keys/ids
+  uint32_t* tstart;         // [long list + 1] first tile of every long queue
+};
+
+// Single queue of a.n_single <= kSegLargeCap requests (a.offsets null), one
+// workgroup, any key width.
+hipError_t launch_single_lds(const BArgs& a, hipStream_t st);
+// The whole batched schedule: planner, the LDS kernels of every size class,
+// the segmented sort of long queues. a.flags and a.ctl zeroed by the caller.
+hipError_t launch_batched(const BArgs& a, hipStream_t st);
+// Workspace parts of the segmented sort for `long_cap` requests in long
+// queues out of num_segments queues.
+uint32_t long_max_tiles(uint64_t long_cap, int64_t num_segments);
 
 // ---------------------------------------------------------------------------
 // Global multi-pass path (one queue longer than kSegLargeCap).

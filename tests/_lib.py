@@ -34,10 +34,14 @@ def gpu_queue(p: np.ndarray, l: np.ndarray):
     return order.cpu().numpy(), wait.cpu().numpy(), totals
 
 
-def gpu_batched(p, l, offsets, num_classes, max_segment=None):
+def gpu_batched(p, l, offsets, num_classes, blocking=False, long_requests=None):
+    """Batched schedule through the C ABI: the asynchronous call (workspace
+    room for ``long_requests`` requests of long queues, default all) or the
+    blocking one."""
     import paper_2506_12204_amd as ss
     tp, tl, to = to_gpu(p.astype(np.uint8), l.astype(np.int32), offsets.astype(np.int64))
-    order, wait, totals = ss.schedule_batched(tp, tl, to, num_classes, max_segment)
+    order, wait, totals = ss.schedule_batched(tp, tl, to, num_classes, blocking=blocking,
+                                              long_requests=long_requests)
     return order.cpu().numpy(), wait.cpu().numpy(), totals
 
 

@@ -41,11 +41,9 @@ def test_strerror(ss):
 
 
 def test_workspace_sizes(ss):
-    small = ss.workspace_bytes(16384, 1)
     big = ss.workspace_bytes(1 << 20, 1)
-    assert small == 256
     assert big > 24 * (1 << 20)  # two u64 key buffers + two u32 id buffers
-    assert ss.workspace_bytes(1 << 20, 1000) == 256
+    assert ss.workspace_bytes(0, 1) >= 256
     assert ss.workspace_bytes(-1, 1) == 0
 
 
@@ -76,11 +74,28 @@ def test_batched_argument_errors(ss):
     assert L.sem_schedule_batched(fake, fake, nul, 3, 4, fake, fake, fake) == ss.SEM_EINVAL
     assert L.sem_schedule_batched(fake, fake, fake, 3, 4, fake, fake, nul) == ss.SEM_EINVAL
     A = L.sem_schedule_batched_async
-    assert A(fake, fake, fake, 3, 4, 10, ss.SEGMENT_CAP + 1, fake, fake, fake, fake, 256,
-             nul) == ss.SEM_ENOTIMPL
-    assert A(fake, fake, fake, 3, 4, -1, 5, fake, fake, fake, fake, 256, nul) == ss.SEM_EINVAL
-    assert A(fake, fake, fake, 3, 4, 10, 5, fake, fake, fake, fake, 128, nul) == ss.SEM_EINVAL
-    assert L.sem_check(nul, nul) == ss.SEM_EINVAL
+    fixed = ss.workspace_bytes(0, 3)
+    assert fixed > 256  # header and work lists
+    # workspace missing, too small for the fixed part, or misaligned
+    assert A(fake, fake, fake, 3, 4, fake, fake, fake, nul, fixed, nul) == ss.SEM_EINVAL
+    assert A(fake, fake, fake, 3, 4, fake, fake, fake, fake, fixed - 1, nul) == ss.SEM_EINVAL
+    assert A(fake, fake, fake, 3, 4, fake, fake, fake, ctypes.c_void_p((1 << 40) + 8), fixed,
+             nul) == ss.SEM_EINVAL
+    assert A(fake, fake, fake, 1 << 31, 4, fake, fake, fake, fake, 1 << 40, nul) == ss.SEM_EINVAL
+    assert A(fake, fake, nul, 3, 4, fake, fake, fake, fake, fixed, nul) == ss.SEM_EINVAL
+
+
+def test_batched_workspace_sizes(ss):
+    # room for long queues grows with the bound on their requests
+    base = ss.workspace_bytes(0, 1000)
+    assert base >= 256 + 4 * 4 * 1000
+    assert ss.workspace_bytes(100000, 1000) > base + 24 * 100000
+    assert ss.workspace_bytes(-1, 1000) == 0
+    assert ss.workspace_bytes(10, -1) == 0
+    # one queue: enough for either call
+    assert ss.workspace_bytes(1 << 20, 1) >= max(ss.workspace_bytes(1 << 20, 2) - 16,
+                                                24 * (1 << 20))
+    assert ss.lib.sem_check(ctypes.c_void_p(0), ctypes.c_void_p(0)) == ss.SEM_EINVAL
 
 
 def test_binding_type_checks(ss):

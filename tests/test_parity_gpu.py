@@ -33,10 +33,13 @@ def check_queue(p, l, label):
     assert_same(gpu_queue(p, l), c_oracle_queue(p, l), label)
 
 
-def check_batched(p, l, off, classes, label, max_segment=None):
-    say(f"[gpu] batched {label}: n={len(p)} segments={len(off) - 1}")
-    assert_same(gpu_batched(p, l, off, classes, max_segment),
-                c_oracle_batched(p, l, off, classes), label)
+def check_batched(p, l, off, classes, label, forms=("async", "blocking"), want=None):
+    if want is None:
+        want = c_oracle_batched(p, l, off, classes)
+    for form in forms:
+        say(f"[gpu] batched {label} ({form}): n={len(p)} segments={len(off) - 1}")
+        assert_same(gpu_batched(p, l, off, classes, blocking=form == "blocking"), want,
+                    f"{label}-{form}")
 
 
 # ---- the five workloads at full size -----------------------------------------
@@ -51,8 +54,10 @@ def test_workload_queue(name):
 def test_workload_batched(name):
     w = generate(name)
     check_batched(w.priority, w.length, w.offsets, w.num_classes, name)
-    maxseg = int(np.diff(w.offsets).max())
-    check_batched(w.priority, w.length, w.offsets, w.num_classes, name + "-async", maxseg)
+    # the workspace without room for long queues (these workloads have none)
+    say(f"[gpu] batched {name} (async, no long-queue room)")
+    assert_same(gpu_batched(w.priority, w.length, w.offsets, w.num_classes, long_requests=0),
+                c_oracle_batched(w.priority, w.length, w.offsets, w.num_classes), name)
 
 
 def test_batched_repeat_many_workgroups_per_cu():
@@ -64,7 +69,7 @@ def test_batched_repeat_many_workgroups_per_cu():
     for k in range(4):
         say(f"[gpu] c5 repeat {k}")
         assert_same(gpu_batched(w.priority, w.length, w.offsets, w.num_classes,
-                                4096 if k % 2 else None), want, f"c5-repeat{k}")
+                                blocking=k % 2 == 1), want, f"c5-repeat{k}")
 
 
 # ---- sizes around every tile and LDS-class boundary -----------------------------
@@ -244,7 +249,7 @@ def test_batched_unaligned_inputs():
     to = _shifted(off, np.int64)
     assert tl.data_ptr() % 16 != 0 and tp.data_ptr() % 4 != 0
     say(f"[gpu] batched unaligned: n={len(p)}")
-    order, wait, totals = ss.schedule_batched(tp, tl, to, 6, None)
+    order, wait, totals = ss.schedule_batched(tp, tl, to, 6)
     assert_same((order.cpu().numpy(), wait.cpu().numpy(), totals),
                 c_oracle_batched(p, l, off, 6), "batched-unaligned")
 
@@ -257,10 +262,53 @@ def test_batched_mixed_sizes_and_empty_queues():
     check_batched(p, l, off, 6, "mixed")
 
 
+def test_batched_long_and_many_small_queues():
+    # queues of every size class, long ones among thousands of small ones
+    rng = np.random.default_rng(24)
+    sizes = rng.integers(0, 600, 5000)
+    sizes[[0, 1, 2, 3, 4]] = [0, 1, 16384, 16385, 70000]
+    sizes[[2500, 4999]] = [40000, 17000]
+    rng.shuffle(sizes)
+    p, l, off = fuzz_segments(sizes, seed=25, classes=5, max_len=32768)
+    check_batched(p, l, off, 5, "long-and-small")
+
+
+def test_batched_many_long_queues():
+    sizes = [16385 + 977 * k for k in range(24)] + [3, 0, 200000]
+    p, l, off = fuzz_segments(sizes, seed=26, classes=8, max_len=100000)
+    check_batched(p, l, off, 8, "many-long")
+
+
+def test_batched_one_long_queue():
+    p, l, off = fuzz_segments([300000], seed=27, classes=5, max_len=32768)
+    check_batched(p, l, off, 5, "one-long")
+
+
+def test_batched_wide_keys_in_short_queues():
+    # lengths over the whole int32 range: short queues whose key does not fit
+    # a 32-bit element go to the 64-bit kernel, long ones to the segmented sort
+    sizes = [5, 256, 300, 2000, 4096, 5000, 16384, 20000, 1]
+    p, l, off = fuzz_segments(sizes, seed=28, classes=256, max_len=2**31 - 1)
+    l[off[2]] = 0
+    l[off[3]] = 2**31 - 1
+    check_batched(p, l, off, 256, "wide-keys")
+
+
+def test_batched_long_queue_totals_beyond_2_64():
+    # one class, every length 2^31 - 1: the queue's total exceeds 2^64
+    n = 200_000
+    p = np.zeros(n + 10, np.uint8)
+    l = np.full(n + 10, 2**31 - 1, np.int32)
+    off = np.array([0, 10, n + 10], np.int64)
+    want = c_oracle_batched(p, l, off, 1)
+    assert want[2][2] > 2**64
+    check_batched(p, l, off, 1, "long-128bit", want=want)
+
+
 def test_batched_async_small():
     sizes = np.random.default_rng(1).integers(0, 700, 3000)
     p, l, off = fuzz_segments(sizes, seed=22, classes=4, max_len=400)
-    check_batched(p, l, off, 4, "async", max_segment=int(sizes.max()))
+    check_batched(p, l, off, 4, "async-small")
 
 
 def test_batched_single_class_count():
@@ -279,14 +327,24 @@ def test_negative_length_is_range_error(n):
         gpu_queue(p, l)
 
 
-def test_priority_out_of_range_in_batched():
+@pytest.mark.parametrize("sizes,where", [([10, 20, 30], 15), ([10, 300, 30], 200),
+                                         ([10, 20000, 30], 12345), ([5, 5000, 7], 2000)])
+def test_priority_out_of_range_in_batched(sizes, where):
     import paper_2506_12204_amd as ss
-    p, l, off = fuzz_segments([10, 20, 30], seed=2, classes=4)
-    p[15] = 4
-    with pytest.raises(ss.SemschedRangeError):
-        gpu_batched(p, l, off, 4)
-    with pytest.raises(ss.SemschedRangeError):
-        gpu_batched(p, l, off, 4, max_segment=30)
+    p, l, off = fuzz_segments(sizes, seed=2, classes=4)
+    p[where] = 4
+    for blocking in (False, True):
+        with pytest.raises(ss.SemschedRangeError):
+            gpu_batched(p, l, off, 4, blocking=blocking)
+
+
+def test_negative_length_in_long_batched_queue():
+    import paper_2506_12204_amd as ss
+    p, l, off = fuzz_segments([10, 20000, 30], seed=5, classes=4)
+    l[9000] = -1
+    for blocking in (False, True):
+        with pytest.raises(ss.SemschedRangeError):
+            gpu_batched(p, l, off, 4, blocking=blocking)
 
 
 def test_bad_offsets():
@@ -294,12 +352,28 @@ def test_bad_offsets():
     p, l, off = fuzz_segments([10, 20, 30], seed=3, classes=4)
     bad = off.copy()
     bad[2] = 5  # decreasing
+    for blocking in (False, True):
+        with pytest.raises(ss.SemschedError):
+            gpu_batched(p, l, bad, 4, blocking=blocking)
+    bad = off.copy()
+    bad[0] = 1  # not starting at 0
+    for blocking in (False, True):
+        with pytest.raises(ss.SemschedError):
+            gpu_batched(p, l, bad, 4, blocking=blocking)
+
+
+def test_long_queue_without_workspace_room():
+    import paper_2506_12204_amd as ss
+    p, l, off = fuzz_segments([10, 20000, 30], seed=6, classes=4)
+    with pytest.raises(ss.SemschedError) as e:
+        gpu_batched(p, l, off, 4, long_requests=0)
+    assert e.value.code == ss.SEM_EINVAL
     with pytest.raises(ss.SemschedError):
-        gpu_batched(p, l, bad, 4)
-    with pytest.raises(ss.SemschedError):
-        gpu_batched(p, l, bad, 4, max_segment=30)
-    with pytest.raises(ss.SemschedError):  # a queue longer than promised
-        gpu_batched(p, l, off, 4, max_segment=20)
+        gpu_batched(p, l, off, 4, long_requests=15000)
+    # exactly enough room
+    check_batched(p, l, off, 4, "exact-room", forms=("async",))
+    assert_same(gpu_batched(p, l, off, 4, long_requests=20000),
+                c_oracle_batched(p, l, off, 4), "exact-room")
 
 
 def test_after_error_next_call_is_clean():
