@@ -111,6 +111,73 @@ def code_sha(path: str) -> str:
     return hashlib.sha256("\n".join(lines).encode()).hexdigest()
 
 
+def host_info() -> dict:
+    """The host the CPU baselines ran on: usable threads and CPU model."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"nproc": usable, "cpu_count": os.cpu_count(), "cpu_model": model}
+
+
+def median_of_runs(fn, runs: int = 3):
+    """Median wall time (s) of `runs` calls of fn, and the first call's result."""
+    import statistics
+    times, first = [], None
+    for k in range(runs):
+        t = time.perf_counter()
+        r = fn()
+        times.append(time.perf_counter() - t)
+        if k == 0:
+            first = r
+    return statistics.median(times), first
+
+
+def time_steps(step, steps: int):
+    """Run `steps` steps on torch's current stream with an event before each
+    and after the last: per-step times, their median and mean (ms). The
+    device is synchronised before the first event and after the last."""
+    import statistics
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for k in range(steps):
+        step(k)
+        ev[k + 1].record()
+    torch.cuda.synchronize()
+    per = [ev[k].elapsed_time(ev[k + 1]) for k in range(steps)]
+    return per, statistics.median(per), ev[0].elapsed_time(ev[-1]) / steps
+
+
+def profile_values(path: str, source: str, keys, n: int):
+    """`key: value` figures of a committed rocprofv3 summary, or None when it
+    was taken on another version of `source` (comments aside) or another n."""
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith(("|", "#", " ")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip().strip("`")
+    if kv.get("code_sha256") != code_sha(source) or kv.get("n") != str(n):
+        return None
+    try:
+        return {k: float(kv[k]) for k in keys}
+    except (KeyError, ValueError):
+        return None
+
+
 def counter_traffic(n: int, counters: str = COUNTERS, source: str = FINAL_SOURCE,
                     prefix: str = ""):
     """HBM bytes per launch of a kernel from committed rocprofv3 counters.
@@ -154,17 +221,6 @@ def copy_probe() -> int:
     ms = s.elapsed_time(e) / 10
     print(json.dumps({"copy_bytes": 4 * n, "ms": ms, "read_plus_write_GBps": 8 * n / ms / 1e6}))
     return 0
-
-
-def cpu_baseline(p, l, order, wait, totals):
-    """Time the C oracle on this host's cores and check the GPU result against it."""
-    from oracle import c_oracle_queue
-    t0 = time.perf_counter()
-    o_order, o_wait, o_totals = c_oracle_queue(p, l)
-    dt = time.perf_counter() - t0
-    same = (o_order.tobytes() == order.tobytes() and o_wait.tobytes() == wait.tobytes()
-            and list(o_totals) == list(totals))
-    return dt, same
 
 
 INSERT_ARRIVALS = 1 << 16
@@ -478,16 +534,19 @@ def bench_cost(args) -> int:
     return 0
 
 
+BATCHED_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "batched.hip")
+
+
 def bench_batched(args) -> int:
-    """Batched independent queues through the allocation-free async entry
-    point: outputs and workspace allocated once, K calls enqueued back to
-    back on torch's current stream and bracketed by events on it. Bytes per
-    request as in the single queue (rank and length read; order and wait
-    written) plus each queue's offset and 128-bit totals."""
+    """Batched independent queues through the asynchronous entry point:
+    outputs and workspace allocated once, K calls enqueued back to back on
+    torch's current stream, an event before every call. Bytes per request as
+    in the single queue (rank and length read; order and wait written) plus
+    each queue's offset and 128-bit totals."""
     import numpy as np
     import torch
     import paper_2506_12204_amd as ss
-    from workloads import generate
+    from workloads import generate, workload_sha256
 
     w = generate(args.workload)
     n = w.n
@@ -510,7 +569,7 @@ def bench_batched(args) -> int:
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     stream = ss._stream_handle(dev)
 
-    def run():
+    def run(_k=0):
         rc = ss.lib.sem_schedule_batched_async(
             ss._ptr(p), ss._ptr(l), ss._ptr(off), s, c, ss._ptr(order),
             ss._ptr(wait), ss._ptr(totals), ss._ptr(ws), ws_bytes, stream)
@@ -524,19 +583,15 @@ def bench_batched(args) -> int:
     for _ in range(args.warmup):
         run()
     check()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize()
-    ev[0].record()
-    for _ in range(args.steps):
-        run()
-    ev[1].record()
-    torch.cuda.synchronize()
+    per, ms_step, ms_mean = time_steps(run, args.steps)
     check()
-    ms_step = ev[0].elapsed_time(ev[1]) / args.steps
     alg_bytes = 17 * n + 8 * (s + 1) + 16 * s * (1 + c)
     gbps = alg_bytes / (ms_step * 1e-3) / 1e9
-    print(f"[bench] {args.steps} calls: {ms_step:.4f} ms each, {gbps:.0f} GB/s algorithmic",
-          file=sys.stderr, flush=True)
+    print(f"[bench] {args.steps} calls: median {ms_step:.4f} ms (mean {ms_mean:.4f}), "
+          f"{gbps:.0f} GB/s algorithmic", file=sys.stderr, flush=True)
+    prof = profile_values(os.path.join(ROOT, "profiles", f"batched_{args.workload}_counters.md"),
+                          BATCHED_SOURCE, ["hbm_bytes_per_call"], n)
+    traffic = prof["hbm_bytes_per_call"] if prof else None
     out = {
         "metric": "scheduled requests/sec, batched independent queues, 1 GPU",
         "value": n / (ms_step * 1e-3),
@@ -545,17 +600,44 @@ def bench_batched(args) -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_mean": ms_mean,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "n": n, "queues": s,
-                   "parallelism": "single GPU"},
+                   "parallelism": "single GPU", "input_sha256": workload_sha256(w)},
         "roofline": {"bound": "hbm", "kernel": "whole batched call", "achieved": gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS,
-                     "traffic": None, "bytes_per_request": 17},
+                     "traffic": traffic, "bytes_per_request": 17,
+                     "counter_GBps": (traffic / (ms_step * 1e-3) / 1e9) if traffic else None},
     }
+    if not args.no_cpu_baseline:
+        from oracle import c_oracle_batched, c_oracle_batched_parallel
+        dt, want = median_of_runs(lambda: c_oracle_batched(w.priority, w.length, w.offsets, c))
+        dtp, wantp = median_of_runs(
+            lambda: c_oracle_batched_parallel(w.priority, w.length, w.offsets, c))
+        got = (order.cpu().numpy(), wait.cpu().numpy(), ss.totals_to_ints(totals))
+        same = (want[0].tobytes() == got[0].tobytes() and want[1].tobytes() == got[1].tobytes()
+                and list(want[2]) == got[2])
+        host = host_info()
+        out["cpu_baseline"] = {
+            "value": n / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": (f"the full workload (n={n}): the plain C oracle, queue by queue "
+                       f"(merge sort + running sum), single thread, median of 3 runs"),
+            **host,
+        }
+        out["cpu_baseline_parallel"] = {
+            "value": n / dtp, "unit": "requests/s", "cores": wantp[3],
+            "kind": "oracle, queues spread over OpenMP threads",
+            "sample": f"the full workload (n={n}), median of 3 runs",
+            **host,
+        }
+        out["parity"] = "bit-exact vs oracle" if same else "MISMATCH vs oracle"
+        if not same:
+            print(json.dumps(out))
+            return 1
     print(json.dumps(out), flush=True)
     return 0
 
@@ -690,7 +772,7 @@ def bench_iteration(args) -> int:
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c3", choices=["c3", "c2", "c4", "c5"],
                     help="c4 and c5 are batched queues (the schedule op only)")
@@ -723,10 +805,19 @@ def main() -> int:
     if args.workload in ("c4", "c5"):
         return bench_batched(args)
 
-    import numpy as np
+    return bench_queue(args)
+
+
+STEP_COUNTERS = os.path.join(ROOT, "profiles", "c3_step_counters.md")
+
+
+def bench_queue(args) -> int:
+    """The single-queue schedule (default: C3, n = 2^26). One step = one
+    whole schedule; per-step events give the median; the library's stage
+    events give the dominant pass's average duration."""
     import torch
     import paper_2506_12204_amd as ss
-    from workloads import generate
+    from workloads import generate, workload_sha256
 
     w = generate(args.workload)
     n = w.n
@@ -746,31 +837,29 @@ def main() -> int:
     stages = [("hist", ss.STAGE_HIST), ("first", ss.STAGE_FIRST), ("final", ss.STAGE_FINAL)]
     pairs = {name: [(hip.create(), hip.create()) for _ in range(args.steps)]
              for name, _ in stages}
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record()
-    for k in range(args.steps):
+
+    def step(k):
         for name, code in stages:
             ss.trace_stage(code, *pairs[name][k])
         sched.run(p, l)
-    t_end.record()
-    torch.cuda.synchronize()
+
+    per, ms_step, ms_mean = time_steps(step, args.steps)
     sched.check()
-    ms_total = t_start.elapsed_time(t_end)
-    ms_step = ms_total / args.steps
     stage_ms = {name: sum(hip.elapsed_ms(a, b) for a, b in pairs[name]) / args.steps
                 for name, _ in stages}
     for lst in pairs.values():
         for a, b in lst:
             hip.destroy(a)
             hip.destroy(b)
-    print(f"[bench] {args.steps} steps: {ms_step:.4f} ms/step; stages {stage_ms}",
-          file=sys.stderr, flush=True)
+    print(f"[bench] {args.steps} steps: median {ms_step:.4f} ms/step (mean {ms_mean:.4f}); "
+          f"stages {stage_ms}", file=sys.stderr, flush=True)
 
     dom = max(stage_ms, key=stage_ms.get)
     achieved = STAGE_BYTES[dom] * n / (stage_ms[dom] * 1e-3) / 1e9
     traffic = counter_traffic(n) if dom == "final" else None
+    step_prof = profile_values(STEP_COUNTERS, FINAL_SOURCE, ["hbm_bytes_per_step"], n)
+    step_bytes = step_prof["hbm_bytes_per_step"] if step_prof else None
+    step_gbps = step_bytes / (ms_step * 1e-3) / 1e9 if step_bytes else None
     out = {
         "metric": METRIC,
         "value": n / (ms_step * 1e-3),
@@ -779,6 +868,7 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_mean": ms_mean,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -788,6 +878,7 @@ def main() -> int:
             "workload": WORKLOAD_TEXT[args.workload],
             "n": n,
             "parallelism": "single GPU",
+            "input_sha256": workload_sha256(w),
         },
         "roofline": {
             "bound": "hbm",
@@ -799,23 +890,33 @@ def main() -> int:
             "traffic": traffic,
             "bytes_per_request": STAGE_BYTES[dom],
             "avg_launch_ms": stage_ms[dom],
+            # the whole step: algorithmic bytes (17 per request) and the HBM
+            # bytes the counters measured for one step, over the median step time
+            "step_algorithmic_GBps": PATH_BYTES * n / (ms_step * 1e-3) / 1e9,
+            "step_algorithmic_frac": PATH_BYTES * n / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "step_counter_bytes": step_bytes,
+            "step_counter_GBps": step_gbps,
+            "step_frac": step_gbps / HBM_PEAK_GBPS if step_gbps else None,
         },
         "stage_ms": stage_ms,
-        "path_algorithmic_GBps": PATH_BYTES * n / (ms_step * 1e-3) / 1e9,
     }
 
     if not args.no_cpu_baseline:
+        from oracle import c_oracle_queue
         order = sched.order.cpu().numpy()
         wait = sched.wait.cpu().numpy()
         totals = ss.totals_to_ints(sched.totals)
-        dt, same = cpu_baseline(w.priority, w.length, order, wait, totals)
+        dt, want = median_of_runs(lambda: c_oracle_queue(w.priority, w.length))
+        same = (want[0].tobytes() == order.tobytes() and want[1].tobytes() == wait.tobytes()
+                and list(want[2]) == list(totals))
         out["cpu_baseline"] = {
             "value": n / dt,
             "unit": "requests/s",
             "cores": 1,
             "kind": "oracle",
-            "sample": f"the full workload (n={n}), one run of the plain C oracle "
-                      f"(merge sort + running sum), single thread",
+            "sample": f"the full workload (n={n}): the plain C oracle (merge sort + "
+                      f"running sum, 128-bit totals), single thread, median of 3 runs",
+            **host_info(),
         }
         out["parity"] = "bit-exact vs oracle" if same else "MISMATCH vs oracle"
         if not same:

@@ -55,9 +55,10 @@ ORACLE_ERANGE = -2
 
 
 def build_c_oracle() -> str:
-    """Compile oracle.c into liboracle.so (plain gcc, single-threaded)."""
+    """Compile oracle.c into liboracle.so (plain gcc; every oracle function is
+    single-threaded except the OpenMP segment-parallel batched baseline)."""
     tmp = _LIB + ".tmp"
-    subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC",
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-shared", "-fPIC",
                            "-o", tmp, _SRC])
     os.replace(tmp, _LIB)
     return _LIB
@@ -77,6 +78,9 @@ def _load():
     lib.oracle_schedule_batched.argtypes = [vp, vp, vp, i64, ctypes.c_int32,
                                             vp, vp, vp, vp]
     lib.oracle_schedule_batched.restype = ctypes.c_int
+    lib.oracle_schedule_batched_parallel.argtypes = [vp, vp, vp, i64, ctypes.c_int32,
+                                                     vp, vp, vp, vp, vp]
+    lib.oracle_schedule_batched_parallel.restype = ctypes.c_int
     lib.oracle_schedule_policy.argtypes = [ctypes.c_int, vp, vp, i64, vp, vp, vp, vp]
     lib.oracle_schedule_policy.restype = ctypes.c_int
     lib.oracle_service_times.argtypes = [vp, vp, vp, i64, vp, vp]
@@ -190,6 +194,32 @@ def c_oracle_batched(p: np.ndarray, l: np.ndarray, offsets: np.ndarray,
         raise ValueError(f"oracle_schedule_batched failed: {rc}")
     return order, wait, _join128(lo[: s * (1 + num_classes)],
                                  hi[: s * (1 + num_classes)])
+
+
+def c_oracle_batched_parallel(p: np.ndarray, l: np.ndarray, offsets: np.ndarray,
+                              num_classes: int):
+    """c_oracle_batched with the queues spread over the host's threads
+    (OpenMP); the per-queue arithmetic is the same. Returns (order, wait,
+    totals, threads used)."""
+    p = np.ascontiguousarray(p, dtype=np.uint8)
+    l = np.ascontiguousarray(l, dtype=np.int32)
+    offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+    n = p.shape[0]
+    s = offsets.shape[0] - 1
+    order = np.empty(n, np.int32)
+    wait = np.empty(n, np.int64)
+    lo = np.zeros(max(1, s * (1 + num_classes)), np.uint64)
+    hi = np.zeros_like(lo)
+    used = np.zeros(1, np.int32)
+    rc = _load().oracle_schedule_batched_parallel(_ptr(p), _ptr(l), _ptr(offsets), s,
+                                                  num_classes, _ptr(order), _ptr(wait),
+                                                  _ptr(lo), _ptr(hi), _ptr(used))
+    if rc == ORACLE_ERANGE:
+        raise OracleRangeError("length < 0 or priority out of range")
+    if rc != ORACLE_OK:
+        raise ValueError(f"oracle_schedule_batched_parallel failed: {rc}")
+    return order, wait, _join128(lo[: s * (1 + num_classes)],
+                                 hi[: s * (1 + num_classes)]), int(used[0])
 
 
 def c_oracle_insert(p: np.ndarray, l: np.ndarray, n_old: int,

@@ -26,6 +26,7 @@
  * per-class totals are defined the same way for every policy.
  */
 #include <stdint.h>
+#include <omp.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -159,6 +160,54 @@ int oracle_schedule_batched(const uint8_t *pri, const int32_t *len,
   }
   free(recs);
   free(tmp);
+  return rc;
+}
+
+/*
+ * The same schedule of independent queues with the queues spread over the
+ * host's threads (OpenMP): each thread runs the per-queue routine above on
+ * whole queues, with buffers of its own. Only the CPU baseline of the
+ * batched workloads uses it; the arithmetic is schedule_one's.
+ */
+int oracle_schedule_batched_parallel(const uint8_t *pri, const int32_t *len,
+                                     const int64_t *offsets, int64_t num_segments,
+                                     int32_t num_classes, int32_t *order, int64_t *wait,
+                                     uint64_t *totals_lo, uint64_t *totals_hi,
+                                     int32_t *threads_used) {
+  if (num_segments < 0 || num_classes < 1 || num_classes > 256)
+    return ORACLE_EINVAL;
+  if (offsets[0] != 0) return ORACLE_EINVAL;
+  int64_t biggest = 0;
+  for (int64_t s = 0; s < num_segments; ++s) {
+    int64_t m = offsets[s + 1] - offsets[s];
+    if (m < 0 || m > INT32_MAX) return ORACLE_EINVAL;
+    if (m > biggest) biggest = m;
+  }
+  const int64_t stride = 1 + num_classes;
+  int rc = ORACLE_OK;
+  int used = 1;
+#pragma omp parallel
+  {
+    rec_t *recs = (rec_t *)malloc((size_t)(biggest ? biggest : 1) * sizeof(rec_t));
+    rec_t *tmp = (rec_t *)malloc((size_t)(biggest ? biggest : 1) * sizeof(rec_t));
+    int mine = (recs && tmp) ? ORACLE_OK : ORACLE_ENOMEM;
+#pragma omp single
+    used = omp_get_num_threads();
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t s = 0; s < num_segments; ++s) {
+      if (mine != ORACLE_OK) continue;
+      int64_t a = offsets[s], m = offsets[s + 1] - offsets[s];
+      int r = schedule_one(pri + a, len + a, m, num_classes, ORACLE_POLICY_SEMANTIC,
+                           order + a, wait + a, totals_lo + s * stride,
+                           totals_hi + s * stride, recs, tmp);
+      if (r != ORACLE_OK) mine = r;
+    }
+#pragma omp critical
+    if (mine != ORACLE_OK) rc = mine;
+    free(recs);
+    free(tmp);
+  }
+  if (threads_used) *threads_used = used;
   return rc;
 }
 

@@ -98,3 +98,15 @@ def test_c_oracle_range_errors():
     with pytest.raises(OracleRangeError):
         c_oracle_batched(np.array([0, 5], np.uint8), np.array([3, 1], np.int32),
                          np.array([0, 2]), 4)
+
+
+def test_parallel_batched_equals_serial():
+    # the OpenMP baseline spreads whole queues over threads: same results
+    from oracle import c_oracle_batched, c_oracle_batched_parallel
+    from workloads import fuzz_segments
+    sizes = np.random.default_rng(9).integers(0, 900, 400)
+    p, l, off = fuzz_segments(sizes, seed=10, classes=6, max_len=2000)
+    o1, w1, t1 = c_oracle_batched(p, l, off, 6)
+    o2, w2, t2, used = c_oracle_batched_parallel(p, l, off, 6)
+    assert used >= 1
+    assert np.array_equal(o1, o2) and np.array_equal(w1, w2) and t1 == t2

@@ -55,3 +55,15 @@ def test_fuzz_segments_layout():
 @pytest.mark.parametrize("name", sorted(CONFIGS))
 def test_config_names(name):
     assert name in ("c1", "c2", "c3", "c4", "c5")
+
+
+@pytest.mark.parametrize("name", sorted(CONFIGS))
+def test_recorded_sha256(name):
+    # the full-size arrays hash to the values recorded by
+    # tests/golden/write_workload_sha.py: the seeded generators are unchanged
+    import json
+    import os
+    from workloads import workload_sha256
+    with open(os.path.join(os.path.dirname(__file__), "golden", "workload_sha256.json")) as f:
+        want = json.load(f)
+    assert workload_sha256(generate(name)) == want[name]

@@ -14,5 +14,6 @@ from .gen import (  # noqa: F401
     fuzz_queue,
     fuzz_segments,
     sha256_arrays,
+    workload_sha256,
     cost_tokens,
 )

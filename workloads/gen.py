@@ -47,6 +47,7 @@ __all__ = [
     "fuzz_queue",
     "fuzz_segments",
     "sha256_arrays",
+    "workload_sha256",
     "cost_tokens",
 ]
 
@@ -206,6 +207,13 @@ def fuzz_segments(sizes, seed: int, classes: int = 4, max_len: int = 500,
     np.cumsum(sizes, out=offsets[1:])
     p, ln = fuzz_queue(int(offsets[-1]), seed, classes, max_len, tie_frac)
     return p, ln, offsets
+
+
+def workload_sha256(w: "Workload") -> str:
+    """SHA-256 of a workload's arrays (priority, length, offsets if batched)."""
+    if w.offsets is None:
+        return sha256_arrays(w.priority, w.length)
+    return sha256_arrays(w.priority, w.length, w.offsets)
 
 
 def sha256_arrays(*arrays) -> str:
