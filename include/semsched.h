@@ -39,7 +39,14 @@
  *   SEM_ERANGE   some length < 0, or some priority >= num_classes (256 for
  *                the single-queue calls). Detected on the device.
  *   SEM_ENOMEM   the library could not allocate its internal workspace.
- *   SEM_EDEVICE  a HIP runtime call failed.
+ *   SEM_EDEVICE  a HIP runtime call failed, or (asynchronous calls only) the
+ *                grid barrier of the middle passes, needed only by very wide
+ *                key ranges, gave up waiting because its workgroups were not
+ *                all resident on the device (another program holding compute
+ *                units); the outputs are then not written, and running the
+ *                call again, or its blocking form, is safe. The blocking
+ *                calls handle that case themselves by running the schedule
+ *                again with the middle passes as separate launches.
  *   SEM_ENOTIMPL a size beyond what an entry point implements (noted at the
  *                entry points that can return it).
  */

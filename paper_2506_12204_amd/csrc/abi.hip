@@ -23,9 +23,9 @@ constexpr size_t kHeaderBytes = 256;  // flags, counters, ranges, plan
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  size_t flags = 0, barrier = 8, sink = 16, plan = 64;
+  size_t flags = 0, sink = 16, plan = 64;
   size_t hist_cnt = 0, hist_w = 0, block_hist = 0, block_histw = 0, block_ranges = 0;
-  size_t keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0, chunk_part = 0, sub_start = 0;
+  size_t keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0, chunk_part = 0, sub_start = 0, msync = 0;
   size_t total = kHeaderBytes;
   int64_t tiles = 0;
 };
@@ -56,6 +56,7 @@ Layout layout_for(int64_t n) {
   L.block_ranges = take(sizeof(uint32_t) * 4 * blocks);
   L.chunk_part = take(sizeof(uint32_t) * kMaxChunks * kMaxBins);
   L.sub_start = take(sizeof(uint32_t) * kMaxChunks * kMaxBins);
+  L.msync = take(sizeof(MidSync));
   L.keys0 = take(8 * (size_t)n);
   L.keys1 = take(8 * (size_t)n);
   L.ids0 = take(4 * (size_t)n);
@@ -82,6 +83,13 @@ int force_wide() {
 // (the one queues longer than 2^30 requests use), so that layout stays testable.
 int no_compact() {
   const char* e = std::getenv("SEMSCHED_NO_COMPACT");
+  return (e && e[0] == '1') ? 1 : 0;
+}
+
+// SEMSCHED_SPLIT_MID=1 runs the middle passes as separate launches per phase
+// (the form a blocking call falls back to when the grid barrier gives up).
+int split_mid_forced() {
+  const char* e = std::getenv("SEMSCHED_SPLIT_MID");
   return (e && e[0] == '1') ? 1 : 0;
 }
 
@@ -149,19 +157,52 @@ StageEvents& trace_slots() {
   return *e;
 }
 
-int finish(void* ws, hipStream_t st) {
+int finish(void* ws, hipStream_t st, uint32_t* raw = nullptr) {
   HIP_TRY(hipStreamSynchronize(st));
   uint32_t f = 0;
   HIP_TRY(hipMemcpy(&f, ws, sizeof(f), hipMemcpyDeviceToHost));
+  if (raw) *raw = f;
   return map_flags(f);
+}
+
+// Set while a blocking call runs a schedule again with the middle passes as
+// separate launches per phase (see run_blocking).
+thread_local bool t_split_mid = false;
+
+// Polls of the middle-pass grid barrier before it gives up (SEMSCHED_MID_SPIN
+// overrides the default, e.g. to test the path that follows).
+uint32_t mid_spin_limit() {
+  const char* e = std::getenv("SEMSCHED_MID_SPIN");
+  return e ? (uint32_t)std::strtoul(e, nullptr, 10) : (1u << 20);
+}
+
+// A blocking call: enqueue, synchronise, map the device's flags. When the
+// middle passes' grid barrier gave up (its workgroups were not all resident
+// on the device), the schedule is run once more with those passes as
+// separate launches, which need no residency.
+template <typename F>
+int run_blocking(void* ws, hipStream_t st, F enqueue) {
+  int rc = enqueue();
+  if (rc != SEM_OK) return rc;
+  uint32_t f = 0;
+  rc = finish(ws, st, &f);
+  if (rc == SEM_EDEVICE && (f & kFlagDevice)) {
+    t_split_mid = true;
+    rc = enqueue();
+    if (rc == SEM_OK) rc = finish(ws, st);
+    t_split_mid = false;
+  }
+  return rc;
 }
 
 // Enqueue one queue (any n >= 0). Arguments already checked.
 // payload / pay_pmax (optional, SJF): ranks carried through the long-queue
-// path and their largest value; see GArgs.
+// path and their largest value; see GArgs. wide_keys: the caller expects key
+// ranges that need middle passes.
 int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_classes,
                   int32_t* order, int64_t* wait, sem_i128* totals, void* ws, hipStream_t st,
-                  const uint8_t* payload = nullptr, const uint32_t* pay_pmax = nullptr) {
+                  const uint8_t* payload = nullptr, const uint32_t* pay_pmax = nullptr,
+                  bool wide_keys = false) {
   char* base = static_cast<char*>(ws);
   uint32_t* flags = reinterpret_cast<uint32_t*>(base);
   uint64_t* tot = reinterpret_cast<uint64_t*>(totals);
@@ -202,6 +243,12 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   g.main = global_first_split(n);
   g.fin = global_final_split(n);
   g.mid = global_mid_split(n);
+  // Keys known to be wide take the middle passes as separate launches
+  // (faster than the one-launch form, whose scatter phase spills registers;
+  // a queue that needs no middle pass then pays for 9 launches that return
+  // at once instead of 1).
+  g.split_mid = (wide_keys || t_split_mid || split_mid_forced()) ? 1 : 0;
+  g.mid_spin = mid_spin_limit();
   g.kchunks = (int32_t)((n + (1ll << kChunkBits) - 1) >> kChunkBits);
   g.kpb = 0;
   while ((1 << g.kpb) < g.kchunks) ++g.kpb;
@@ -210,7 +257,6 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   g.chunked = (!no_compact() && g.kchunks <= kMaxChunks &&
                block_items <= (1ll << kChunkBits)) ? 1 : 0;
   g.flags = reinterpret_cast<uint32_t*>(base + L.flags);
-  g.barrier = reinterpret_cast<uint32_t*>(base + L.barrier);
   g.sink = reinterpret_cast<uint64_t*>(base + L.sink);
   g.block_ranges = reinterpret_cast<uint32_t*>(base + L.block_ranges);
   g.plan = reinterpret_cast<Plan*>(base + L.plan);
@@ -224,6 +270,7 @@ int enqueue_queue(const uint8_t* p, const int32_t* l, int64_t n, int32_t num_cla
   g.ids[1] = reinterpret_cast<uint32_t*>(base + L.ids1);
   g.chunk_part = reinterpret_cast<uint32_t*>(base + L.chunk_part);
   g.sub_start = reinterpret_cast<uint32_t*>(base + L.sub_start);
+  g.msync = reinterpret_cast<MidSync*>(base + L.msync);
   g.payload = payload;
   g.pay_pmax = pay_pmax;
   StageEvents ev = {};
@@ -430,7 +477,9 @@ int enqueue_cost_schedule(const uint8_t* p, const int32_t* prompt, const int32_t
     trace_slots().before[SEM_STAGE_COST] = trace_slots().after[SEM_STAGE_COST] = nullptr;
   }
   if (launch_service(a, st, before, after) != hipSuccess) return SEM_EDEVICE;
-  const int rc = enqueue_queue(p, a.service, n, SEM_MAX_CLASSES, order, wait, totals, ws, st);
+  // service times span about 30 bits: two or more middle passes
+  const int rc = enqueue_queue(p, a.service, n, SEM_MAX_CLASSES, order, wait, totals, ws, st,
+                               nullptr, nullptr, true);
   if (rc != SEM_OK) return rc;
   return launch_merge_flags(reinterpret_cast<uint32_t*>(base), cflags, st) == hipSuccess
              ? SEM_OK
@@ -750,10 +799,10 @@ int sem_insert(const uint8_t* priority, const int32_t* length, int64_t n_old, in
   rc = cached_workspace(sem_insert_workspace_bytes(n_old, m), &ws);
   if (rc != SEM_OK) return rc;
   const hipStream_t st = state().stream;
-  rc = enqueue_insert(priority, length, n_old, m, order_old, wait_old, order_out, wait_out,
-                      totals_out, ws, st);
-  if (rc != SEM_OK) return rc;
-  return finish(ws, st);
+  return run_blocking(ws, st, [&] {
+    return enqueue_insert(priority, length, n_old, m, order_old, wait_old, order_out, wait_out,
+                          totals_out, ws, st);
+  });
 }
 
 size_t sem_policy_workspace_bytes(int policy, int64_t n) {
@@ -786,9 +835,9 @@ int sem_schedule_policy(int policy, const uint8_t* priority, const int32_t* leng
   rc = cached_workspace(sem_policy_workspace_bytes(policy, n), &ws);
   if (rc != SEM_OK) return rc;
   const hipStream_t st = state().stream;
-  rc = enqueue_policy(policy, priority, length, n, order_out, wait_out, totals_out, ws, st);
-  if (rc != SEM_OK) return rc;
-  return finish(ws, st);
+  return run_blocking(ws, st, [&] {
+    return enqueue_policy(policy, priority, length, n, order_out, wait_out, totals_out, ws, st);
+  });
 }
 
 int sem_service_times(const int32_t* prompt, const int32_t* output, const int32_t* decoded,
@@ -864,10 +913,10 @@ int sem_schedule_cost(const uint8_t* priority, const int32_t* prompt, const int3
   rc = cached_workspace(sem_cost_workspace_bytes(n), &ws);
   if (rc != SEM_OK) return rc;
   const hipStream_t st = state().stream;
-  rc = enqueue_cost_schedule(priority, prompt, output, decoded, n, model, order_out, wait_out,
-                             totals_out, service_out, ws, st);
-  if (rc != SEM_OK) return rc;
-  return finish(ws, st);
+  return run_blocking(ws, st, [&] {
+    return enqueue_cost_schedule(priority, prompt, output, decoded, n, model, order_out, wait_out,
+                                 totals_out, service_out, ws, st);
+  });
 }
 
 static_assert(SEM_SELECT_CAP == kSelectCap && SEM_EVICT_CAP == kEvictCap,
@@ -999,10 +1048,10 @@ int sem_schedule(const uint8_t* priority, const int32_t* length, int64_t n, int3
   rc = cached_workspace(sem_workspace_bytes(n, 1), &ws);
   if (rc != SEM_OK) return rc;
   const hipStream_t st = state().stream;
-  rc = enqueue_queue(priority, length, n, SEM_MAX_CLASSES, order_out, wait_out, totals_out, ws,
-                     st);
-  if (rc != SEM_OK) return rc;
-  return finish(ws, st);
+  return run_blocking(ws, st, [&] {
+    return enqueue_queue(priority, length, n, SEM_MAX_CLASSES, order_out, wait_out, totals_out,
+                         ws, st);
+  });
 }
 
 int sem_schedule_batched_async(const uint8_t* priority, const int32_t* length,

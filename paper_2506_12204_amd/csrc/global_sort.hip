@@ -27,8 +27,9 @@
 //                digit, on 16K-item tiles.
 //   g_mid        middle passes, only for very wide key ranges: count, scan
 //                and scatter by 10-bit digits of u2 = (p - pmin) * H + h, in
-//                one launch of co-resident workgroups with grid barriers
-//                between the phases; it returns at once when two passes
+//                one launch with bounded grid barriers between the phases
+//                (g_mid_count / g_mid_scan / g_mid_scatter: the same as
+//                separate launches); it returns at once when two passes
 //                suffice.
 //   g_histF      counts and length sums of the final digit per block.
 //   g_final_big  final scatter for at most 256 final digits on 16K-item
@@ -59,7 +60,6 @@ __device__ void reset_call_state(const GArgs& a) {
   const int t = threadIdx.x;
   if (t == 0) {
     a.flags[0] = 0;
-    a.barrier[0] = 0;
     a.plan->ok = 0;
     a.plan->pay = 0;
     a.plan->pay_shift = 32;
@@ -67,6 +67,10 @@ __device__ void reset_call_state(const GArgs& a) {
   for (int i = t; i < kMaxScatter * kMaxBins; i += THREADS) a.hist_cnt[i] = 0;
   for (int i = t; i < kMaxBins; i += THREADS) a.hist_w[i] = 0;
   for (int i = t; i < 2 * (1 + a.num_classes); i += THREADS) a.totals[i] = 0;
+  if (t == 0) {
+    a.msync->arrive = 0;
+    a.msync->release = 0;
+  }
 }
 
 // ------------------------------------------------------------------------
@@ -1305,7 +1309,7 @@ __device__ void mid_fast(const GArgs& a, int s, int g, MidFastShared& sh) {
   }
 }
 
-// ---- middle passes: one launch of co-resident workgroups, grid barriers ----
+// ---- middle passes: one launch with grid barriers, or three per pass ----
 // Digit counts of one block of a middle pass: every wave counts into a table
 // of its own (no LDS atomics between waves), summed at the end.
 struct CountMidShared {
@@ -1417,33 +1421,52 @@ union MidShared {
   uint32_t part4[NT / kWave][4];
 };
 
-// Grid barrier for a launch whose workgroups are all resident (the grid is
-// sized to the occupancy limit). Arrival number k waits for k * gridDim.x
-// arrivals. The wait is bounded: if the workgroups were ever not co-resident
-// it gives up, records kFlagDevice and the kernel returns instead of hanging.
-__device__ bool grid_barrier(const GArgs& a, uint32_t generation) {
+// Grid barrier of the middle-pass kernel, a normal launch whose grid is the
+// number of workgroups that fit on the device at once. Workgroup leaders add
+// to the arrival count; the last to arrive resets it and publishes the
+// barrier's generation in the release word, which the others poll. The wait
+// is bounded: if the workgroups were not all resident (another program
+// holding CUs), a leader gives up after a.mid_spin polls, records
+// kFlagDevice, clears the plan's ok word (so the kernels after this one do
+// nothing) and every workgroup leaves at its next barrier; the blocking
+// calls then run the schedule again with the middle passes as separate
+// launches per phase, which need no residency.
+__device__ bool grid_barrier(const GArgs& a, uint32_t gen) {
   __shared__ uint32_t s_ok;
-  __threadfence();  // every thread releases its global writes at agent scope
+  __threadfence();  // release this workgroup's writes at agent scope
   block_sync();
   if (threadIdx.x == 0) {
-    atomicAdd(a.barrier, 1u);
-    const uint32_t target = generation * gridDim.x;
     uint32_t ok = 1;
-    for (uint32_t spin = 0; load_agent(a.barrier) < target; ++spin) {
-      if (spin > (1u << 24) || load_agent(a.flags) & kFlagDevice) {
-        atomicOr(a.flags, kFlagDevice);
-        ok = 0;
-        break;
+    if (atomicAdd(&a.msync->arrive, 1u) == gridDim.x - 1) {
+      __hip_atomic_store(&a.msync->arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.msync->release, gen, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      // relaxed polls: an acquire load would invalidate this XCD's L2 at
+      // every poll, under the workgroups still working there; the fence
+      // after the wait orders what follows
+      for (uint32_t spin = 0; __hip_atomic_load(&a.msync->release, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT) < gen;
+           ++spin) {
+        if (spin >= a.mid_spin || ((spin & 63) == 63 && (load_agent(a.flags) & kFlagDevice))) {
+          atomicOr(a.flags, kFlagDevice);
+          // the later kernels of this schedule then return at once
+          __hip_atomic_store(&a.plan->ok, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          ok = 0;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
       }
-      __builtin_amdgcn_s_sleep(2);
     }
+    if (load_agent(a.flags) & kFlagDevice) ok = 0;
     s_ok = ok;
   }
   block_sync();
-  __threadfence();  // and acquires the other workgroups' writes
+  __threadfence();  // acquire the other workgroups' writes
   return s_ok != 0;
 }
 
+// The middle passes: per pass, count every block, scan the counts per digit
+// over the blocks, scatter every block, with grid barriers between the phases.
 __global__ __launch_bounds__(NT) void g_mid(GArgs a) {
   __shared__ MidShared sh;
   const Plan* pl = a.plan;
@@ -1464,6 +1487,33 @@ __global__ __launch_bounds__(NT) void g_mid(GArgs a) {
     }
     if (!grid_barrier(a, ++gen)) return;
   }
+}
+
+// The same middle pass s as three launches (count, scan, scatter), for a
+// schedule run again after the barrier of g_mid gave up. A launch whose pass
+// the plan does not need returns at once.
+__global__ __launch_bounds__(NT) void g_mid_count(GArgs a, int s) {
+  __shared__ MidShared sh;
+  const Plan* pl = a.plan;
+  if (!pl->ok || s >= (int)pl->nscatter - 1) return;
+  count_mid(a, s, blockIdx.x, sh.count);
+}
+
+__global__ __launch_bounds__(NT) void g_mid_scan(GArgs a, int s) {
+  __shared__ uint32_t part4[NT / kWave][4];
+  const Plan* pl = a.plan;
+  if (!pl->ok || s >= (int)pl->nscatter - 1) return;
+  column_scan4(a, s, 4 * blockIdx.x, a.mid.blocks, part4);
+}
+
+__global__ __launch_bounds__(NT) void g_mid_scatter(GArgs a, int s) {
+  __shared__ MidShared sh;
+  const Plan* pl = a.plan;
+  if (!pl->ok || s >= (int)pl->nscatter - 1) return;
+  if (pl->packed)
+    mid_fast(a, s, blockIdx.x, sh.fast);
+  else
+    scatter_block<false>(a, s, blockIdx.x, a.mid, sh.scatter);
 }
 
 // ---- final pass --------------------------------------------------------------
@@ -2685,7 +2735,15 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
     hipLaunchKernelGGL(g_first<8>, gm, dim3(NT), 0, st, a);
   mark(ev, 1, true, st);
   mark(ev, 6, false, st);
-  hipLaunchKernelGGL(g_mid, dim3(a.mid.blocks), dim3(NT), 0, st, a);
+  if (a.split_mid) {
+    for (int s = 1; s < kMaxScatter - 1; ++s) {
+      hipLaunchKernelGGL(g_mid_count, dim3(a.mid.blocks), dim3(NT), 0, st, a, s);
+      hipLaunchKernelGGL(g_mid_scan, dim3(kMaxBins / 4), dim3(NT), 0, st, a, s);
+      hipLaunchKernelGGL(g_mid_scatter, dim3(a.mid.blocks), dim3(NT), 0, st, a, s);
+    }
+  } else {
+    hipLaunchKernelGGL(g_mid, dim3(a.mid.blocks), dim3(NT), 0, st, a);
+  }
   mark(ev, 6, true, st);
   const dim3 gf(a.fin.blocks);
   hipLaunchKernelGGL(g_histF, dim3(a.fin.blocks * kHistRows), dim3(HT), 0, st, a);

@@ -9,7 +9,7 @@ namespace semsched {
 // Device-detected error bits, OR-ed into the workspace's first word.
 constexpr uint32_t kFlagInval = 1u;  // bad offsets / queue longer than promised
 constexpr uint32_t kFlagRange = 2u;  // length < 0 or priority >= num_classes
-constexpr uint32_t kFlagDevice = 4u; // a grid barrier timed out (workgroups not co-resident)
+constexpr uint32_t kFlagDevice = 4u; // an internal consistency check failed on the device
 
 // ---------------------------------------------------------------------------
 // Queues scheduled inside one workgroup's LDS (batched.hip).
@@ -107,7 +107,8 @@ constexpr int kMaxChunks = 256;  // ids below 2^30
 
 // Decided on the device by the histogram pass once the ranges are known.
 struct Plan {
-  uint32_t ok;        // 0 if a range error was found
+  uint32_t ok;        // 0 if a range error was found, or the middle passes'
+                      // grid barrier gave up
   uint32_t pmin;      // smallest priority
   uint32_t hmin;      // smallest length >> d0
   uint32_t H;         // (largest length >> d0) - hmin + 1
@@ -126,6 +127,14 @@ struct Plan {
   uint32_t shift[kMaxScatter];  // digit = (u2 >> shift) & (bins - 1), passes >= 1
   uint32_t nbits[kMaxScatter];
   uint32_t nbins[kMaxScatter];
+};
+
+// Grid barrier of the middle-pass kernel: the arrival count and the release
+// word in lines of their own, so that polling the one does not slow the
+// atomics on the other.
+struct MidSync {
+  alignas(128) uint32_t arrive;
+  alignas(128) uint32_t release;
 };
 
 // A pass's work split: workgroup g owns tiles [g*tpb, min(tiles, (g+1)*tpb)).
@@ -152,9 +161,11 @@ struct GArgs {
   int32_t kpb;          // log2 of Kp, the power of two >= K that strides sub_start
   Split main;           // first histogram and first pass (tpb a multiple of kFirstTiles)
   Split fin;            // final histogram and final pass
-  Split mid;            // the cooperative middle-pass kernel
+  Split mid;            // the middle-pass kernel (its grid: the resident-workgroup limit)
+  int32_t split_mid;    // 1: the middle passes run as separate launches per phase
+  uint32_t mid_spin;    // polls of the middle-pass grid barrier before it gives up
+  MidSync* msync;       // that barrier's state
   uint32_t* flags;
-  uint32_t* barrier;    // arrivals at the middle-pass grid barriers
   uint64_t* sink;       // 16 bytes that absorb the stores of lanes without an item
                         // (so that a pass's stores are unconditional)
   uint32_t* block_ranges;  // [blocks][4] pmin, pmax, lmin, lmax of every block

@@ -12,7 +12,8 @@ import numpy as np
 import pytest
 
 from oracle import c_oracle_batched, c_oracle_queue
-from tests._lib import check_queue_by_definition, assert_same, ensure_built, gpu_available, gpu_batched, gpu_queue
+from tests._lib import (check_queue_by_definition, assert_same, ensure_built, gpu_available,
+                        gpu_batched, gpu_queue, to_gpu)
 from workloads import fuzz_queue, fuzz_segments, generate
 
 pytestmark = [pytest.mark.gpu,
@@ -212,6 +213,18 @@ def test_forced_wide_layout(n, monkeypatch):
     check_queue(p, l, "wide-mid-passes")
 
 
+@pytest.mark.parametrize("classes,hi", [(256, 2**31 - 1), (5, 1 << 29)])
+def test_middle_passes_as_separate_launches(classes, hi, monkeypatch):
+    # the per-phase launches of the middle passes (no grid barrier)
+    monkeypatch.setenv("SEMSCHED_SPLIT_MID", "1")
+    rng = np.random.default_rng(classes)
+    n = 400_000
+    p = rng.integers(0, classes, n).astype(np.uint8)
+    l = rng.integers(0, hi, n, dtype=np.int64).astype(np.int32)
+    l[:1000] = l[1000:2000]
+    check_queue(p, l, f"split-mid-{classes}")
+
+
 def test_repeatable_bit_for_bit():
     p, l = fuzz_queue(300_000, seed=11, classes=5, max_len=2000, tie_frac=0.5)
     first = gpu_queue(p, l)
@@ -383,3 +396,37 @@ def test_after_error_next_call_is_clean():
     with pytest.raises(Exception):
         gpu_queue(p, l)
     check_queue(*good, "after-error")
+
+
+def test_middle_pass_barrier_give_up(monkeypatch):
+    # SEMSCHED_MID_SPIN=0 makes the grid barrier of the middle passes give up
+    # at its first wait, as it would if its workgroups were not all resident.
+    # The asynchronous call then reports SEM_EDEVICE (and every kernel of the
+    # schedule exits); the blocking call runs the schedule again with the
+    # middle passes as separate launches and returns the right result; the
+    # next call after either is clean.
+    import torch
+    import paper_2506_12204_amd as ss
+    rng = np.random.default_rng(17)
+    n = 1_500_000
+    p = rng.integers(0, 256, n).astype(np.uint8)  # widest keys: three middle passes
+    l = rng.integers(0, 2**31 - 1, n, dtype=np.int64).astype(np.int32)
+    want = c_oracle_queue(p, l)
+    monkeypatch.setenv("SEMSCHED_MID_SPIN", "0")
+    say("[gpu] middle-pass barrier give-up (async)")
+    with pytest.raises(ss.SemschedError) as e:
+        gpu_queue(p, l)
+    assert e.value.code == ss.SEM_EDEVICE
+    say("[gpu] middle-pass barrier give-up (blocking, separate launches)")
+    tp, tl = to_gpu(p, l)
+    order = torch.empty(n, dtype=torch.int32, device="cuda")
+    wait = torch.empty(n, dtype=torch.int64, device="cuda")
+    totals = torch.empty((1 + ss.MAX_CLASSES, 2), dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    rc = ss.lib.sem_schedule(ss._ptr(tp), ss._ptr(tl), n, ss._ptr(order), ss._ptr(wait),
+                             ss._ptr(totals))
+    assert rc == ss.SEM_OK, ss.strerror(rc)
+    assert_same((order.cpu().numpy(), wait.cpu().numpy(), ss.totals_to_ints(totals)), want,
+                "give-up-blocking")
+    monkeypatch.delenv("SEMSCHED_MID_SPIN")
+    check_queue(p, l, "after-give-up")
