@@ -326,18 +326,31 @@ int sem_schedule_cost_async(const uint8_t *priority, const int32_t *prompt,
  *   batch_out [b] DEVICE: the next batch in key order;
  *   pushed_out [b + n_ongoing] DEVICE: the pushed-back requests in key order;
  *   counts_out [2] int64 DEVICE: batch size, pushed-back count.
+ * Sizes up to SEM_SELECT_CAP (b, n_buffer and n_ongoing each) run in one
+ * workgroup's LDS; larger ones sort the lists in chunks and merge them in
+ * the workspace (a few kernels more, no limit below SEM_WIDE_MAX).
  * Errors: SEM_EINVAL (negative sizes, null pointers, an id outside
- * [0, n_ids)), SEM_ENOTIMPL (b, n_buffer or n_ongoing above SEM_SELECT_CAP).
+ * [0, n_ids)), SEM_ENOTIMPL (min(b, n_heap) + n_buffer + n_ongoing above
+ * SEM_WIDE_MAX).
  */
 #define SEM_SELECT_CAP 4096
+#define SEM_WIDE_MAX (1LL << 30)
 int sem_select_batch(const uint8_t *priority, const int32_t *length, const uint8_t *stage,
                      int64_t n_ids, const int32_t *heap_order, int64_t n_heap,
                      const int32_t *buffer, int64_t n_buffer, const int32_t *ongoing,
                      int64_t n_ongoing, int64_t b, int32_t *batch_out, int32_t *pushed_out,
                      int64_t *counts_out);
 
-/* Asynchronous sem_select_batch: workspace of at least 256 bytes (DEVICE,
- * 256-byte aligned) and the stream; errors by sem_check(workspace, stream). */
+/* Workspace size in bytes of sem_select_batch_async: 256 up to the LDS sizes,
+ * then about 24 bytes per candidate and ongoing request (0 for negative
+ * sizes). */
+size_t sem_select_workspace_bytes(int64_t n_heap, int64_t n_buffer, int64_t n_ongoing,
+                                  int64_t b);
+
+/* Asynchronous sem_select_batch: a DEVICE workspace of at least
+ * sem_select_workspace_bytes(n_heap, n_buffer, n_ongoing, b) bytes (256-byte
+ * aligned) and the stream; allocates nothing, does not synchronise; errors by
+ * sem_check(workspace, stream). */
 int sem_select_batch_async(const uint8_t *priority, const int32_t *length,
                            const uint8_t *stage, int64_t n_ids, const int32_t *heap_order,
                            int64_t n_heap, const int32_t *buffer, int64_t n_buffer,
@@ -358,10 +371,12 @@ int sem_select_batch_async(const uint8_t *priority, const int32_t *length,
  *   victims_out [n_cached] DEVICE: the first upto_out[n_demands-1] entries
  *     receive the victims in eviction order;
  *   upto_out [n_demands] int64 DEVICE: victims after each incoming request.
- * Sums of usage and demands must stay below 2^63.
+ * Sums of usage and demands must stay below 2^63. Up to SEM_EVICT_CAP
+ * cached requests are sorted in one workgroup's LDS; more are sorted in
+ * chunks and merged in the workspace.
  * Errors: SEM_EINVAL (negative sizes, null pointers, an id outside [0, n_ids)),
  * SEM_ERANGE (a negative KV size or demand), SEM_ENOTIMPL (n_cached above
- * SEM_EVICT_CAP).
+ * SEM_WIDE_MAX).
  */
 #define SEM_EVICT_CAP 8192
 int sem_evict(const uint8_t *priority, const int32_t *length, int64_t n_ids,
@@ -369,7 +384,13 @@ int sem_evict(const uint8_t *priority, const int32_t *length, int64_t n_ids,
               int64_t capacity, const int64_t *demands, int64_t n_demands,
               int32_t *victims_out, int64_t *upto_out);
 
-/* Asynchronous sem_evict: workspace of at least 256 bytes and the stream. */
+/* Workspace size in bytes of sem_evict_async: 256 up to SEM_EVICT_CAP cached
+ * requests, then about 36 bytes per cached request (0 for n_cached < 0). */
+size_t sem_evict_workspace_bytes(int64_t n_cached);
+
+/* Asynchronous sem_evict: a DEVICE workspace of at least
+ * sem_evict_workspace_bytes(n_cached) bytes (256-byte aligned) and the
+ * stream; allocates nothing, does not synchronise; errors by sem_check. */
 int sem_evict_async(const uint8_t *priority, const int32_t *length, int64_t n_ids,
                     const int32_t *cached, const int64_t *kv, int64_t n_cached, int64_t usage,
                     int64_t capacity, const int64_t *demands, int64_t n_demands,
@@ -430,8 +451,8 @@ const char *sem_strerror(int code);
  *                           that sums the waits per class),
  *          SEM_STAGE_COST  (sem_schedule_cost*: the service-time pass),
  *          SEM_STAGE_MID   (multi-pass path: the middle scatter passes that keys
- *                           wider than two digits need; nothing is launched
- *                           in between for narrower keys).
+ *                           wider than two digits need; for narrower keys one
+ *                           launch that returns at once).
  * Passing NULL events disarms the stage. Returns SEM_EINVAL for an unknown
  * stage. The events are owned by the caller and must outlive the call.
  */

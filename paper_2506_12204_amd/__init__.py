@@ -55,15 +55,18 @@ SYMBOLS = (
     "sem_cost_workspace_bytes",
     "sem_schedule_cost_async",
     "sem_select_batch",
+    "sem_select_workspace_bytes",
     "sem_select_batch_async",
     "sem_evict",
+    "sem_evict_workspace_bytes",
     "sem_evict_async",
     "sem_schedule_static",
 )
 STATIC_MAX_N = 1048576
 STATIC_SCRATCH_BYTES = 33554432
-SELECT_CAP = 4096
-EVICT_CAP = 8192
+SELECT_CAP = 4096  # selection sizes in one workgroup's LDS
+EVICT_CAP = 8192   # cached requests in one workgroup's LDS
+WIDE_MAX = 1 << 30
 PREFILL, DECODE = 0, 1
 STAGE_HIST, STAGE_FIRST, STAGE_FINAL, STAGE_MERGE, STAGE_POLICY, STAGE_COST, STAGE_MID = range(7)
 # comparison policies (Section 4): the key fields before the id
@@ -129,6 +132,10 @@ def _load() -> ctypes.CDLL:
     lib.sem_select_batch.argtypes = [vp, vp, vp, i64, vp, i64, vp, i64, vp, i64, i64, vp, vp, vp]
     lib.sem_select_batch_async.argtypes = [vp, vp, vp, i64, vp, i64, vp, i64, vp, i64, i64, vp,
                                            vp, vp, vp, sz, vp]
+    lib.sem_select_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.sem_select_workspace_bytes.restype = sz
+    lib.sem_evict_workspace_bytes.argtypes = [i64]
+    lib.sem_evict_workspace_bytes.restype = sz
     lib.sem_evict.argtypes = [vp, vp, i64, vp, vp, i64, i64, i64, vp, i64, vp, vp]
     lib.sem_evict_async.argtypes = [vp, vp, i64, vp, vp, i64, i64, i64, vp, i64, vp, vp, vp, sz,
                                     vp]

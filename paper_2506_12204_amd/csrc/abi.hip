@@ -920,7 +920,61 @@ int sem_schedule_cost(const uint8_t* priority, const int32_t* prompt, const int3
 }
 
 static_assert(SEM_SELECT_CAP == kSelectCap && SEM_EVICT_CAP == kEvictCap,
-              "the header's caps are the kernels'");
+              "the header's LDS sizes are the kernels'");
+static_assert(SEM_WIDE_MAX == kWideMax, "the header's largest lists are the kernels'");
+
+// Selection and eviction: one workgroup over LDS up to the SEM_*_CAP sizes;
+// beyond them the workspace holds the sort buffers of the lists (two
+// ping-pong buffers of keys, ids and, for eviction, indices into the caller's
+// arrays), then the kept-member prefix (selection) or the KV prefix sums and
+// the eviction order (eviction).
+bool select_in_lds(int64_t n_buffer, int64_t n_ongoing, int64_t b) {
+  return b <= kSelectCap && n_buffer <= kSelectCap && n_ongoing <= kSelectCap;
+}
+
+struct WideLayout {
+  size_t key[2] = {0, 0}, id[2] = {0, 0}, pay[2] = {0, 0}, dec = 0, psum = 0, eorder = 0;
+  size_t total = kHeaderBytes;
+};
+
+WideLayout wide_layout(int64_t entries, bool evict) {
+  WideLayout L;
+  size_t off = kHeaderBytes;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  const size_t n = (size_t)entries;
+  for (int k = 0; k < 2; ++k) L.key[k] = take(8 * n);
+  for (int k = 0; k < 2; ++k) L.id[k] = take(4 * n);
+  if (evict) {
+    for (int k = 0; k < 2; ++k) L.pay[k] = take(4 * n);
+    L.psum = take(8 * n);
+    L.eorder = take(4 * n);
+  } else {
+    L.dec = take(4 * (n + 1));
+  }
+  L.total = off;
+  return L;
+}
+
+int64_t select_entries(int64_t n_heap, int64_t n_buffer, int64_t n_ongoing, int64_t b) {
+  return std::min(b, n_heap) + n_buffer + n_ongoing;
+}
+
+size_t sem_select_workspace_bytes(int64_t n_heap, int64_t n_buffer, int64_t n_ongoing,
+                                  int64_t b) {
+  if (n_heap < 0 || n_buffer < 0 || n_ongoing < 0 || b < 0) return 0;
+  if (select_in_lds(n_buffer, n_ongoing, b)) return kHeaderBytes;
+  return wide_layout(select_entries(n_heap, n_buffer, n_ongoing, b), false).total;
+}
+
+size_t sem_evict_workspace_bytes(int64_t n_cached) {
+  if (n_cached < 0) return 0;
+  if (n_cached <= kEvictCap) return kHeaderBytes;
+  return wide_layout(n_cached, true).total;
+}
 
 int check_select(const uint8_t* p, const int32_t* l, const uint8_t* stage, int64_t n_ids,
                  const int32_t* heap, int64_t n_heap, const int32_t* buffer, int64_t n_buffer,
@@ -928,7 +982,7 @@ int check_select(const uint8_t* p, const int32_t* l, const uint8_t* stage, int64
                  int32_t* pushed, int64_t* counts) {
   if (n_ids < 0 || n_ids > INT32_MAX || n_heap < 0 || n_buffer < 0 || n_ongoing < 0 || b < 0)
     return SEM_EINVAL;
-  if (b > kSelectCap || n_buffer > kSelectCap || n_ongoing > kSelectCap) return SEM_ENOTIMPL;
+  if (select_entries(n_heap, n_buffer, n_ongoing, b) > kWideMax) return SEM_ENOTIMPL;
   if (!counts) return SEM_EINVAL;
   const bool any = std::min(b, n_heap) + n_buffer + n_ongoing > 0;
   if (any && (!p || !l || !stage)) return SEM_EINVAL;
@@ -944,9 +998,31 @@ int enqueue_select(const uint8_t* p, const int32_t* l, const uint8_t* stage, int
                    int32_t* pushed, int64_t* counts, void* ws, hipStream_t st) {
   SelArgs a = {p, l, stage, n_ids, heap, n_heap, buffer, n_buffer, ongoing, n_ongoing, b,
                batch, pushed, counts, static_cast<uint32_t*>(ws)};
-  if (launch_fill_zero(a.flags, 1, st) != hipSuccess || launch_select(a, st) != hipSuccess)
-    return SEM_EDEVICE;
-  return SEM_OK;
+  if (launch_fill_zero(a.flags, 1, st) != hipSuccess) return SEM_EDEVICE;
+  if (select_in_lds(n_buffer, n_ongoing, b))
+    return launch_select(a, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
+  // candidates (the heap's first b, then the buffer) and ongoing requests
+  const int64_t nh = std::min(b, n_heap);
+  const WideLayout L = wide_layout(nh + n_buffer + n_ongoing, false);
+  char* base = static_cast<char*>(ws);
+  WideSort w = {};
+  w.priority = p;
+  w.length = l;
+  w.n_ids = n_ids;
+  w.kv = nullptr;
+  w.list[0] = {heap, nh, buffer, n_buffer, 0};
+  w.list[1] = {ongoing, n_ongoing, nullptr, 0, nh + n_buffer};
+  w.nlists = 2;
+  w.total = nh + n_buffer + n_ongoing;
+  for (int k = 0; k < 2; ++k) {
+    w.key[k] = reinterpret_cast<uint64_t*>(base + L.key[k]);
+    w.id[k] = reinterpret_cast<uint32_t*>(base + L.id[k]);
+    w.pay[k] = nullptr;
+  }
+  w.flags = a.flags;
+  return launch_select_wide(a, w, reinterpret_cast<uint32_t*>(base + L.dec), st) == hipSuccess
+             ? SEM_OK
+             : SEM_EDEVICE;
 }
 
 int sem_select_batch_async(const uint8_t* priority, const int32_t* length, const uint8_t* stage,
@@ -957,7 +1033,7 @@ int sem_select_batch_async(const uint8_t* priority, const int32_t* length, const
   const int rc = check_select(priority, length, stage, n_ids, heap_order, n_heap, buffer,
                               n_buffer, ongoing, n_ongoing, b, batch_out, pushed_out, counts_out);
   if (rc != SEM_OK) return rc;
-  if (!workspace || ws_bytes < kHeaderBytes ||
+  if (!workspace || ws_bytes < sem_select_workspace_bytes(n_heap, n_buffer, n_ongoing, b) ||
       (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
     return SEM_EINVAL;
   return enqueue_select(priority, length, stage, n_ids, heap_order, n_heap, buffer, n_buffer,
@@ -975,7 +1051,7 @@ int sem_select_batch(const uint8_t* priority, const int32_t* length, const uint8
   if (rc != SEM_OK) return rc;
   std::lock_guard<std::mutex> g(state().mu);
   void* ws = nullptr;
-  rc = cached_workspace(kHeaderBytes, &ws);
+  rc = cached_workspace(sem_select_workspace_bytes(n_heap, n_buffer, n_ongoing, b), &ws);
   if (rc != SEM_OK) return rc;
   const hipStream_t st = state().stream;
   rc = enqueue_select(priority, length, stage, n_ids, heap_order, n_heap, buffer, n_buffer,
@@ -988,7 +1064,7 @@ int check_evict(const uint8_t* p, const int32_t* l, int64_t n_ids, const int32_t
                 const int64_t* kv, int64_t n_cached, const int64_t* demands, int64_t n_demands,
                 int32_t* victims, int64_t* upto) {
   if (n_ids < 0 || n_ids > INT32_MAX || n_cached < 0 || n_demands < 0) return SEM_EINVAL;
-  if (n_cached > kEvictCap) return SEM_ENOTIMPL;
+  if (n_cached > kWideMax) return SEM_ENOTIMPL;
   if (n_cached > 0 && (!p || !l || !cached || !kv || !victims)) return SEM_EINVAL;
   if (n_demands > 0 && (!demands || !upto)) return SEM_EINVAL;
   return SEM_OK;
@@ -1002,7 +1078,29 @@ int enqueue_evict(const uint8_t* p, const int32_t* l, int64_t n_ids, const int32
                  victims, upto, static_cast<uint32_t*>(ws)};
   if (launch_fill_zero(a.flags, 1, st) != hipSuccess) return SEM_EDEVICE;
   if (n_cached + n_demands == 0) return SEM_OK;
-  return launch_evict_victims(a, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
+  if (n_cached <= kEvictCap)
+    return launch_evict_victims(a, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
+  const WideLayout L = wide_layout(n_cached, true);
+  char* base = static_cast<char*>(ws);
+  WideSort w = {};
+  w.priority = p;
+  w.length = l;
+  w.n_ids = n_ids;
+  w.kv = kv;
+  w.list[0] = {cached, n_cached, nullptr, 0, 0};
+  w.list[1] = {nullptr, 0, nullptr, 0, n_cached};
+  w.nlists = 1;
+  w.total = n_cached;
+  for (int k = 0; k < 2; ++k) {
+    w.key[k] = reinterpret_cast<uint64_t*>(base + L.key[k]);
+    w.id[k] = reinterpret_cast<uint32_t*>(base + L.id[k]);
+    w.pay[k] = reinterpret_cast<uint32_t*>(base + L.pay[k]);
+  }
+  w.flags = a.flags;
+  return launch_evict_wide(a, w, reinterpret_cast<uint64_t*>(base + L.psum),
+                           reinterpret_cast<uint32_t*>(base + L.eorder), st) == hipSuccess
+             ? SEM_OK
+             : SEM_EDEVICE;
 }
 
 int sem_evict_async(const uint8_t* priority, const int32_t* length, int64_t n_ids,
@@ -1013,7 +1111,7 @@ int sem_evict_async(const uint8_t* priority, const int32_t* length, int64_t n_id
   const int rc = check_evict(priority, length, n_ids, cached, kv, n_cached, demands, n_demands,
                              victims_out, upto_out);
   if (rc != SEM_OK) return rc;
-  if (!workspace || ws_bytes < kHeaderBytes ||
+  if (!workspace || ws_bytes < sem_evict_workspace_bytes(n_cached) ||
       (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
     return SEM_EINVAL;
   return enqueue_evict(priority, length, n_ids, cached, kv, n_cached, usage, capacity, demands,
@@ -1030,7 +1128,7 @@ int sem_evict(const uint8_t* priority, const int32_t* length, int64_t n_ids,
   if (rc != SEM_OK) return rc;
   std::lock_guard<std::mutex> g(state().mu);
   void* ws = nullptr;
-  rc = cached_workspace(kHeaderBytes, &ws);
+  rc = cached_workspace(sem_evict_workspace_bytes(n_cached), &ws);
   if (rc != SEM_OK) return rc;
   const hipStream_t st = state().stream;
   rc = enqueue_evict(priority, length, n_ids, cached, kv, n_cached, usage, capacity, demands,

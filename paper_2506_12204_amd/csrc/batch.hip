@@ -19,6 +19,8 @@
 //             order gives, for each incoming request, the number of
 //             victims after its step: the shortest prefix covering
 //             usage + (demands so far) - capacity.
+#include <algorithm>
+
 #include "block_common.h"
 #include "kernels.h"
 
@@ -181,8 +183,68 @@ __device__ __forceinline__ uint32_t count_below(const uint64_t* key, const uint3
   return lo;
 }
 
+// Number of entries of a sorted list not above (k, i).
+__device__ __forceinline__ uint32_t count_not_above(const uint64_t* key, const uint32_t* id,
+                                                    uint32_t n, uint64_t k, uint32_t i) {
+  uint32_t lo = 0, hi = n;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (!less(k, i, key[mid], id[mid])) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
 __device__ __forceinline__ uint64_t key_of(const SelArgs& a, uint32_t id) {
   return (uint64_t)a.priority[id] << 32 | (uint32_t)a.length[id];
+}
+
+// Output of entry idx of C (idx < nc) or of O (idx - nc), given both sorted
+// and dec[i] = kept (decoding, or every, when the most urgent entry is in
+// prefill) members of C before index i, for i <= nc. M = kept members of C
+// and O merged by key; the batch is M's first b; pushed back are C's
+// filtered members and M beyond b, merged by key.
+template <typename D>
+__device__ __forceinline__ void select_place(const SelArgs& a, const uint64_t* ckey,
+                                             const uint32_t* cid, uint32_t nc,
+                                             const uint64_t* okey, const uint32_t* oid,
+                                             uint32_t no, const D* dec, uint32_t idx) {
+  // (|M| < 2^31: a larger b places the same way)
+  const uint32_t b = (uint32_t)min(a.b, (int64_t)1 << 31);
+  // members of M below (k, i): kept members of C and members of O
+  auto m_below = [&](uint64_t k, uint32_t i) {
+    const uint32_t c = count_below(ckey, cid, nc, k, i);
+    return (uint32_t)dec[c] + count_below(okey, oid, no, k, i);
+  };
+  // filtered (prefill) members of C below (k, i)
+  auto pre_below = [&](uint64_t k, uint32_t i) {
+    const uint32_t c = count_below(ckey, cid, nc, k, i);
+    return c - (uint32_t)dec[c];
+  };
+  auto place_m = [&](uint32_t q, uint32_t id, uint64_t k) {  // q = position in M
+    if (q < b) {
+      a.batch[q] = (int32_t)id;
+    } else {
+      a.pushed[(q - b) + pre_below(k, id)] = (int32_t)id;
+    }
+  };
+  if (idx < nc) {
+    const uint32_t i = idx;
+    const uint64_t k = ckey[i];
+    const uint32_t id = cid[i];
+    const uint32_t rk = (uint32_t)dec[i];
+    const bool kept = (uint32_t)dec[i + 1] != rk;
+    if (kept) {
+      place_m(rk + count_below(okey, oid, no, k, id), id, k);
+    } else {
+      const uint32_t mb = m_below(k, id);
+      a.pushed[(i - rk) + (mb > b ? mb - b : 0)] = (int32_t)id;
+    }
+  } else {
+    const uint32_t j = idx - nc;
+    const uint64_t k = okey[j];
+    const uint32_t id = oid[j];
+    place_m(j + (uint32_t)dec[count_below(ckey, cid, nc, k, id)], id, k);
+  }
 }
 
 struct SelectShared {
@@ -271,48 +333,52 @@ __global__ __launch_bounds__(BT) void b_select(SelArgs a) {
   }
   if (t == 0) sh.dec_excl[nc] = (uint16_t)ndec;
   block_sync();
-  const uint32_t nm = ndec + no;           // |M|
+  const uint32_t nm = ndec + no;  // |M|
   const uint32_t b = (uint32_t)a.b;
   const uint32_t npre = nc - ndec;
   const uint32_t over = nm > b ? nm - b : 0;  // M beyond the batch
-  // members of M below (k, i): kept members of C and members of O
-  auto m_below = [&](uint64_t k, uint32_t i) {
-    const uint32_t c = count_below(sh.ckey, sh.cid, nc, k, i);
-    return sh.dec_excl[c] + count_below(sh.okey, sh.oid, no, k, i);
-  };
-  // filtered (prefill) members of C below (k, i)
-  auto pre_below = [&](uint64_t k, uint32_t i) {
-    const uint32_t c = count_below(sh.ckey, sh.cid, nc, k, i);
-    return c - sh.dec_excl[c];
-  };
-  auto place_m = [&](uint32_t q, uint32_t id, uint64_t k) {  // q = position in M
-    if (q < b) {
-      a.batch[q] = (int32_t)id;
-    } else {
-      a.pushed[(q - b) + pre_below(k, id)] = (int32_t)id;
-    }
-  };
-  for (uint32_t i = t; i < nc; i += BT) {
-    const uint64_t k = sh.ckey[i];
-    const uint32_t id = sh.cid[i];
-    const uint32_t rk = sh.dec_excl[i];
-    const bool kept = (uint32_t)sh.dec_excl[i + 1] != rk;
-    if (kept) {
-      place_m(rk + count_below(sh.okey, sh.oid, no, k, id), id, k);
-    } else {
-      const uint32_t mb = m_below(k, id);
-      a.pushed[(i - rk) + (mb > b ? mb - b : 0)] = (int32_t)id;
-    }
-  }
-  for (uint32_t j = t; j < no; j += BT) {
-    const uint64_t k = sh.okey[j];
-    const uint32_t id = sh.oid[j];
-    place_m(j + sh.dec_excl[count_below(sh.ckey, sh.cid, nc, k, id)], id, k);
-  }
+  for (uint32_t i = t; i < nc + no; i += BT)
+    select_place(a, sh.ckey, sh.cid, nc, sh.okey, sh.oid, no, sh.dec_excl, i);
   if (t == 0) {
     a.counts[0] = min(b, nm);
     a.counts[1] = npre + over;
   }
+}
+
+// Victims after each incoming request j: the first k of the eviction order
+// whose KV prefix psum[k - 1] reaches need_j = usage + (demands 0..j) -
+// capacity (all nr if none does); then the victims of the last request, in
+// eviction order, from eorder. `last` is a u32 of LDS.
+__device__ __forceinline__ void evict_demands(const EvictArgs& a, const uint64_t* psum,
+                                              const uint32_t* eorder, uint32_t nr,
+                                              uint64_t* scan64, uint32_t* last) {
+  const uint32_t t = threadIdx.x;
+  bool bad = false;
+  int64_t carry = 0;  // demands of the earlier chunks
+  for (int64_t j0 = 0; j0 < a.n_demands; j0 += BT) {
+    const int64_t j = j0 + t;
+    const int64_t s = j < a.n_demands ? a.demands[j] : 0;
+    bad |= s < 0;
+    uint64_t tot;
+    const uint64_t before = block_excl_scan_u64<BT>(s < 0 ? 0 : (uint64_t)s, scan64, tot);
+    const int64_t need = a.usage + carry + (int64_t)before + (s < 0 ? 0 : s) - a.capacity;
+    uint32_t k = 0;
+    if (need > 0) {
+      uint32_t lo = 0, hi = nr;  // first index whose inclusive sum reaches need
+      while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if ((int64_t)psum[mid] >= need) hi = mid; else lo = mid + 1;
+      }
+      k = lo < nr ? lo + 1 : nr;
+    }
+    if (j < a.n_demands) a.upto[j] = k;
+    if (j == a.n_demands - 1) *last = k;
+    carry += (int64_t)tot;  // (every thread holds the chunk's total)
+    block_sync();
+  }
+  if (__ballot(bad) && lane_id() == 0) atomicOr(a.flags, kFlagRange);
+  const uint32_t k_last = a.n_demands > 0 ? *last : 0;
+  for (uint32_t e = t; e < k_last; e += BT) a.victims[e] = (int32_t)eorder[e];
 }
 
 struct EvictShared {
@@ -379,38 +445,225 @@ __global__ __launch_bounds__(BT) void b_evict(EvictArgs a) {
     }
   }
   block_sync();
-  // victims after each incoming request j: the first k whose prefix reaches
-  // need_j = usage + (demands 0..j) - capacity
-  uint32_t k_last = 0;
-  bool bad = false;
-  int64_t carry = 0;  // demands of the earlier chunks
-  for (int64_t j0 = 0; j0 < a.n_demands; j0 += BT) {
-    const int64_t j = j0 + t;
-    const int64_t s = j < a.n_demands ? a.demands[j] : 0;
-    bad |= s < 0;
-    uint64_t tot;
-    const uint64_t before = block_excl_scan_u64<BT>(s < 0 ? 0 : (uint64_t)s, sh.scan64, tot);
-    const int64_t need = a.usage + carry + (int64_t)before + (s < 0 ? 0 : s) - a.capacity;
-    uint32_t k = 0;
-    if (need > 0) {
-      uint32_t lo = 0, hi = nr;  // first index whose inclusive sum reaches need
-      while (lo < hi) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if ((int64_t)sh.key[mid] >= need) hi = mid; else lo = mid + 1;
-      }
-      k = lo < nr ? lo + 1 : nr;
+  evict_demands(a, sh.key, sh.id, nr, sh.scan64, &sh.bad);
+}
+
+// ---- lists beyond one workgroup's LDS -----------------------------------------
+// The lists are sorted in chunks of kWideChunk entries, one workgroup each
+// (the LDS sort above), and the sorted runs are then merged pairwise, one
+// launch per round: an entry's place in the merged run is its index in its
+// own run plus the number of entries of the other run before it, found by
+// binary search (entries of the first run go before equal entries of the
+// second, so the merge keeps the order of equal keys).
+
+__device__ __forceinline__ int64_t list_size(const WideList& l) { return l.n0 + l.n1; }
+__device__ __forceinline__ int64_t list_chunks(const WideList& l) {
+  return (list_size(l) + kWideChunk - 1) / kWideChunk;
+}
+
+template <bool PAY>
+struct ChunkShared {
+  uint64_t key[kWideChunk];
+  uint32_t id[kWideChunk];
+  uint32_t pay[PAY ? kWideChunk : 1];
+  SortScratch sort;
+};
+
+// PAY (eviction): entries carry their index in the caller's arrays, and a
+// negative KV size is a range error. Ids outside [0, n_ids) are reported and
+// sort last; the outputs of a call with an error are not written.
+template <bool PAY>
+__global__ __launch_bounds__(BT) void w_chunk_sort(WideSort a) {
+  __shared__ ChunkShared<PAY> sh;
+  __shared__ uint32_t s_bad;
+  int64_t c = blockIdx.x;
+  const bool second = a.nlists > 1 && c >= list_chunks(a.list[0]);
+  const WideList l = second ? a.list[1] : a.list[0];
+  if (second) c -= list_chunks(a.list[0]);
+  const int64_t c0 = c * kWideChunk;
+  const uint32_t nc = (uint32_t)min((int64_t)kWideChunk, list_size(l) - c0);
+  const uint32_t t = threadIdx.x;
+  if (t == 0) s_bad = 0;
+  block_sync();
+  uint32_t bad = 0;
+  for (uint32_t i = t; i < nc; i += BT) {
+    const int64_t gi = c0 + i;
+    const int32_t v = gi < l.n0 ? l.src0[gi] : l.src1[gi - l.n0];
+    uint64_t k = ~0ull;
+    uint32_t id = ~0u;
+    if (v < 0 || v >= a.n_ids) {
+      bad |= 1u;
+    } else if (PAY && a.kv[gi] < 0) {
+      bad |= 2u;  // negative KV size
+    } else {
+      id = (uint32_t)v;
+      k = (uint64_t)a.priority[id] << 32 | (uint32_t)a.length[id];
     }
-    if (j < a.n_demands) a.upto[j] = k;
-    if (j == a.n_demands - 1) sh.bad = k;
-    carry += (int64_t)tot;  // (every thread holds the chunk's total)
-    block_sync();
+    sh.key[i] = k;
+    sh.id[i] = id;
+    if (PAY) sh.pay[i] = (uint32_t)gi;
   }
-  if (__ballot(bad) && lane_id() == 0) atomicOr(a.flags, kFlagRange);
-  k_last = a.n_demands > 0 ? sh.bad : 0;
-  for (uint32_t e = t; e < k_last; e += BT) a.victims[e] = (int32_t)sh.id[e];
+  if (bad) atomicOr(&s_bad, bad);
+  block_sync();
+  if (t == 0 && s_bad) atomicOr(a.flags, (s_bad & 1u) ? kFlagInval : kFlagRange);
+  block_sort<kWideChunk / BT, PAY>(sh.key, sh.id, sh.pay, nc, sh.sort);
+  for (uint32_t i = t; i < nc; i += BT) {
+    const int64_t o = l.base + c0 + i;
+    a.key[0][o] = sh.key[i];
+    a.id[0][o] = sh.id[i];
+    if (PAY) a.pay[0][o] = sh.pay[i];
+  }
+}
+
+// One merge round: runs of `run` entries (sorted) in buffer `from` become
+// runs of 2 * run in the other buffer.
+template <bool PAY>
+__global__ __launch_bounds__(BT) void w_merge(WideSort a, int64_t run, int from) {
+  const uint64_t* kin = a.key[from];
+  const uint32_t* iin = a.id[from];
+  const int to = from ^ 1;
+  for (int64_t g = (int64_t)blockIdx.x * BT + threadIdx.x; g < a.total;
+       g += (int64_t)gridDim.x * BT) {
+    const bool second = a.nlists > 1 && g >= a.list[1].base;
+    const int64_t base = second ? a.list[1].base : a.list[0].base;
+    const int64_t n = list_size(second ? a.list[1] : a.list[0]);
+    const int64_t i = g - base;
+    const int64_t ps = i / (2 * run) * (2 * run);   // the pair's first entry
+    const int64_t am = min(ps + run, n);             // end of its first run
+    const int64_t be = min(ps + 2 * run, n);         // end of its second run
+    const uint64_t k = kin[g];
+    const uint32_t id = iin[g];
+    int64_t pos;
+    if (i < am)
+      pos = i + count_below(kin + base + am, iin + base + am, (uint32_t)(be - am), k, id);
+    else
+      pos = ps + (i - am) + count_not_above(kin + base + ps, iin + base + ps, (uint32_t)(am - ps),
+                                            k, id);
+    a.key[to][base + pos] = k;
+    a.id[to][base + pos] = id;
+    if (PAY) a.pay[to][base + pos] = a.pay[from][g];
+  }
+}
+
+// Selection on the sorted candidates (list 0; C = their first nc) and ongoing
+// requests (list 1): the stage filter, the kept members of C before each
+// index (dec), and the counts.
+__global__ __launch_bounds__(BT) void w_select_scan(SelArgs a, WideSort w, int buf,
+                                                    uint32_t* dec) {
+  __shared__ uint32_t scan32[BT / kWave + 1];
+  const uint32_t t = threadIdx.x;
+  if (load_agent(a.flags) != 0) {  // an id outside [0, n_ids)
+    if (t == 0) a.counts[0] = a.counts[1] = 0;
+    return;
+  }
+  const uint64_t* ck = w.key[buf];
+  const uint32_t* ci = w.id[buf];
+  const uint64_t* ok = ck + w.list[1].base;
+  const uint32_t* oi = ci + w.list[1].base;
+  const uint32_t nc = (uint32_t)min(a.b, list_size(w.list[0]));
+  const uint32_t no = (uint32_t)list_size(w.list[1]);
+  if (nc == 0 && no == 0) {
+    if (t == 0) a.counts[0] = a.counts[1] = 0;
+    return;
+  }
+  const bool top_in_c = nc > 0 && (no == 0 || less(ck[0], ci[0], ok[0], oi[0]));
+  const bool keep_all = a.stage[top_in_c ? ci[0] : oi[0]] == 0;
+  const uint32_t per = (nc + BT - 1) / BT;
+  const uint32_t c0 = min(nc, t * per), c1 = min(nc, c0 + per);
+  uint32_t mine = 0;
+  for (uint32_t i = c0; i < c1; ++i) mine += (keep_all || a.stage[ci[i]] != 0) ? 1u : 0u;
+  uint32_t ndec;
+  uint32_t run = block_excl_scan_u32<BT>(mine, scan32, ndec);
+  for (uint32_t i = c0; i < c1; ++i) {
+    dec[i] = run;
+    run += (keep_all || a.stage[ci[i]] != 0) ? 1u : 0u;
+  }
+  if (t == 0) {
+    dec[nc] = ndec;
+    const uint64_t b = (uint64_t)a.b, nm = (uint64_t)ndec + no;
+    a.counts[0] = (int64_t)min(b, nm);
+    a.counts[1] = (int64_t)((nc - ndec) + (nm > b ? nm - b : 0));
+  }
+}
+
+__global__ __launch_bounds__(BT) void w_select_place(SelArgs a, WideSort w, int buf,
+                                                     const uint32_t* dec) {
+  if (load_agent(a.flags) != 0) return;
+  const uint64_t* ck = w.key[buf];
+  const uint32_t* ci = w.id[buf];
+  const uint32_t nc = (uint32_t)min(a.b, list_size(w.list[0]));
+  const uint32_t no = (uint32_t)list_size(w.list[1]);
+  for (uint32_t g = blockIdx.x * BT + threadIdx.x; g < nc + no; g += gridDim.x * BT)
+    select_place(a, ck, ci, nc, ck + w.list[1].base, ci + w.list[1].base, no, dec, g);
+}
+
+// Eviction on the sorted cached requests: KV prefix sums in eviction order
+// (the sorted order read backwards) and the eviction order itself, then the
+// victims of every incoming request.
+__global__ __launch_bounds__(BT) void w_evict(EvictArgs a, WideSort w, int buf, uint64_t* psum,
+                                              uint32_t* eorder) {
+  __shared__ uint64_t scan64[BT / kWave + 1];
+  __shared__ uint32_t last;
+  if (load_agent(a.flags) != 0) return;  // a bad id or KV size
+  const uint32_t t = threadIdx.x;
+  const uint32_t nr = (uint32_t)a.n_cached;
+  const uint32_t* id = w.id[buf];
+  const uint32_t* src = w.pay[buf];
+  const uint32_t per = (nr + BT - 1) / BT;
+  const uint32_t e0 = min(nr, t * per), e1 = min(nr, e0 + per);
+  uint64_t mine = 0;
+  for (uint32_t e = e0; e < e1; ++e) mine += (uint64_t)a.kv[src[nr - 1 - e]];
+  uint64_t total;
+  uint64_t run = block_excl_scan_u64<BT>(mine, scan64, total);
+  for (uint32_t e = e0; e < e1; ++e) {
+    run += (uint64_t)a.kv[src[nr - 1 - e]];
+    psum[e] = run;            // KV evicted by the first e + 1 victims
+    eorder[e] = id[nr - 1 - e];
+  }
+  block_sync();  // (orders this workgroup's global writes before its reads)
+  evict_demands(a, psum, eorder, nr, scan64, &last);
+}
+
+// Chunk sort and merge rounds; returns the buffer that holds the result.
+template <bool PAY>
+int wide_sort(const WideSort& w, hipStream_t st) {
+  int64_t chunks = 0, longest = 0;
+  for (int l = 0; l < w.nlists; ++l) {
+    const int64_t n = w.list[l].n0 + w.list[l].n1;
+    chunks += (n + kWideChunk - 1) / kWideChunk;
+    longest = std::max(longest, n);
+  }
+  if (chunks == 0) return 0;
+  hipLaunchKernelGGL(w_chunk_sort<PAY>, dim3((unsigned)chunks), dim3(BT), 0, st, w);
+  const unsigned grid = (unsigned)std::min<int64_t>((w.total + BT - 1) / BT, 4096);
+  int from = 0;
+  for (int64_t run = kWideChunk; run < longest; run *= 2) {
+    hipLaunchKernelGGL(w_merge<PAY>, dim3(grid), dim3(BT), 0, st, w, run, from);
+    from ^= 1;
+  }
+  return from;
 }
 
 }  // namespace
+
+hipError_t launch_select_wide(const SelArgs& a, WideSort w, uint32_t* dec, hipStream_t st) {
+  const int buf = wide_sort<false>(w, st);
+  hipLaunchKernelGGL(w_select_scan, dim3(1), dim3(BT), 0, st, a, w, buf, dec);
+  const int64_t nc = std::min(a.b, w.list[0].n0 + w.list[0].n1);
+  const int64_t m = nc + w.list[1].n0 + w.list[1].n1;
+  if (m > 0) {
+    const unsigned grid = (unsigned)std::min<int64_t>((m + BT - 1) / BT, 4096);
+    hipLaunchKernelGGL(w_select_place, dim3(grid), dim3(BT), 0, st, a, w, buf, dec);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_evict_wide(const EvictArgs& a, WideSort w, uint64_t* psum, uint32_t* eorder,
+                             hipStream_t st) {
+  const int buf = wide_sort<true>(w, st);
+  hipLaunchKernelGGL(w_evict, dim3(1), dim3(BT), 0, st, a, w, buf, psum, eorder);
+  return hipGetLastError();
+}
 
 hipError_t launch_select(const SelArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(b_select, dim3(1), dim3(BT), 0, st, a);

@@ -288,9 +288,12 @@ hipError_t launch_evict(const CostArgs& a, hipStream_t st);
 hipError_t launch_merge_flags(uint32_t* dst, const uint32_t* src, hipStream_t st);
 
 // ---------------------------------------------------------------------------
-// Batch selection and eviction (batch.hip), one workgroup each.
-constexpr int kSelectCap = 4096;  // largest batch, buffer and ongoing set
-constexpr int kEvictCap = 8192;   // most cached requests
+// Batch selection and eviction (batch.hip): one workgroup over LDS up to
+// these sizes, several kernels over the workspace beyond them.
+constexpr int kSelectCap = 4096;  // largest batch, buffer and ongoing set in LDS
+constexpr int kEvictCap = 8192;   // most cached requests in LDS
+constexpr int kWideChunk = 8192;  // entries sorted by one workgroup beyond those
+constexpr int64_t kWideMax = 1ll << 30;  // entries of all lists of one call
 
 struct SelArgs {
   const uint8_t* priority;  // [n_ids]
@@ -325,7 +328,40 @@ struct EvictArgs {
   uint32_t* flags;
 };
 
+// A list of request ids to sort by key: src0[0 .. n0) then src1[0 .. n1),
+// placed at entries [base, base + n0 + n1) of the sort arrays.
+struct WideList {
+  const int32_t* src0;
+  int64_t n0;
+  const int32_t* src1;
+  int64_t n1;
+  int64_t base;
+};
+
+// The sort of up to two lists beyond one workgroup's LDS: (key, id) entries
+// (and, for eviction, the index into the caller's arrays) in two buffers that
+// the chunk sort and the merge rounds ping-pong between.
+struct WideSort {
+  const uint8_t* priority;
+  const int32_t* length;
+  int64_t n_ids;
+  const int64_t* kv;  // eviction: KV sizes, checked for >= 0; else null
+  WideList list[2];
+  int32_t nlists;
+  int64_t total;      // entries of all lists
+  uint64_t* key[2];
+  uint32_t* id[2];
+  uint32_t* pay[2];   // eviction only
+  uint32_t* flags;
+};
+
 hipError_t launch_select(const SelArgs& a, hipStream_t st);
 hipError_t launch_evict_victims(const EvictArgs& a, hipStream_t st);
+// Beyond the LDS sizes: w holds the lists (candidates, then ongoing; or the
+// cached requests) and the sort buffers; dec [candidates + 1] u32, psum
+// [n_cached] u64 and eorder [n_cached] u32 are workspace arrays.
+hipError_t launch_select_wide(const SelArgs& a, WideSort w, uint32_t* dec, hipStream_t st);
+hipError_t launch_evict_wide(const EvictArgs& a, WideSort w, uint64_t* psum, uint32_t* eorder,
+                             hipStream_t st);
 
 }  // namespace semsched

@@ -178,17 +178,30 @@ def test_select_and_evict_argument_errors(ss):
     S = L.sem_select_batch
     assert S(fake, fake, fake, -1, fake, 5, nul, 0, nul, 0, 2, fake, fake, fake) == ss.SEM_EINVAL
     assert S(fake, fake, fake, 10, fake, 5, nul, 0, nul, 0, -1, fake, fake, fake) == ss.SEM_EINVAL
-    assert S(fake, fake, fake, 10, fake, 5, nul, 0, nul, 0, ss.SELECT_CAP + 1, fake, fake,
+    # beyond the LDS sizes the lists are merged in the workspace, up to WIDE_MAX entries
+    assert S(fake, fake, fake, 10, fake, ss.WIDE_MAX, nul, 0, fake, 1, ss.WIDE_MAX, fake, fake,
              fake) == ss.SEM_ENOTIMPL
-    assert S(fake, fake, fake, 10, fake, 5, fake, ss.SELECT_CAP + 1, nul, 0, 2, fake, fake,
+    assert S(fake, fake, fake, 10, fake, 5, fake, ss.WIDE_MAX, fake, 1, 2, fake, fake,
              fake) == ss.SEM_ENOTIMPL
+    SW = L.sem_select_workspace_bytes
+    assert SW(5, 10, 10, 2) == 256 and SW(-1, 0, 0, 0) == 0
+    big = SW(10000, ss.SELECT_CAP + 1, 100, 20000)
+    assert big >= 256 + 24 * (10000 + ss.SELECT_CAP + 1 + 100)
+    A = L.sem_select_batch_async
+    assert A(fake, fake, fake, 10, fake, 10000, fake, ss.SELECT_CAP + 1, fake, 100, 20000, fake,
+             fake, fake, fake, big - 1, nul) == ss.SEM_EINVAL
     assert S(fake, fake, nul, 10, fake, 5, nul, 0, nul, 0, 2, fake, fake, fake) == ss.SEM_EINVAL
     assert S(fake, fake, fake, 10, nul, 5, nul, 0, nul, 0, 2, fake, fake, fake) == ss.SEM_EINVAL
     assert S(fake, fake, fake, 10, fake, 5, nul, 0, nul, 0, 2, fake, fake, nul) == ss.SEM_EINVAL
     E = L.sem_evict
     assert E(fake, fake, 10, fake, fake, -1, 0, 0, fake, 1, fake, fake) == ss.SEM_EINVAL
-    assert E(fake, fake, 10, fake, fake, ss.EVICT_CAP + 1, 0, 0, fake, 1, fake,
+    assert E(fake, fake, 10, fake, fake, ss.WIDE_MAX + 1, 0, 0, fake, 1, fake,
              fake) == ss.SEM_ENOTIMPL
+    EW = L.sem_evict_workspace_bytes
+    assert EW(ss.EVICT_CAP) == 256 and EW(-1) == 0
+    assert EW(ss.EVICT_CAP + 1) >= 256 + 36 * (ss.EVICT_CAP + 1)
+    assert L.sem_evict_async(fake, fake, 10, fake, fake, ss.EVICT_CAP + 1, 0, 0, fake, 1, fake,
+                             fake, fake, EW(ss.EVICT_CAP + 1) - 1, nul) == ss.SEM_EINVAL
     assert E(fake, fake, 10, fake, nul, 5, 0, 0, fake, 1, fake, fake) == ss.SEM_EINVAL
     assert E(fake, fake, 10, fake, fake, 5, 0, 0, nul, 1, fake, fake) == ss.SEM_EINVAL
     assert L.sem_evict_async(fake, fake, 10, fake, fake, 5, 0, 0, fake, 1, fake, fake, nul, 256,

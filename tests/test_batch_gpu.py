@@ -59,6 +59,42 @@ def test_select_batch(case, decode_frac):
     assert run_select(p, l, stage, heap, buf, ong, b) == want
 
 
+# Beyond one workgroup's LDS (b, buffer or ongoing above 4096): the lists are
+# sorted in 8192-entry chunks and merged in the workspace.
+@pytest.mark.parametrize("case", [
+    (1 << 20, 40000, 10000, 5000, 16384), (200000, 16384, 0, 16384, 16384),
+    (100000, 5000, 5000, 0, 4097), (100000, 0, 4097, 0, 100), (100000, 100, 0, 4097, 50),
+    (300000, 70000, 20000, 30000, 60000), (50000, 20000, 0, 0, 8193)])
+@pytest.mark.parametrize("decode_frac", [0.0, 0.5, 1.0])
+def test_select_batch_beyond_lds(case, decode_frac):
+    n_ids, nh, nu, no, b = case
+    print(f"[gpu] select (merged in the workspace) n_ids={n_ids} heap={nh} buffer={nu} "
+          f"ongoing={no} b={b}", flush=True)
+    p, l, stage, heap, buf, ong = instance(sum(case) + int(10 * decode_frac), n_ids, nh, nu, no,
+                                           decode_frac=decode_frac)
+    want = select_batch(p.tolist(), l.tolist(), stage.tolist(), heap.tolist(), buf.tolist(),
+                        ong.tolist(), b)
+    assert run_select(p, l, stage, heap, buf, ong, b) == want
+
+
+def test_select_batch_beyond_lds_ties():
+    # few distinct keys across 40000 candidates: the merge rounds must keep
+    # equal (rank, length) pairs in id order across chunks
+    n = 200000
+    rng = np.random.default_rng(8)
+    p = rng.integers(0, 2, n).astype(np.uint8)
+    l = rng.integers(0, 3, n).astype(np.int32)
+    stage = (rng.random(n) < 0.5).astype(np.uint8)
+    ids = rng.permutation(n)
+    w = ids[:30000]
+    heap = w[np.lexsort((w, l[w], p[w]))]
+    buf, ong = ids[30000:40000], ids[40000:50000]
+    print("[gpu] select (merged in the workspace), ties", flush=True)
+    want = select_batch(p.tolist(), l.tolist(), stage.tolist(), heap.tolist(), buf.tolist(),
+                        ong.tolist(), 12000)
+    assert run_select(p, l, stage, heap, buf, ong, 12000) == want
+
+
 def test_select_batch_ties_and_inversion():
     # many equal keys (ties go to the lower id) and an urgent decoding request
     n = 20000
@@ -96,6 +132,55 @@ def test_evict(n_cached, n_dem):
                         dev(kv, np.int64), usage, capacity, dev(demands, np.int64))
         assert v.cpu().numpy().tolist() == want_v
         assert u.cpu().numpy().tolist() == want_u
+
+
+@pytest.mark.parametrize("n_cached,n_dem", [(8193, 10), (65536, 16384), (100000, 0),
+                                            (65536, 1), (20000, 70000)])
+def test_evict_beyond_lds(n_cached, n_dem):
+    import paper_2506_12204_amd as ss
+    rng = np.random.default_rng(n_cached + 7 * n_dem)
+    n_ids = 1 << 20
+    p = rng.integers(0, 5, n_ids).astype(np.uint8)
+    l = rng.integers(0, 100, n_ids).astype(np.int32)  # small range: many ties
+    cached = rng.permutation(n_ids)[:n_cached].astype(np.int32)
+    kv = rng.integers(0, 1 << 30, n_cached).astype(np.int64)
+    kv[: n_cached // 10] = 0
+    demands = rng.integers(0, 1 << 20, n_dem).astype(np.int64)
+    usage = int(kv.sum()) + 12345
+    for capacity in (usage + int(demands.sum()) + 1, usage // 2, 0):
+        print(f"[gpu] evict (merged in the workspace) cached={n_cached} demands={n_dem} "
+              f"capacity={capacity}", flush=True)
+        want_v, want_u = evict(p.tolist(), l.tolist(), cached.tolist(), kv.tolist(), usage,
+                               capacity, demands.tolist())
+        v, u = ss.evict(dev(p, np.uint8), dev(l, np.int32), dev(cached, np.int32),
+                        dev(kv, np.int64), usage, capacity, dev(demands, np.int64))
+        assert v.cpu().numpy().tolist() == want_v
+        assert u.cpu().numpy().tolist() == want_u
+
+
+def test_errors_beyond_lds():
+    import paper_2506_12204_amd as ss
+    n = 50000
+    p = dev(np.zeros(n, np.uint8), np.uint8)
+    l = dev(np.arange(n, dtype=np.int32), np.int32)
+    st = dev(np.ones(n, np.uint8), np.uint8)
+    buf = np.arange(5000, dtype=np.int32)
+    buf[4321] = n + 3  # an id outside [0, n_ids)
+    with pytest.raises(ss.SemschedError):
+        ss.select_batch(p, l, st, None, dev(buf, np.int32), None, 4500)
+    cached = np.arange(9000, dtype=np.int32)
+    kv = np.ones(9000, np.int64)
+    kv[8999] = -1
+    with pytest.raises(ss.SemschedRangeError):
+        ss.evict(p, l, dev(cached, np.int32), dev(kv, np.int64), 5, 1, dev(np.array([1]), np.int64))
+    # later good calls are not affected
+    buf[4321] = 4321
+    bt, pu = ss.select_batch(p, l, st, None, dev(buf, np.int32), None, 4500)
+    assert bt.cpu().tolist() == list(range(4500)) and pu.cpu().tolist() == []
+    kv[8999] = 1
+    v, u = ss.evict(p, l, dev(cached, np.int32), dev(kv, np.int64), 9000, 9000,
+                    dev(np.array([2]), np.int64))
+    assert u.cpu().tolist() == [2] and v.cpu().tolist() == [8999, 8998]
 
 
 def test_errors():
