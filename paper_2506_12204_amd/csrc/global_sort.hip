@@ -621,6 +621,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, uin
                                            0x00020000 /* 32-bit data format, gfx9 */);
 }
 
+// Cache policy of loads that stream through data read once: the non-temporal
+// bit, so that these lines are the first the L2 evicts and the partly written
+// output lines of the scatter stay until their runs complete.
+constexpr int kLoadStream = 2;
+
 // Inputs of one big tile of `cnt` items starting at item tb, round-major per
 // wave (round r of wave w holds items w*64*R1 + r*64 + lane). Items past the
 // tile's end read as zero.
@@ -636,8 +641,8 @@ __device__ __forceinline__ void load_first(const GArgs& a, const uint8_t* pri, i
   for (int r = 0; r < R1; ++r) {
     // the whole offset goes in the vector operand: only that part (with the
     // immediate) is range-checked, the scalar offset is not
-    pv[r] = __builtin_amdgcn_raw_buffer_load_b8(rp, lane + r * kWave, 0, 0);
-    lv[r] = __builtin_amdgcn_raw_buffer_load_b32(rl, (lane + r * kWave) * 4, 0, 0);
+    pv[r] = __builtin_amdgcn_raw_buffer_load_b8(rp, lane + r * kWave, 0, kLoadStream);
+    lv[r] = __builtin_amdgcn_raw_buffer_load_b32(rl, (lane + r * kWave) * 4, 0, kLoadStream);
   }
 }
 
