@@ -50,6 +50,13 @@ constexpr int T = kGlobalTile;
 constexpr int BPT = kMaxBins / NT;  // bins per thread, blocked: t*BPT .. t*BPT+BPT-1
 static_assert(BPT * NT == kMaxBins, "every bin has a thread");
 static_assert(NW * kMaxBins * 2 <= T * 8, "wave counters must fit in the stage");
+// Compact final pass: sub-bucket starts of at most this many (bucket, id
+// chunk) pairs per block are searched in LDS; blocks spanning more take the
+// global-window kernel.
+constexpr int kWinCap = 512;
+// Requests below this count store through buffer resources (byte offsets of
+// the waits stay below 2^31); larger queues take the global-window kernel.
+constexpr int64_t kBufferStoreItems = 1ll << 28;
 
 // ------------------------------------------------------------------------
 // Run by one workgroup of the first histogram pass: no other workgroup of
@@ -374,6 +381,54 @@ __device__ void column_scan(const GArgs& a, int s, int b, bool weights, int G,
 // final != 0: scan the final pass (its index and bin count come from the Plan).
 // Pass 0 (final == 0): workgroups 0 .. 2^d0-1 scan the first digit's bins
 // and workgroup 2^d0 writes the Plan. Final pass: one workgroup per bin.
+// Whether any block of the compact final pass needs the global-window
+// kernel: its positions span more (first-digit bucket, id chunk) pairs than
+// the LDS window holds, or the queue is too long for buffer-resource stores.
+// One workgroup; the bucket starts are the exclusive scan of the first
+// digit's counts. The kernels that return at once for the other kind of
+// block then return before their set-up.
+__device__ void window_check(const GArgs& a, Plan* pl, uint32_t* scan32) {
+  __shared__ uint32_t bstart[kMaxBins + 1];
+  __shared__ uint32_t any;
+  constexpr int PER = kMaxBins / SCT;
+  const int nd = 1 << a.d0;
+  uint32_t c[PER];
+  uint32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int d = threadIdx.x * PER + i;
+    c[i] = d < nd ? a.hist_cnt[d] : 0u;
+    sum += c[i];
+  }
+  if (threadIdx.x == 0) any = a.n >= kBufferStoreItems ? 1u : 0u;
+  uint32_t tot;
+  uint32_t ex = block_excl_scan_u32<SCT>(sum, scan32, tot);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int d = threadIdx.x * PER + i;
+    if (d <= nd) bstart[d] = ex;
+    ex += c[i];
+  }
+  block_sync();
+  auto bucket = [&](uint32_t pos) {  // last d < nd with bstart[d] <= pos
+    int lo = 0, hi = nd - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (bstart[mid] <= pos) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+  };
+  for (int g = threadIdx.x; g < a.fin.blocks; g += SCT) {
+    const int64_t lo = (int64_t)g * a.fin.tpb * T;
+    const int64_t hi = min(a.n, lo + (int64_t)a.fin.tpb * T);
+    if (hi <= lo) continue;
+    const int wn = (bucket((uint32_t)(hi - 1)) - bucket((uint32_t)lo) + 1) << a.kpb;
+    if (wn > kWinCap) any = 1u;
+  }
+  block_sync();
+  if (threadIdx.x == 0) pl->cglb = any;
+}
+
 __global__ __launch_bounds__(SCT) void g_scan(GArgs a, int final) {
   __shared__ uint32_t scan32[SCT / kWave + 1];
   __shared__ uint64_t scan64[SCT / kWave + 1];
@@ -387,8 +442,12 @@ __global__ __launch_bounds__(SCT) void g_scan(GArgs a, int final) {
                      a.chunked != 0);
     return;
   }
-  const Plan* pl = a.plan;
+  Plan* pl = a.plan;
   if (!pl->ok) return;
+  if (b == kMaxBins) {
+    if (pl->compact) window_check(a, pl, scan32);
+    return;
+  }
   const int s = (int)pl->nscatter - 1;
   if (b >= (int)pl->nbins[s]) return;
   column_scan<SCT>(a, s, b, true, a.fin.blocks * kHistRows, scan32, scan64);
@@ -719,7 +778,15 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
   // either way its low D0 bits are the digit
   // the ranking's lane masks live in this wave's slice of the stage, which
   // only this wave reads after staging and is done with when it ranks
-  u64_alias* masks = reinterpret_cast<u64_alias*>(sh.stage + wb);
+  // S32 (compact, no carried ranks): the staged item is one u32, u2 << 24 |
+  // first digit << 14 | index in the tile (u2 < 256, D0 <= 10, tiles of 2^14),
+  // in the first half of the stage; the wave's mask table is then its share of
+  // that half.
+  constexpr bool S32 = COMPACT && !PAY;
+  static_assert(!S32 || (D0 <= 10 && T1 <= (1 << 14)), "staged item fits 32 bits");
+  u32_alias* stage32 = reinterpret_cast<u32_alias*>(sh.stage);
+  u64_alias* masks = S32 ? reinterpret_cast<u64_alias*>(stage32 + wb)
+                         : reinterpret_cast<u64_alias*>(sh.stage + wb);
   auto rank_tile = [&](int cv) {
     clear_wave_masks<NBIN>(masks);
 #pragma unroll
@@ -735,7 +802,12 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
         if (wb + r * kWave + lane >= cv) key[r] |= M0;
     }
 #pragma unroll
-    for (int r = 0; r < R1; ++r) rk[r] = rank_round_mask(key[r] & M0, masks, mycnt);
+    for (int r = 0; r < R1; ++r) {
+#if defined(SEMSCHED_FIRST_HYBRID)
+      if (r % SEMSCHED_FIRST_HYBRID == 0) { rk[r] = rank_round_c<D0>(key[r] & M0, mycnt); continue; }
+#endif
+      rk[r] = rank_round_mask(key[r] & M0, masks, mycnt);
+    }
   };
 
   load_first(a, pri, lo, tile_items(lo), pv, lv);
@@ -784,9 +856,16 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
 #pragma unroll
     for (int r = 0; r < R1; ++r) rk[r] += mycnt[opaque(key[r]) & M0];
     clear_wave_counters<NBIN>(mycnt);  // only this wave reads them until the next ranking
+    if constexpr (S32) {
 #pragma unroll
-    for (int r = 0; r < R1; ++r)
-      sh.stage[rk[r]] = ((uint64_t)key[r] << 32) | (uint32_t)(tb + wb + r * kWave + lane);
+      for (int r = 0; r < R1; ++r)
+        stage32[rk[r]] = ((key[r] >> D0) << 24) | ((key[r] & M0) << 14) |
+                         (uint32_t)(wb + r * kWave + lane);
+    } else {
+#pragma unroll
+      for (int r = 0; r < R1; ++r)
+        sh.stage[rk[r]] = ((uint64_t)key[r] << 32) | (uint32_t)(tb + wb + r * kWave + lane);
+    }
     block_sync();  // the tile is staged in digit order
 
     // stores are unconditional: lanes without an item write to the sink
@@ -794,6 +873,16 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
 #pragma unroll
     for (int r = 0; r < R1; ++r) {
       const int j = wb + r * kWave + lane;
+      if constexpr (S32) {
+        const uint32_t e = stage32[j];
+        const uint32_t pos = sh.base[(e >> 14) & M0] + (uint32_t)j;
+        const bool item = (full || j < cv) && pos < (uint64_t)a.n;
+        uint32_t* po = item ? out32 + pos : reinterpret_cast<uint32_t*>(a.sink);
+        *po = ((e >> 24) << kChunkBits) |
+              ((uint32_t)(tb + (e & 0x3fffu)) & ((1u << kChunkBits) - 1));
+        if (r % 8 == 7) __builtin_amdgcn_sched_barrier(0);
+        continue;
+      }
       const uint64_t e = sh.stage[j];
       const uint32_t pos = sh.base[(uint32_t)(e >> 32) & M0] + (uint32_t)j;
       const bool item = (full || j < cv) && pos < (uint64_t)a.n;  // (pos < n for consistent counts)
@@ -2266,13 +2355,12 @@ __device__ void final_big(const GArgs& a, int g, FinalBigShared& sh) {
 // bits; the staged value carries (u2, d) and the id, the rest is the
 // big-tile final pass.
 
-constexpr int kWinCap = 512;
-
 struct FinalCompactShared {
   uint64_t stage[TB];
   uint16_t cnt[NWB][MAXB];     // wave counters, then the waves' tile offsets
   uint32_t base_c[MAXB];       // output position of the tile's first item of a digit
   uint64_t base_w[MAXB];       // wait base of a digit in this tile
+  uint64_t flen[MAXB];         // one-bucket tiles: base_c | the digit's length << 32
   uint64_t wsum[MAXB];         // length sums of the tile's digits
   uint64_t clo[256], chi[256]; // class totals, low and high words
   uint32_t bstart[kMaxBins + 1];
@@ -2283,10 +2371,6 @@ struct FinalCompactShared {
   uint64_t part_w[NWB + 1];
   uint64_t chunk[NWB];
 };
-
-// Requests below this count store through buffer resources (byte offsets of
-// the waits stay below 2^31); larger queues take the global-window kernel.
-constexpr int64_t kBufferStoreItems = 1ll << 28;
 
 __device__ __forceinline__ void load_final_compact(const uint32_t* keys, int64_t tb, int cnt,
                                                    uint32_t (&e)[KB]) {
@@ -2413,6 +2497,14 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   // here: its requests of digit u2 contribute count * (lbase[u2] + d), which
   // the digit's owner forms from the wave's counter. The other waves add each
   // length to the digit's LDS sum.
+  // Full tiles whose positions all lie in one first-digit bucket d (nearly
+  // all: a bucket spans about n / 2^d0 positions) hold one length per final
+  // digit u2, lbase[u2] + d. The k-th request of u2 in such a tile then waits
+  // (wait of u2's first request in the tile) + k * length, so no length scan
+  // is needed, and the owner of u2 adds the digit's share of its class total
+  // in closed form: count * first wait + length * count * (count - 1) / 2.
+  bool tile_one = false;
+  U128 own_tot = {0, 0};  // owners: closed-form class-total shares of their digit
   auto phase1 = [&](int64_t tb) {
     const int cv = tile_items(tb);
     // the sub-buckets this tile's positions lie in, then those of this wave's
@@ -2420,6 +2512,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     // uniform, so the searches below have uniform trip counts
     const int ja = __builtin_amdgcn_readfirstlane(find((uint32_t)tb, 0, wn - 1));
     const int jb = __builtin_amdgcn_readfirstlane(find((uint32_t)(tb + cv - 1), ja, wn - 1));
+    tile_one = !PAY && cv == TB && ((win0 + ja) >> kpb) == ((win0 + jb) >> kpb);
     const uint32_t wlast = (uint32_t)(tb + cv - 1);
     const int wja = __builtin_amdgcn_readfirstlane(
         find(min((uint32_t)(tb + wb), wlast), ja, jb));
@@ -2483,6 +2576,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
       ex_c += sh.part_c[v];
       ex_w += sh.part_w[v];
     }
+    const bool one = tile_one;  // (uniform)
     if (owner) {
       uint32_t run = ex_c;
 #pragma unroll
@@ -2492,7 +2586,16 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
         run += c;
       }
       sh.base_c[t] = carry_c - ex_c;
-      sh.base_w[t] = carry_w - ex_w;
+      if (one) {
+        const uint32_t len = sh.lbase[t] + (uint32_t)sh.wd[0];
+        sh.flen[t] = ((uint64_t)len << 32) | (carry_c - ex_c);
+        sh.base_w[t] = carry_w - (uint64_t)ex_c * len;
+        // the digit's waits in this tile: carry_w + k * len for k < tot
+        add128(own_tot, U128{(uint64_t)tot * carry_w, __umul64hi((uint64_t)tot, carry_w)});
+        add128(own_tot, (uint64_t)len * ((uint64_t)tot * (tot - 1) / 2));
+      } else {
+        sh.base_w[t] = carry_w - ex_w;
+      }
       carry_c += tot;
       carry_w += ws;
     }
@@ -2516,6 +2619,31 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     if (more) load_final_compact(keys_in, tb + TB, tile_items(tb + TB), e);
     block_sync();  // the tile is staged
 
+    if (one) {
+      // ---- phase 2, one-bucket tile: waits in closed form ------------------
+#pragma unroll
+      for (int r = 0; r < KB; ++r) {
+        const int j = wb + r * kWave + lane;
+        const uint64_t x = sh.stage[j];
+        const uint64_t f = sh.flen[(uint32_t)(x >> 42)];
+        const uint64_t wt = sh.base_w[(uint32_t)(x >> 42)] + (uint64_t)(uint32_t)j * (f >> 32);
+        const uint32_t pos = (uint32_t)f + (uint32_t)j;
+        const bool item = pos < (uint64_t)a.n;  // (pos < n for consistent counts)
+        if constexpr (WIN_LDS) {
+          const uint32_t slot = item ? pos : (uint32_t)a.n;
+          __builtin_amdgcn_raw_buffer_store_b32((uint32_t)x, rs_order, slot * 4u, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2{(uint32_t)wt, (uint32_t)(wt >> 32)},
+                                                rs_wait, slot * 8u, 0, 0);
+        } else {
+          int32_t* po = item ? a.order + pos : reinterpret_cast<int32_t*>(a.sink);
+          int64_t* pw = item ? a.wait + pos : reinterpret_cast<int64_t*>(a.sink + 1);
+          *po = (int32_t)(uint32_t)x;
+          *pw = (int64_t)wt;
+        }
+      }
+      if (more) phase1(tb + TB);
+      continue;
+    }
     // ---- phase 2: tile length prefix, order, waits, class totals -----------
     uint32_t exc[KB], rt[KB];  // exclusive length prefix within the round; round total
     uint64_t chunk = 0;
@@ -2581,6 +2709,10 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     cur_end = 0;
     if (more) phase1(tb + TB);
   }
+  if (owner && (own_tot.lo | own_tot.hi)) {
+    const uint32_t c = class_of((uint32_t)t, magic);
+    atomic_add128(sh.clo + c, sh.chi + c, own_tot);
+  }
   block_sync();  // every lane's total is in
   // (carried ranks are the caller's ranks themselves)
   const int P = PAY ? (int)*a.pay_pmax + 1 : (int)pl->P;
@@ -2630,7 +2762,7 @@ __global__ __launch_bounds__(NTB) void g_final_cglb(GArgs a) {
     final_big<true>(a, blockIdx.x, sh.big);
     return;
   }
-  if (!pl->compact || pl->pay) return;
+  if (!pl->compact || pl->pay || !pl->cglb) return;
   final_compact<false, false>(a, blockIdx.x, sh.compact);
 }
 
@@ -2647,7 +2779,7 @@ __global__ __launch_bounds__(NTB) void g_final_pay(GArgs a) {
 __global__ __launch_bounds__(NTB) void g_final_pay_cglb(GArgs a) {
   __shared__ FinalCompactShared sh;
   const Plan* pl = a.plan;
-  if (!pl->ok || !pl->compact || !pl->pay) return;
+  if (!pl->ok || !pl->compact || !pl->pay || !pl->cglb) return;
   final_compact<false, true>(a, blockIdx.x, sh);
 }
 
@@ -2752,7 +2884,7 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   mark(ev, 6, true, st);
   const dim3 gf(a.fin.blocks);
   hipLaunchKernelGGL(g_histF, dim3(a.fin.blocks * kHistRows), dim3(HT), 0, st, a);
-  hipLaunchKernelGGL(g_scan, dim3(kMaxBins), dim3(SCT), 0, st, a, 1);
+  hipLaunchKernelGGL(g_scan, dim3(kMaxBins + 1), dim3(SCT), 0, st, a, 1);
   mark(ev, 2, false, st);
   // exactly one of the two does the work; the plan on the device decides
   hipLaunchKernelGGL(g_final_big, gf, dim3(NTB), 0, st, a);

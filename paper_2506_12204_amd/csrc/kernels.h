@@ -124,6 +124,9 @@ struct Plan {
   uint32_t pay;       // 1: compact elements also carry the caller's rank above the
                       // final digit (the rank takes no part in the order)
   uint32_t pay_shift; // bit of a compact element where that rank starts
+  uint32_t cglb;      // compact: 1 if some block of the final pass needs the
+                      // global-window kernel (sub-bucket starts beyond the LDS
+                      // window, or a queue too long for buffer-resource stores)
   uint32_t shift[kMaxScatter];  // digit = (u2 >> shift) & (bins - 1), passes >= 1
   uint32_t nbits[kMaxScatter];
   uint32_t nbins[kMaxScatter];
