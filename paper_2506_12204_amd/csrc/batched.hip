@@ -243,11 +243,11 @@ __device__ __forceinline__ void digit_positions(uint16_t (*cnt)[NB], uint32_t* s
   group_sync<NW>();
 }
 
-// Lanes of the wave whose digit agrees with this lane's on the low nbits bits
-// (nbits uniform). Per bit: the lane's bit as a 0/-1 mask, its ballot, and
-// one three-input bit operation per half that ORs the lanes whose bit differs
-// into the mismatch set.
-__device__ __forceinline__ uint64_t match_bits(uint32_t d, uint32_t nbits) {
+// Lanes of the wave whose digit differs from this lane's in at least one of
+// the low nbits bits (nbits uniform). Per bit: the lane's bit as a 0/-1 mask,
+// its ballot, and one three-input bit operation per half that ORs the lanes
+// whose bit differs into the set.
+__device__ __forceinline__ uint64_t mismatch_bits(uint32_t d, uint32_t nbits) {
   uint32_t lo = 0, hi = 0;
   for (uint32_t b = 0; b < nbits; ++b) {
     uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)d, b, 1);
@@ -256,19 +256,20 @@ __device__ __forceinline__ uint64_t match_bits(uint32_t d, uint32_t nbits) {
     lo = __builtin_amdgcn_bitop3_b32(lo, (uint32_t)bal, m, 0xF6);  // lo | (bal ^ m)
     hi = __builtin_amdgcn_bitop3_b32(hi, (uint32_t)(bal >> 32), m, 0xF6);
   }
-  return ~(((uint64_t)hi << 32) | lo);
+  return ((uint64_t)hi << 32) | lo;
 }
 
 // Stable rank of one round of 64 digits of nbits bits against this wave's
 // running counters: the number of earlier elements of the wave (earlier
 // rounds, then lower lanes of this round) with the same digit. Every peer
-// writes the same new count.
+// writes the same new count. (Peers below = lanes below - mismatching lanes
+// below; peers = 64 - mismatching lanes.)
 __device__ __forceinline__ uint32_t rank_round_n(uint32_t d, uint32_t nbits, uint16_t* cnt) {
-  const uint64_t peers = match_bits(d, nbits);
-  const uint32_t below = __builtin_amdgcn_mbcnt_hi(
-      (uint32_t)(peers >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
+  const uint64_t other = mismatch_bits(d, nbits);
+  const uint32_t below = (uint32_t)lane_id() - __builtin_amdgcn_mbcnt_hi(
+      (uint32_t)(other >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)other, 0u));
   const uint32_t base = cnt[d];
-  cnt[d] = (uint16_t)(base + (uint32_t)__popcll(peers));
+  cnt[d] = (uint16_t)(base + (uint32_t)kWave - (uint32_t)__popcll(other));
   uint32_t rank = base + below;
   asm volatile("" : "+v"(rank));
   return rank;

@@ -69,13 +69,14 @@ __device__ __forceinline__ uint32_t rank_round(uint32_t d, int nbits,
   return base + below;
 }
 
-// match_digit for a digit width known at compile time. Per bit: the lane's
-// bit as a 0/-1 mask, its ballot, and one three-input bit operation per half
-// that ORs (ballot XOR mask) -- the lanes whose bit differs -- into the
-// accumulated mismatch set. Four VALU operations per bit. The empty asm keeps
-// the compiler from recomputing the ballot's predicate by other means.
+// The lanes of the wave whose digit differs from this lane's in at least one
+// of the low NB bits (NB known at compile time). Per bit: the lane's bit as a
+// 0/-1 mask, its ballot, and one three-input bit operation per half that ORs
+// (ballot XOR mask) -- the lanes whose bit differs -- into the set. Four VALU
+// operations per bit. The empty asm keeps the compiler from recomputing the
+// ballot's predicate by other means.
 template <int NB>
-__device__ __forceinline__ uint64_t match_digit_c(uint32_t d) {
+__device__ __forceinline__ uint64_t mismatch_digit_c(uint32_t d) {
   uint32_t lo = 0, hi = 0;
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -86,18 +87,28 @@ __device__ __forceinline__ uint64_t match_digit_c(uint32_t d) {
     lo = __builtin_amdgcn_bitop3_b32(lo, (uint32_t)bal, m, 0xF6);
     hi = __builtin_amdgcn_bitop3_b32(hi, (uint32_t)(bal >> 32), m, 0xF6);
   }
-  return ~(((uint64_t)hi << 32) | lo);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// The lanes with the same digit as this lane (match_digit for a compile-time
+// width).
+template <int NB>
+__device__ __forceinline__ uint64_t match_digit_c(uint32_t d) {
+  return ~mismatch_digit_c<NB>(d);
 }
 
 // rank_round for a compile-time digit width. Every peer writes the same new
-// count, so no lane has to be singled out for the update.
+// count, so no lane has to be singled out for the update. The peers and the
+// other lanes split the wave, so the peers below this lane are the lanes
+// below it minus the mismatching ones below it, and the peers number 64 minus
+// the mismatching lanes.
 template <int NB>
 __device__ __forceinline__ uint32_t rank_round_c(uint32_t d, uint16_t* cnt) {
-  const uint64_t peers = match_digit_c<NB>(d);
-  const uint32_t below = __builtin_amdgcn_mbcnt_hi(
-      (uint32_t)(peers >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
+  const uint64_t other = mismatch_digit_c<NB>(d);
+  const uint32_t below = (uint32_t)lane_id() - __builtin_amdgcn_mbcnt_hi(
+      (uint32_t)(other >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)other, 0u));
   const uint32_t base = cnt[d];
-  cnt[d] = (uint16_t)(base + (uint32_t)__popcll(peers));
+  cnt[d] = (uint16_t)(base + (uint32_t)kWave - (uint32_t)__popcll(other));
   uint32_t rank = base + below;
   // settle the rank now: left to itself the compiler keeps the count, the
   // peer mask and the address of every round alive until their last use

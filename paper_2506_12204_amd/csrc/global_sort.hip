@@ -2473,13 +2473,16 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     return jl;
   };
 
-  // The loop is rotated: the first phase of tile t + 1 runs at the end of
-  // iteration t, after the prefetch of its elements and the stores of tile
-  // t. The compiler then sees, in straight-line order, the loads, the (exactly
-  // counted, unconditional) stores and the first use of the loads, and waits
-  // only for the loads: the stores drain while the next tile is ranked.
+  // The elements of tile t + 1 are loaded before the stores of tile t, and
+  // ranked (at the top of the next iteration) after them. The compiler then
+  // sees the loads, the (exactly counted, unconditional) stores and the first
+  // use of the loads in that order, and waits only for the loads: the stores
+  // drain while the next tile is ranked.
   uint32_t e[KB];   // elements of the tile being ranked
-  uint32_t rw[KB];  // per item: rank (below 2^14) | window index << 14 (below 2^18)
+  // per item: rank (below 2^14) | window index << 14 (below 2^18; with the
+  // LDS window below 2^9, and then the final digit follows at bit 23)
+  uint32_t rw[KB];
+  static_assert(kWinCap <= 512, "window index, rank and digit share 32 bits");
   // output resources (used when n < kBufferStoreItems: byte offsets below 2^31)
   const __amdgpu_buffer_rsrc_t rs_order = raw_rsrc(a.order, (uint32_t)a.n * 4u);
   const __amdgpu_buffer_rsrc_t rs_wait = raw_rsrc(a.wait, (uint32_t)a.n * 8u);
@@ -2532,7 +2535,7 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
           const uint32_t ls = j >= cv ? 0u : sh.lbase[dg] + d;
           atomicAdd((unsigned long long*)&sh.wsum[dg], (unsigned long long)ls);
         }
-        rw[r] = rank_round_c<8>(dg, mycnt) | (jj << 14);
+        rw[r] = rank_round_c<8>(dg, mycnt) | (jj << 14) | (WIN_LDS ? dg << 23 : 0u);
       }
     };
     if (one_digit)
@@ -2542,8 +2545,8 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
   };
 
   load_final_compact(keys_in, lo, tile_items(lo), e);
-  phase1(lo);
   for (int64_t tb = lo; tb < hi; tb += TB) {
+    phase1(tb);
     const int cv = tile_items(tb);
     const bool full = cv == TB;
     block_sync();  // counters and length sums are complete; phase 2 of the last tile is over
@@ -2604,16 +2607,18 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     // ---- stage (digit, first digit, id) in digit order; load the next tile ---
     uint32_t rk[KB];
 #pragma unroll
-    for (int r = 0; r < KB; ++r) rk[r] = (rw[r] & 0x3fffu) + mycnt[opaque(digit_of(r, cv))];
+    for (int r = 0; r < KB; ++r)
+      rk[r] = (rw[r] & 0x3fffu) + mycnt[opaque(WIN_LDS ? rw[r] >> 23 : digit_of(r, cv))];
     clear_wave_counters<MAXB>(mycnt);
 #pragma unroll
     for (int r = 0; r < KB; ++r) {
-      const int idx = win0 + (int)(rw[r] >> 14);
+      const int idx = win0 + (int)((rw[r] >> 14) & (WIN_LDS ? 511u : 0x3ffffu));
       const uint32_t d = (uint32_t)(idx >> kpb);
       const uint32_t id = ((uint32_t)(idx & ((1 << kpb) - 1)) << kChunkBits) |
                           (e[r] & ((1u << kChunkBits) - 1));
       const uint32_t rank_bits = PAY ? (e[r] >> pay_shift) << 18 : 0u;
-      sh.stage[rk[r]] = ((uint64_t)(rank_bits | (digit_of(r, cv) << 10) | d) << 32) | id;
+      const uint32_t dg = WIN_LDS ? rw[r] >> 23 : digit_of(r, cv);
+      sh.stage[rk[r]] = ((uint64_t)(rank_bits | (dg << 10) | d) << 32) | id;
     }
     const bool more = tb + TB < hi;
     if (more) load_final_compact(keys_in, tb + TB, tile_items(tb + TB), e);
@@ -2641,7 +2646,6 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
           *pw = (int64_t)wt;
         }
       }
-      if (more) phase1(tb + TB);
       continue;
     }
     // ---- phase 2: tile length prefix, order, waits, class totals -----------
@@ -2707,7 +2711,6 @@ __device__ void final_compact(const GArgs& a, int g, FinalCompactShared& sh) {
     if (cur != ~0u) flush_class();  // the next tile starts again at the first class
     cur = ~0u;
     cur_end = 0;
-    if (more) phase1(tb + TB);
   }
   if (owner && (own_tot.lo | own_tot.hi)) {
     const uint32_t c = class_of((uint32_t)t, magic);
