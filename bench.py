@@ -45,10 +45,14 @@ else:
         "final": 16,  # read the element (4 B), write order (4 B) + wait (8 B)
     }
 PATH_BYTES = 17  # the whole schedule's own inputs + outputs per request
-COUNTERS = os.path.join(ROOT, "profiles", "final_pass_c3_counters.md")
-FINAL_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "global_sort.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "c3_step_counters.md")
+CSRC = os.path.join(ROOT, "paper_2506_12204_amd", "csrc")
+# the headers every kernel is built with: a counter measurement belongs to a
+# kernel source together with these
+COMMON = tuple(os.path.join(CSRC, h) for h in ("device_common.h", "block_common.h", "kernels.h"))
+FINAL_SOURCE = (os.path.join(CSRC, "global_sort.hip"),) + COMMON
 MERGE_COUNTERS = os.path.join(ROOT, "profiles", "insert_merge_c3_counters.md")
-MERGE_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "insert.hip")
+MERGE_SOURCE = (os.path.join(CSRC, "insert.hip"),) + COMMON
 WORKLOAD_TEXT = {
     "c3": "single queue n=2^26, 5 urgency classes uniform, lengths uniform int32 in [1,32768], "
           "seed 2",
@@ -58,7 +62,7 @@ WORKLOAD_TEXT = {
           "with 30 % copied from the left neighbour, seed 4",
 }
 POLICY_COUNTERS = os.path.join(ROOT, "profiles", "policy_c3_counters.md")
-POLICY_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "policy.hip")
+POLICY_SOURCE = (os.path.join(CSRC, "policy.hip"),) + COMMON
 # The pass each policy's roofline is taken on: its name, the algorithmic
 # bytes per request (FCFS and HPJF: rank and length read, order and wait
 # written; SJF's final sort pass: its compact element read, order and wait
@@ -99,15 +103,20 @@ class HipEvents:
         self.rt.hipEventDestroy(ctypes.c_void_p(ev))
 
 
-def code_sha(path: str) -> str:
-    """SHA-256 of a C++ source with its // comments and blank lines removed:
-    what identifies the kernel a counter measurement belongs to."""
+def code_sha(paths) -> str:
+    """SHA-256 of C++ sources (a path or a sequence of paths, in order) with
+    their // comments and blank lines removed: what identifies the kernel a
+    counter measurement belongs to."""
+    if isinstance(paths, str):
+        paths = (paths,)
     lines = []
-    with open(path) as f:
-        for line in f:
-            code = line.split("//", 1)[0].rstrip()
-            if code:
-                lines.append(code)
+    for path in paths:
+        lines.append("// " + os.path.basename(path))
+        with open(path) as f:
+            for line in f:
+                code = line.split("//", 1)[0].rstrip()
+                if code:
+                    lines.append(code)
     return hashlib.sha256("\n".join(lines).encode()).hexdigest()
 
 
@@ -534,7 +543,7 @@ def bench_cost(args) -> int:
     return 0
 
 
-BATCHED_SOURCE = os.path.join(ROOT, "paper_2506_12204_amd", "csrc", "batched.hip")
+BATCHED_SOURCE = (os.path.join(CSRC, "batched.hip"),) + COMMON
 
 
 def bench_batched(args) -> int:
@@ -808,7 +817,11 @@ def main() -> int:
     return bench_queue(args)
 
 
-STEP_COUNTERS = os.path.join(ROOT, "profiles", "c3_step_counters.md")
+STEP_COUNTERS = COUNTERS
+# Peak rate of 32-bit integer VALU work on MI355X: 256 CUs x 4 SIMDs x 16
+# lanes per clock (a wave64 instruction takes 4 clocks on a SIMD) x 2.4 GHz,
+# in lane operations per second.
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 
 
 def bench_queue(args) -> int:
@@ -855,11 +868,41 @@ def bench_queue(args) -> int:
           f"stages {stage_ms}", file=sys.stderr, flush=True)
 
     dom = max(stage_ms, key=stage_ms.get)
-    achieved = STAGE_BYTES[dom] * n / (stage_ms[dom] * 1e-3) / 1e9
+    hbm_achieved = STAGE_BYTES[dom] * n / (stage_ms[dom] * 1e-3) / 1e9
     traffic = counter_traffic(n) if dom == "final" else None
-    step_prof = profile_values(STEP_COUNTERS, FINAL_SOURCE, ["hbm_bytes_per_step"], n)
-    step_bytes = step_prof["hbm_bytes_per_step"] if step_prof else None
+    prof = profile_values(STEP_COUNTERS, FINAL_SOURCE,
+                          ["hbm_bytes_per_step", "final_valu_insts_per_launch"], n)
+    step_bytes = prof["hbm_bytes_per_step"] if prof else None
     step_gbps = step_bytes / (ms_step * 1e-3) / 1e9 if step_bytes else None
+    kernel = f"{dom} scatter pass" if dom != "hist" else "histogram pass"
+    hbm = {
+        # the dominant pass's algorithmic bytes per request over its launch time
+        "hbm_achieved_GBps": hbm_achieved,
+        "hbm_peak_GBps": HBM_PEAK_GBPS,
+        "hbm_frac": hbm_achieved / HBM_PEAK_GBPS,
+        "bytes_per_request": STAGE_BYTES[dom],
+        "avg_launch_ms": stage_ms[dom],
+        # the whole step: algorithmic bytes (17 per request) and the HBM
+        # bytes the counters measured for one step, over the median step time
+        "step_algorithmic_GBps": PATH_BYTES * n / (ms_step * 1e-3) / 1e9,
+        "step_algorithmic_frac": PATH_BYTES * n / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "step_counter_bytes": step_bytes,
+        "step_counter_GBps": step_gbps,
+        "step_frac": step_gbps / HBM_PEAK_GBPS if step_gbps else None,
+    }
+    if dom == "final" and prof:
+        # The committed counters show the final pass bound by instruction
+        # issue (VALU), not by HBM: its roofline is the integer VALU rate,
+        # its VALU wave-instructions per launch (counters) x 64 lanes over the
+        # launch time measured here.
+        valu_tops = prof["final_valu_insts_per_launch"] * 64 / (stage_ms[dom] * 1e-3) / 1e12
+        roofline = {"bound": "alu", "kernel": kernel, "achieved": valu_tops,
+                    "peak": VALU_PEAK_TOPS, "unit": "TOP/s (32-bit integer VALU lane operations)",
+                    "frac": valu_tops / VALU_PEAK_TOPS, "traffic": traffic, **hbm}
+    else:
+        roofline = {"bound": "hbm", "kernel": kernel, "achieved": hbm_achieved,
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": hbm_achieved / HBM_PEAK_GBPS,
+                    "traffic": traffic, **hbm}
     out = {
         "metric": METRIC,
         "value": n / (ms_step * 1e-3),
@@ -880,24 +923,7 @@ def bench_queue(args) -> int:
             "parallelism": "single GPU",
             "input_sha256": workload_sha256(w),
         },
-        "roofline": {
-            "bound": "hbm",
-            "kernel": f"{dom} scatter pass" if dom != "hist" else "histogram pass",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic,
-            "bytes_per_request": STAGE_BYTES[dom],
-            "avg_launch_ms": stage_ms[dom],
-            # the whole step: algorithmic bytes (17 per request) and the HBM
-            # bytes the counters measured for one step, over the median step time
-            "step_algorithmic_GBps": PATH_BYTES * n / (ms_step * 1e-3) / 1e9,
-            "step_algorithmic_frac": PATH_BYTES * n / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-            "step_counter_bytes": step_bytes,
-            "step_counter_GBps": step_gbps,
-            "step_frac": step_gbps / HBM_PEAK_GBPS if step_gbps else None,
-        },
+        "roofline": roofline,
         "stage_ms": stage_ms,
     }
 

@@ -937,7 +937,7 @@ struct WideLayout {
   size_t total = kHeaderBytes;
 };
 
-WideLayout wide_layout(int64_t entries, bool evict) {
+static WideLayout wide_layout(int64_t entries, bool evict) {
   WideLayout L;
   size_t off = kHeaderBytes;
   auto take = [&](size_t bytes) {

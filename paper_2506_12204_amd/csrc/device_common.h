@@ -126,9 +126,14 @@ __device__ __forceinline__ uint32_t rank_round_c(uint32_t d, uint16_t* cnt) {
 // earlier items of the wave with the same digit and advances the counter.
 __device__ __forceinline__ uint32_t rank_round_mask(uint32_t d, u64_alias* masks,
                                                     uint16_t* cnt) {
-  atomicOr(reinterpret_cast<unsigned long long*>(masks + d), 1ull << lane_id());
+  // Each half of the wave sets and clears only its own 32-bit half of the
+  // digit's mask (one bank per lane instead of two); the peers are read as
+  // the whole 64-bit mask.
+  const uint32_t lane = (uint32_t)lane_id();
+  u32_alias* half = reinterpret_cast<u32_alias*>(masks + d) + (lane >> 5);
+  atomicOr(reinterpret_cast<unsigned int*>(half), 1u << (lane & 31u));
   const uint64_t peers = masks[d];
-  masks[d] = 0;
+  *half = 0;
   const uint32_t below = __builtin_amdgcn_mbcnt_hi(
       (uint32_t)(peers >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
   const uint32_t base = cnt[d];
@@ -259,17 +264,12 @@ __device__ __forceinline__ void atomic_add128(uint64_t* lo, uint64_t* hi,
             (unsigned long long)(v.hi + carry));
 }
 
-// Relaxed agent-scope loads and stores for the look-back status words. Each
-// word carries its own flag and value, so no ordering with other memory is
-// needed, only coherence across the XCDs' L2 caches.
+// Relaxed agent-scope load of a word other workgroups (possibly on other
+// XCDs) update with atomics, such as the error flags: coherent across the
+// XCDs' L2 caches, with no ordering against other memory.
 template <typename T>
 __device__ __forceinline__ T load_agent(const T* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-template <typename T>
-__device__ __forceinline__ void store_agent(T* p, T v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 }  // namespace semsched

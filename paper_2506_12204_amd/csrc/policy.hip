@@ -250,6 +250,21 @@ __device__ __forceinline__ uint32_t max_byte(uint32_t m, uint32_t x) {
 
 // Largest rank over all requests: 16-byte loads over the aligned body,
 // single bytes before and after it.
+// Adds this workgroup's largest value to *dst: a wave maximum, the workgroup
+// maximum in LDS, then one global atomic, skipped when *dst already holds at
+// least as much (one device-scope atomic on a single word serialises at
+// about 11 ns; one per wave over a 2^26-request queue took longer than the
+// loads themselves). Every thread of the workgroup must call it.
+__device__ __forceinline__ void group_max_to(uint32_t* dst, uint32_t m) {
+  __shared__ uint32_t gmax;
+  if (threadIdx.x == 0) gmax = 0;
+  __syncthreads();
+  m = wave_max_u32(m);
+  if (lane_id() == 0 && m) atomicMax(&gmax, m);
+  __syncthreads();
+  if (threadIdx.x == 0 && gmax && gmax > load_agent(dst)) atomicMax(dst, gmax);
+}
+
 __global__ __launch_bounds__(PT) void p_range(PolArgs a) {
   const uintptr_t addr = reinterpret_cast<uintptr_t>(a.priority);
   const int64_t head = std::min<int64_t>(a.n, (int64_t)((16 - (addr & 15)) & 15));
@@ -265,8 +280,7 @@ __global__ __launch_bounds__(PT) void p_range(PolArgs a) {
   if (t < head) m = max(m, (uint32_t)a.priority[t]);
   const int64_t tail = head + body * 16;
   if (tail + t < a.n) m = max(m, (uint32_t)a.priority[tail + t]);  // (fewer than 16 left)
-  m = wave_max_u32(m);
-  if (lane_id() == 0 && m) atomicMax(a.pmax, m);
+  group_max_to(a.pmax, m);
 }
 
 // Calls f(length, rank, live) for every element of the range starting at k0
@@ -315,8 +329,8 @@ __device__ __forceinline__ bool vec_ok(const PolArgs& a) {
 // FCFS: length sum of every range and the largest rank; negative lengths
 // are flagged.
 __global__ __launch_bounds__(PT) void f_sums(PolArgs a, int64_t ranges) {
-  const int64_t w = wave_index();
-  if (w >= ranges) return;
+  const int64_t w = min(wave_index(), ranges - 1);  // (waves past the end repeat the last range)
+  const bool live = wave_index() < ranges;
   const int64_t k0 = w * kPolRange;
   uint64_t s = 0;
   uint32_t m = 0;
@@ -336,10 +350,9 @@ __global__ __launch_bounds__(PT) void f_sums(PolArgs a, int64_t ranges) {
   if (__ballot(bad)) {
     if (lane_id() == 0) atomicOr(a.flags, kFlagRange);
   }
-  m = wave_max_u32(m);
-  if (lane_id() == 0 && m) atomicMax(a.pmax, m);
+  group_max_to(a.pmax, m);
   s = readlane_u64(wave_incl_scan_u64(s), 63);
-  if (lane_id() == 0) a.rsum[w] = s;
+  if (lane_id() == 0 && live) a.rsum[w] = s;
 }
 
 // Exclusive scan in place of `count` contiguous values (one block; thread t
@@ -828,7 +841,7 @@ int64_t ranges_of(int64_t n) { return (n + kPolRange - 1) / kPolRange; }
 int64_t blocks_of(int64_t n) { return (ranges_of(n) + kWaves - 1) / kWaves; }
 
 hipError_t launch_p_range(const PolArgs& a, hipStream_t st) {
-  const int64_t g = std::min<int64_t>((a.n + PT * 64 - 1) / (PT * 64), 4096);
+  const int64_t g = std::min<int64_t>((a.n + PT * 64 - 1) / (PT * 64), 1024);
   hipLaunchKernelGGL(p_range, dim3((unsigned)std::max<int64_t>(g, 1)), dim3(PT), 0, st, a);
   return hipGetLastError();
 }
