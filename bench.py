@@ -45,6 +45,10 @@ else:
         "final": 16,  # read the element (4 B), write order (4 B) + wait (8 B)
     }
 PATH_BYTES = 17  # the whole schedule's own inputs + outputs per request
+# Peak rate of 32-bit integer VALU work on MI355X: 256 CUs x 4 SIMDs x 16
+# lanes per clock (a wave64 instruction takes 4 clocks on a SIMD) x 2.4 GHz,
+# in lane operations per second.
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 COUNTERS = os.path.join(ROOT, "profiles", "c3_step_counters.md")
 CSRC = os.path.join(ROOT, "paper_2506_12204_amd", "csrc")
 # the headers every kernel is built with: a counter measurement belongs to a
@@ -599,8 +603,22 @@ def bench_batched(args) -> int:
     print(f"[bench] {args.steps} calls: median {ms_step:.4f} ms (mean {ms_mean:.4f}), "
           f"{gbps:.0f} GB/s algorithmic", file=sys.stderr, flush=True)
     prof = profile_values(os.path.join(ROOT, "profiles", f"batched_{args.workload}_counters.md"),
-                          BATCHED_SOURCE, ["hbm_bytes_per_call"], n)
+                          BATCHED_SOURCE, ["hbm_bytes_per_call", "valu_insts_per_call"], n)
     traffic = prof["hbm_bytes_per_call"] if prof else None
+    hbm = {"hbm_achieved_GBps": gbps, "hbm_peak_GBps": HBM_PEAK_GBPS,
+           "hbm_frac": gbps / HBM_PEAK_GBPS, "bytes_per_request": 17,
+           "counter_GBps": (traffic / (ms_step * 1e-3) / 1e9) if traffic else None}
+    if prof:
+        # the committed counters show the call's kernels bound by instruction
+        # issue: VALU wave-instructions per call x 64 lanes over the call time
+        valu_tops = prof["valu_insts_per_call"] * 64 / (ms_step * 1e-3) / 1e12
+        roofline = {"bound": "alu", "kernel": "whole batched call", "achieved": valu_tops,
+                    "peak": VALU_PEAK_TOPS, "unit": "TOP/s (32-bit integer VALU lane operations)",
+                    "frac": valu_tops / VALU_PEAK_TOPS, "traffic": traffic, **hbm}
+    else:
+        roofline = {"bound": "hbm", "kernel": "whole batched call", "achieved": gbps,
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS,
+                    "traffic": traffic, **hbm}
     out = {
         "metric": "scheduled requests/sec, batched independent queues, 1 GPU",
         "value": n / (ms_step * 1e-3),
@@ -617,10 +635,7 @@ def bench_batched(args) -> int:
         "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "n": n, "queues": s,
                    "parallelism": "single GPU", "input_sha256": workload_sha256(w)},
-        "roofline": {"bound": "hbm", "kernel": "whole batched call", "achieved": gbps,
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS,
-                     "traffic": traffic, "bytes_per_request": 17,
-                     "counter_GBps": (traffic / (ms_step * 1e-3) / 1e9) if traffic else None},
+        "roofline": roofline,
     }
     if not args.no_cpu_baseline:
         from oracle import c_oracle_batched, c_oracle_batched_parallel
@@ -818,10 +833,6 @@ def main() -> int:
 
 
 STEP_COUNTERS = COUNTERS
-# Peak rate of 32-bit integer VALU work on MI355X: 256 CUs x 4 SIMDs x 16
-# lanes per clock (a wave64 instruction takes 4 clocks on a SIMD) x 2.4 GHz,
-# in lane operations per second.
-VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 
 
 def bench_queue(args) -> int:
