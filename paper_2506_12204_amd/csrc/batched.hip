@@ -243,38 +243,6 @@ __device__ __forceinline__ void digit_positions(uint16_t (*cnt)[NB], uint32_t* s
   group_sync<NW>();
 }
 
-// Lanes of the wave whose digit differs from this lane's in at least one of
-// the low nbits bits (nbits uniform). Per bit: the lane's bit as a 0/-1 mask,
-// its ballot, and one three-input bit operation per half that ORs the lanes
-// whose bit differs into the set.
-__device__ __forceinline__ uint64_t mismatch_bits(uint32_t d, uint32_t nbits) {
-  uint32_t lo = 0, hi = 0;
-  for (uint32_t b = 0; b < nbits; ++b) {
-    uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)d, b, 1);
-    asm("" : "+v"(m));
-    const uint64_t bal = __builtin_amdgcn_ballot_w64(m != 0);
-    lo = __builtin_amdgcn_bitop3_b32(lo, (uint32_t)bal, m, 0xF6);  // lo | (bal ^ m)
-    hi = __builtin_amdgcn_bitop3_b32(hi, (uint32_t)(bal >> 32), m, 0xF6);
-  }
-  return ((uint64_t)hi << 32) | lo;
-}
-
-// Stable rank of one round of 64 digits of nbits bits against this wave's
-// running counters: the number of earlier elements of the wave (earlier
-// rounds, then lower lanes of this round) with the same digit. Every peer
-// writes the same new count. (Peers below = lanes below - mismatching lanes
-// below; peers = 64 - mismatching lanes.)
-__device__ __forceinline__ uint32_t rank_round_n(uint32_t d, uint32_t nbits, uint16_t* cnt) {
-  const uint64_t other = mismatch_bits(d, nbits);
-  const uint32_t below = (uint32_t)lane_id() - __builtin_amdgcn_mbcnt_hi(
-      (uint32_t)(other >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)other, 0u));
-  const uint32_t base = cnt[d];
-  cnt[d] = (uint16_t)(base + (uint32_t)kWave - (uint32_t)__popcll(other));
-  uint32_t rank = base + below;
-  asm volatile("" : "+v"(rank));
-  return rank;
-}
-
 // Calls f(std::integral_constant<int, B>) for the B = nb in 1 .. NBITS
 // (nb uniform), so that the ranking of a pass matches a compile-time number
 // of digit bits.
@@ -429,15 +397,18 @@ __device__ bool schedule_loaded(const BArgs& a, int64_t s, int64_t base, int m,
     const uint32_t nb = min(bpp, kb - q * bpp);
     clear_counters<NB>(mycnt);
     uint32_t dg[R], rk[R];
-    // A wave alone ranks with the bit count compiled in (unrolled matching);
-    // for workgroups the extra registers of that cost more occupancy than the
-    // loop over bits costs issue slots.
+    // A wave alone ranks with the pass's bit count compiled in (a form per
+    // width); a workgroup matches its full digit width D in one form, since
+    // more forms cost it registers and occupancy.
     if constexpr (NW > 1) {
+      // Every lane's digit has zeros above its nb live bits, so matching all
+      // D bits finds the same peers, unrolled at compile time with no loop
+      // over the bits (a second, narrower form would cost registers).
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         if (r < kr) {
           dg[r] = (uint32_t)(e[r] >> shift) & ((1u << nb) - 1u);
-          rk[r] = rank_round_n(dg[r], nb, mycnt);
+          rk[r] = rank_round_c<D>(dg[r], mycnt);
         }
       }
     } else
