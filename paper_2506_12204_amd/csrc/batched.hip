@@ -165,11 +165,9 @@ __device__ __forceinline__ uint32_t group_excl_scan_u32(uint32_t v, uint32_t* sc
   }
 __device__ __forceinline__ uint32_t op_min(uint32_t a, uint32_t b) { return min(a, b); }
 __device__ __forceinline__ uint32_t op_max(uint32_t a, uint32_t b) { return max(a, b); }
-__device__ __forceinline__ uint32_t op_or(uint32_t a, uint32_t b) { return a | b; }
 __device__ __forceinline__ uint32_t op_add(uint32_t a, uint32_t b) { return a + b; }
 SEMSCHED_DPP_REDUCE(wave_rmin, op_min, 0xffffffffu)
 SEMSCHED_DPP_REDUCE(wave_rmax, op_max, 0u)
-SEMSCHED_DPP_REDUCE(wave_ror, op_or, 0u)
 SEMSCHED_DPP_REDUCE(wave_radd, op_add, 0u)
 #undef SEMSCHED_DPP_REDUCE
 
@@ -323,12 +321,11 @@ __device__ bool schedule_loaded(const BArgs& a, int64_t s, int64_t base, int m,
   const int j0 = wb + lane;          // this lane's position in round 0
 
   // ---- ranges and validation (past the end: 0, neutral for max) --------------------
-  uint32_t lmin = 0xffffffffu, lmax = 0, pmin = 0xffu, pmax = 0, bad = 0;
+  uint32_t lmin = 0xffffffffu, lmax = 0, pmin = 0xffu, pmax = 0;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     if (r < kr) {
       const bool valid = j0 + r * kWave < m;
-      bad |= ((int32_t)lv[r] < 0) | (pv[r] >= (uint32_t)a.num_classes);
       lmin = min(lmin, valid ? lv[r] : 0xffffffffu);
       lmax = max(lmax, lv[r]);
       pmin = min(pmin, valid ? pv[r] : 0xffu);
@@ -339,34 +336,32 @@ __device__ bool schedule_loaded(const BArgs& a, int64_t s, int64_t base, int m,
   lmax = wave_rmax(lmax);
   pmin = wave_rmin(pmin);
   pmax = wave_rmax(pmax);
-  bad = wave_ror(bad);
   if constexpr (NW > 1) {
     if (lane == 0) {
       sh.red[0][w] = lmin;
       sh.red[1][w] = lmax;
       sh.red[2][w] = pmin;
-      sh.red[3][w] = pmax | (bad << 31);
+      sh.red[3][w] = pmax;
     }
     group_sync<NW>();
     lmin = 0xffffffffu;
     lmax = 0;
     pmin = 0xffu;
     pmax = 0;
-    bad = 0;
 #pragma unroll
     for (int v = 0; v < NW; ++v) {
       lmin = min(lmin, sh.red[0][v]);
       lmax = max(lmax, sh.red[1][v]);
       pmin = min(pmin, sh.red[2][v]);
-      pmax = max(pmax, sh.red[3][v] & 0xffu);
-      bad |= sh.red[3][v] >> 31;
+      pmax = max(pmax, sh.red[3][v]);
     }
   }
   lmin = uni(lmin);
   lmax = uni(lmax);
   pmin = uni(pmin);
   pmax = uni(pmax);
-  if (uni(bad)) {
+  // a negative length is above 2^31 as u32, so it shows in lmax
+  if ((lmax >> 31) | (pmax >= (uint32_t)a.num_classes)) {
     if (t == 0) atomicOr(a.flags, kFlagRange);
     return true;
   }
@@ -504,25 +499,20 @@ __device__ bool schedule_loaded(const BArgs& a, int64_t s, int64_t base, int m,
   // ---- totals of the queue: exact, and below 2^59, so the high words are 0 ------
   const int64_t C1 = 1 + a.num_classes;
   uint64_t* tot = a.totals + 2 * s * C1;
-  uint64_t part = 0;
   for (int c = t; c < a.num_classes; c += NT) {
     const uint64_t v = ((uint32_t)c >= pmin && (uint32_t)c <= pmax) ? sh.cls[c - pmin] : 0ull;
     tot[2 * (1 + c)] = v;
     tot[2 * (1 + c) + 1] = 0;
-    part += v;
   }
-  part = wave_rsum_u64(part);
-  if constexpr (NW > 1) {
-    group_sync<NW>();  // every wave has read `wtot` above
-    if (lane == 0) sh.wtot[w] = part;
-    group_sync<NW>();
-    part = 0;
-#pragma unroll
-    for (int v = 0; v < NW; ++v) part += sh.wtot[v];
-  }
-  if (t == 0) {
-    tot[0] = part;
-    tot[1] = 0;
+  // the queue's total, the sum of its classes' sums, by the first wave alone
+  if (w == 0) {
+    uint64_t part = 0;
+    for (uint32_t c = lane; c < P; c += kWave) part += sh.cls[c];
+    part = wave_rsum_u64(part);
+    if (lane == 0) {
+      tot[0] = part;
+      tot[1] = 0;
+    }
   }
   return true;
 }
@@ -642,8 +632,13 @@ __global__ __launch_bounds__(kPlanThreads, 8) void b_plan(BArgs a, int chunk) {
   }
 }
 
-// Queues of 257 .. 4096 requests: one 256-thread workgroup each.
-using MediumLds = GroupLds<4, 16, 10, uint32_t>;
+// Queues of 257 .. 4096 requests: one 256-thread workgroup each, digits of
+// at most 7 bits. A workgroup matches all D bits of every pass, so the bits
+// matched per request are D times the passes: 14 for keys of up to 14 bits
+// (8 classes and lengths spanning less than 2^11), where 10-bit digits match
+// 20 and 8-bit ones 16; keys of 15 .. 20 bits take three passes (21 bits, one
+// more than two 10-bit passes).
+using MediumLds = GroupLds<4, 16, 7, uint32_t>;
 
 // Queues of up to 16384 requests with any key: one 1024-thread workgroup each,
 // 64-bit elements. Also the single-queue call for n <= 16384.
@@ -679,7 +674,7 @@ __device__ void block_list_loop(const BArgs& a, int L, GroupLds<NW, R, D, ET>& s
 // queues than the four that 113 registers allowed (six spill).
 __global__ __launch_bounds__(256, 5) void b_medium(BArgs a) {
   __shared__ MediumLds sh;
-  block_list_loop<4, 16, 12, 10, uint32_t>(a, kListMedium, sh);
+  block_list_loop<4, 16, 12, 7, uint32_t>(a, kListMedium, sh);
 }
 
 __global__ __launch_bounds__(kWideThreads) void b_wide(BArgs a) {

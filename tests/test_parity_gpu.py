@@ -360,6 +360,20 @@ def test_negative_length_in_long_batched_queue():
             gpu_batched(p, l, off, 4, blocking=blocking)
 
 
+@pytest.mark.parametrize("sizes,where", [([10, 20, 30], 15), ([10, 300, 30], 200),
+                                         ([5, 5000, 7], 2000)])
+@pytest.mark.parametrize("bad_len", [-1, -2**31])
+def test_negative_length_in_batched_queue(sizes, where, bad_len):
+    # one queue of each size class below the segmented sort (one wave,
+    # 256-thread and 1024-thread workgroups)
+    import paper_2506_12204_amd as ss
+    p, l, off = fuzz_segments(sizes, seed=7, classes=4)
+    l[where] = bad_len
+    for blocking in (False, True):
+        with pytest.raises(ss.SemschedRangeError):
+            gpu_batched(p, l, off, 4, blocking=blocking)
+
+
 def test_bad_offsets():
     import paper_2506_12204_amd as ss
     p, l, off = fuzz_segments([10, 20, 30], seed=3, classes=4)
