@@ -588,7 +588,8 @@ BLayout batched_layout(int64_t S, uint64_t long_cap) {
     return at;
   };
   L.grab = take(sizeof(GrabLine) * kLists * kSubLists);
-  L.lists = take(4 * (size_t)kLists * (size_t)S);
+  // the medium and wide lists' segments, then the long list
+  L.lists = take(4 * (2 * kSubLists * (size_t)list_segment_cap(S) + (size_t)S));
   if (long_cap > 0) {
     const uint64_t queues = std::min<uint64_t>((uint64_t)S, long_cap / (kSegLargeCap + 1));
     L.max_tiles = long_max_tiles(long_cap, S);
@@ -643,6 +644,7 @@ int enqueue_batched(const uint8_t* p, const int32_t* l, const int64_t* offsets,
   a.ctl = reinterpret_cast<BCtl*>(base + L.ctl);
   a.grab = reinterpret_cast<GrabLine*>(base + L.grab);
   a.lists = reinterpret_cast<uint32_t*>(base + L.lists);
+  a.seg_cap = list_segment_cap(num_segments);
   a.long_cap = cap;
   a.max_tiles = L.max_tiles;
   if (cap > 0) {

@@ -17,12 +17,15 @@
 //             those on), one 1024-thread workgroup each on 64-bit elements
 //   b_long    queues of more than 16384 requests: one segmented LSD radix
 //             sort over all of them, in a cooperative launch
-// Each work list is split into kSubLists interleaved sub-lists with a grab
-// counter each. A workgroup starts on the sub-list of its XCD (blockIdx % 8),
-// takes queues from it, and moves on to the others when it is empty, so
-// queues of ragged sizes spread evenly over the grid (one counter for the
-// whole list would serialise the grabs of every workgroup). The short queues
-// of the planner need no such grabs: each chunk's are few and similar.
+// The medium and wide work lists are split into kSubLists segments, each
+// with an entry counter and a grab counter in a line of its own: the
+// planner files a chunk's queues into the segment of the chunk's index
+// modulo kSubLists, and a workgroup starts on the segment of its XCD
+// (blockIdx % 8), takes queues from it, and moves on to the others when it
+// is empty, so queues of ragged sizes spread evenly over the grid. One
+// counter for a whole list would serialise the filing atomics of every
+// planner workgroup and the grabs of every workgroup. The short queues of
+// the planner need no such grabs: each chunk's are few and similar.
 //
 // Inside a workgroup a queue of m requests is loaded once (coalesced rounds
 // of 64), its live key bits (priority - pmin, length - lmin) are found by a
@@ -65,38 +68,50 @@ __device__ __forceinline__ void queue_bounds(const BArgs& a, int64_t s, int64_t&
   }
 }
 
-// Entry k of list L belongs to sub-list k % kSubLists; batch i of sub-list j
-// holds its entries i*B .. i*B + B - 1, i.e. list entries (i*B + b) * 8 + j.
-// Grabbers (a wave or a workgroup, per_wg of them per workgroup) on XCD j
-// (blockIdx % 8) serve sub-list j. Grabber li of them takes batch li first,
-// with no atomic; a grabber whose first batch is past the end stops there
-// (the sub-lists differ by at most one entry, so the others are served too).
-// Later batches come from the sub-list's counter, offset by the number of its
-// grabbers, then from the other sub-lists' counters. Called by one lane;
-// `state` starts at -1. Returns the first list entry of the batch (the others
-// follow at strides of kSubLists) or a negative value when done.
+// First slot in a.lists of segment j of list L (medium or wide), or of the
+// long list.
+__device__ __forceinline__ int64_t list_base(const BArgs& a, int L, int j) {
+  return L == kListLong ? 2 * kSubLists * a.seg_cap
+                        : ((int64_t)(L - kListMedium) * kSubLists + j) * a.seg_cap;
+}
+
+// The segment of list L that the slot k of a.lists lies in.
+__device__ __forceinline__ int segment_of(const BArgs& a, int L, int64_t k) {
+  return (int)((k - list_base(a, L, 0)) / a.seg_cap);
+}
+
+// Batch i of segment j holds its entries i*B .. i*B + B - 1. Grabbers (a
+// wave or a workgroup, per_wg of them per workgroup) on XCD j (blockIdx % 8)
+// serve segment j first: grabber li of them takes batch li with no atomic;
+// later batches come from the segment's counter, offset by the number of its
+// grabbers, then from the other segments' counters (a grabber whose first
+// batch is past its segment's end goes straight to those). Called by one
+// lane, with the segments' entry counts n; `state` starts at -1. Returns the
+// slot in a.lists of the batch's first entry (the others follow) or a
+// negative value when done.
 __device__ __forceinline__ uint32_t grabbers_on(int j, int per_wg) {
   const int g = (int)gridDim.x;
   return j < g ? (uint32_t)(((g - 1 - j) / kSubLists + 1) * per_wg) : 0u;
 }
 
 template <int B>
-__device__ int64_t next_batch(const BArgs& a, int L, int per_wg, uint32_t li, int& state) {
-  const uint32_t n = a.ctl->count[L];
+__device__ int64_t next_batch(const BArgs& a, int L, const uint32_t* n, int per_wg, uint32_t li,
+                              int& state) {
   const int j0 = (int)(blockIdx.x & (kSubLists - 1));
   if (state < 0) {
     state = 0;
-    const uint64_t k = (uint64_t)li * B * kSubLists + (uint64_t)j0;
-    return k < n ? (int64_t)k : -1;
+    const uint64_t k = (uint64_t)li * B;
+    if (k < n[j0]) return list_base(a, L, j0) + (int64_t)k;
   }
   while (state < kSubLists) {
     const int j = (j0 + state) & (kSubLists - 1);
-    // the hint saves the atomic on a sub-list another grabber found empty
-    if ((uint32_t)j < n && !__hip_atomic_load(&a.ctl->empty[L][j], __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT)) {
-      const uint32_t i = grabbers_on(j, per_wg) + atomicAdd(&a.grab[L * kSubLists + j].next, 1u);
-      const uint64_t k = (uint64_t)i * B * kSubLists + (uint64_t)j;
-      if (k < n) return (int64_t)k;
+    const uint32_t free = grabbers_on(j, per_wg);  // batches taken without an atomic
+    // the hint saves the atomic on a segment another grabber found empty
+    if ((uint64_t)free * B < n[j] && !__hip_atomic_load(&a.ctl->empty[L][j], __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT)) {
+      const uint32_t i = free + atomicAdd(&a.grab[L * kSubLists + j].next, 1u);
+      const uint64_t k = (uint64_t)i * B;
+      if (k < n[j]) return list_base(a, L, j) + (int64_t)k;
       __hip_atomic_store(&a.ctl->empty[L][j], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     ++state;
@@ -104,9 +119,10 @@ __device__ int64_t next_batch(const BArgs& a, int L, int per_wg, uint32_t li, in
   return -1;
 }
 
-__device__ __forceinline__ void hand_on(const BArgs& a, int L, int64_t s) {
-  const uint32_t pos = atomicAdd(&a.ctl->count[L], 1u);
-  a.lists[(size_t)L * a.num_segments + pos] = (uint32_t)s;
+// Appends queue s to segment j of list L (the segment of the chunk it came from).
+__device__ __forceinline__ void hand_on(const BArgs& a, int L, int j, int64_t s) {
+  const uint32_t pos = atomicAdd(&a.grab[L * kSubLists + j].count, 1u);
+  a.lists[list_base(a, L, j) + pos] = (uint32_t)s;
 }
 
 // ---- one queue in LDS ------------------------------------------------------------
@@ -536,10 +552,9 @@ __device__ bool schedule_in_lds(const BArgs& a, int64_t s, int64_t base, int m,
 // wave at a time, round robin (no workgroup barrier, and the inputs of a
 // wave's next queue load while it schedules the current one); longer queues
 // into the global work lists of the other kernels (one atomic per list and
-// chunk reserves their room).
+// chunk, on the chunk's segment, reserves their room).
 constexpr int kPlanThreads = 256;
 constexpr int kPlanWaves = kPlanThreads / kWave;
-constexpr int kPlanChunk = 256;  // largest chunk (its lists must leave room for eight workgroups per CU)
 using TinyLds = GroupLds<1, 4, 8, uint32_t>;
 
 // Eight waves per SIMD (at most 64 registers, and LDS for eight workgroups
@@ -555,6 +570,10 @@ __global__ __launch_bounds__(kPlanThreads, 8) void b_plan(BArgs a, int chunk) {
   const int lane = lane_id();
   const int64_t S = a.num_segments;
   const int64_t C1 = 1 + a.num_classes;
+  // The chunk's segment of the medium and wide lists: chunk c is planned by
+  // workgroup c % gridDim.x, and the grid is a multiple of kSubLists or has
+  // one chunk per workgroup, so this is c % kSubLists.
+  const int seg = (int)(blockIdx.x & (kSubLists - 1));
   for (int64_t c0 = (int64_t)blockIdx.x * chunk; c0 < S; c0 += (int64_t)gridDim.x * chunk) {
     if (t < kLists) lcnt[t] = 0;
     if (t == 0) llong = 0;
@@ -586,13 +605,16 @@ __global__ __launch_bounds__(kPlanThreads, 8) void b_plan(BArgs a, int chunk) {
       if (L == kListLong) atomicAdd(&llong, (unsigned long long)m);
     }
     __syncthreads();
-    if (t > kListTiny && t < kLists && lcnt[t]) lbase[t] = atomicAdd(&a.ctl->count[t], lcnt[t]);
+    if (t > kListTiny && t < kLists && lcnt[t])
+      lbase[t] = atomicAdd(t == kListLong ? &a.ctl->count[kListLong]
+                                          : &a.grab[t * kSubLists + seg].count,
+                           lcnt[t]);
     if (t == 0 && llong)
       atomicAdd(reinterpret_cast<unsigned long long*>(&a.ctl->long_elems), llong);
     __syncthreads();
     for (int L = kListTiny + 1; L < kLists; ++L)
       for (uint32_t i = t; i < lcnt[L]; i += kPlanThreads)
-        a.lists[(size_t)L * S + lbase[L] + i] = lst[L][i];
+        a.lists[list_base(a, L, seg) + lbase[L] + i] = lst[L][i];
 
     // the chunk's queues of at most 256 requests, wave w taking every 4th
     const uint32_t nt = lcnt[kListTiny];
@@ -617,7 +639,7 @@ __global__ __launch_bounds__(kPlanThreads, 8) void b_plan(BArgs a, int chunk) {
         load_queue<1, 4>(a, base1, (int)m1, 0, pn, ln);
       }
       if (!schedule_loaded<1, 4, 8, 8, uint32_t>(a, s, base, (int)m, pv, lv, tl[w], 0, lane))
-        if (lane == 0) hand_on(a, kListWide, s);
+        if (lane == 0) hand_on(a, kListWide, seg, s);
       i = i1;
       s = s1;
       base = base1;
@@ -653,18 +675,27 @@ __device__ void block_list_loop(const BArgs& a, int L, GroupLds<NW, R, D, ET>& s
   const int w = wave_index();
   const uint32_t li = blockIdx.x / kSubLists;
   int state = -1;
-  if (t == 0) sh.next = next_batch<1>(a, L, 1, li, state);
+  // the segments' entry counts (final: the kernels before this one filed
+  // them), read once by the grabbing thread
+  __shared__ uint32_t n[kSubLists];
+  if (t == 0) {
+    uint32_t c[kSubLists];
+#pragma unroll
+    for (int j = 0; j < kSubLists; ++j) c[j] = a.grab[L * kSubLists + j].count;
+#pragma unroll
+    for (int j = 0; j < kSubLists; ++j) n[j] = c[j];
+    sh.next = next_batch<1>(a, L, n, 1, li, state);
+  }
   block_sync();
   int64_t k = sh.next;
-  const uint32_t n = a.ctl->count[L];
-  while (k >= 0 && k < (int64_t)n) {  // (next_batch never returns k >= n)
+  while (k >= 0) {
     block_sync();  // every thread has read sh.next
-    if (t == 0) sh.next = next_batch<1>(a, L, 1, li, state);
-    const int64_t s = a.lists[(size_t)L * a.num_segments + k];
+    if (t == 0) sh.next = next_batch<1>(a, L, n, 1, li, state);
+    const int64_t s = a.lists[k];
     int64_t base, m;
     queue_bounds(a, s, base, m);
     if (!schedule_in_lds<NW, R, IDB, D, ET>(a, s, base, (int)m, sh, w, t))
-      if (t == 0) hand_on(a, kListWide, s);
+      if (t == 0) hand_on(a, kListWide, segment_of(a, L, k), s);
     block_sync();
     k = sh.next;
   }
@@ -732,7 +763,7 @@ __device__ LongTile long_tile(const BArgs& a, uint32_t t, uint32_t K) {
   }
   LongTile x;
   x.k = lo;
-  x.s = a.lists[(size_t)kListLong * a.num_segments + lo];
+  x.s = a.lists[list_base(a, kListLong, 0) + lo];
   x.base = a.offsets[x.s];
   x.m = a.offsets[x.s + 1] - x.base;
   x.lo = (int64_t)(t - a.tstart[lo]) * kLongTile;
@@ -762,7 +793,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       const uint32_t k = k0 + t;
       uint64_t m = 0;
       if (k < K) {
-        const int64_t s = a.lists[(size_t)kListLong * a.num_segments + k];
+        const int64_t s = a.lists[list_base(a, kListLong, 0) + k];
         m = (uint64_t)(a.offsets[s + 1] - a.offsets[s]);
       }
       const uint32_t tiles = (uint32_t)((m + kLongTile - 1) / kLongTile);
@@ -789,7 +820,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   }
   for (int64_t i = (int64_t)blockIdx.x * kLT + t; i < (int64_t)K * 2 * C1;
        i += (int64_t)gridDim.x * kLT) {
-    const int64_t s = a.lists[(size_t)kListLong * a.num_segments + i / (2 * C1)];
+    const int64_t s = a.lists[list_base(a, kListLong, 0) + i / (2 * C1)];
     a.totals[2 * s * C1 + i % (2 * C1)] = 0;
   }
   grid.sync();
@@ -1079,10 +1110,13 @@ hipError_t launch_batched(const BArgs& a, hipStream_t st) {
   static const int r_wide = resident(b_wide, kWideThreads);
   static const int r_long = resident(b_long, kLT);
   const int64_t S = a.num_segments;
-  // chunks of about S / (resident planner workgroups) queues, at most kPlanChunk
-  const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(kPlanChunk, (S + r_plan - 1) / r_plan));
-  hipLaunchKernelGGL(b_plan, dim3(grid_for(r_plan, (S + chunk - 1) / chunk)), dim3(kPlanThreads),
-                     0, st, a, (int)chunk);
+  // chunks of about S / (resident planner workgroups) queues, at most
+  // kPlanChunk; a grid of one workgroup per chunk, or else a multiple of
+  // kSubLists (the planner files chunk c into list segment c % kSubLists)
+  const int r8 = std::max(kSubLists, r_plan / kSubLists * kSubLists);
+  const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(kPlanChunk, (S + r8 - 1) / r8));
+  hipLaunchKernelGGL(b_plan, dim3(grid_for(r8, (S + chunk - 1) / chunk)), dim3(kPlanThreads), 0,
+                     st, a, (int)chunk);
   hipLaunchKernelGGL(b_medium, dim3(grid_for(r_medium, S)), dim3(256), 0, st, a);
   hipLaunchKernelGGL(b_wide, dim3(grid_for(r_wide, S)), dim3(kWideThreads), 0, st, a);
   if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;

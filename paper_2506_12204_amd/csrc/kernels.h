@@ -26,22 +26,34 @@ constexpr int kLongTile = 8192;   // requests per tile of the segmented sort
 
 // Work lists of the batched call, one per kernel.
 enum BList { kListTiny = 0, kListMedium = 1, kListWide = 2, kListLong = 3, kLists = 4 };
-constexpr int kSubLists = 8;      // per list: one grab counter per XCD
+constexpr int kSubLists = 8;      // the medium and wide lists: 8 segments each
+constexpr int kPlanChunk = 256;   // most queues the planner files per chunk
+
+// The medium and wide lists are kept in kSubLists segments: segment j holds
+// the queues of the planner's chunks c with c % kSubLists == j (and the
+// queues of those chunks handed on), so that the planner's filing atomics
+// spread over kSubLists counters. A segment holds at most ceil(S / 8) +
+// kPlanChunk queues for S queues and chunks of at most kPlanChunk.
+inline int64_t list_segment_cap(int64_t num_segments) {
+  return (num_segments + kSubLists - 1) / kSubLists + kPlanChunk;
+}
 
 // Per-call control block at the start of a batched workspace (after the
-// 64-byte flags line), followed by the grab counters.
+// 64-byte flags line), followed by the segment lines.
 struct BCtl {
-  uint32_t count[kLists];             // entries of every list
-  uint32_t empty[kLists][kSubLists];  // 1 once a sub-list was found exhausted (a hint)
+  uint32_t count[kLists];             // entries of the long list (count[kListLong])
+  uint32_t empty[kLists][kSubLists];  // 1 once a segment was found exhausted (a hint)
   uint64_t long_elems;                // requests in the long list's queues
   uint32_t ranges[4];                 // long queues: pmin, pmax, lmin, lmax
 };
-// Next batch index of one sub-list, alone in its 128-byte line: atomics on
-// one line are serialised wherever they come from, so counters that shared a
-// line would be one counter.
+// One segment of a list, alone in its 128-byte line: its entry count (the
+// planner's filing atomics) and the next batch to grab (the kernels'
+// atomics). Atomics on one line are serialised wherever they come from, so
+// counters that shared a line would be one counter.
 struct alignas(128) GrabLine {
   uint32_t next;
-  uint32_t pad[31];
+  uint32_t count;
+  uint32_t pad[30];
 };
 
 struct BArgs {
@@ -57,7 +69,10 @@ struct BArgs {
   uint32_t* flags;
   BCtl* ctl;
   GrabLine* grab;           // [kLists][kSubLists]
-  uint32_t* lists;          // [kLists][num_segments] queue indices
+  // queue indices: the medium list's kSubLists segments of seg_cap entries,
+  // the wide list's, then the long list's num_segments entries
+  uint32_t* lists;
+  int64_t seg_cap;          // list_segment_cap(num_segments)
   // segmented sort of the long queues (capacity: requests in long queues)
   uint64_t long_cap;
   uint32_t max_tiles;

@@ -286,6 +286,19 @@ def test_batched_long_and_many_small_queues():
     check_batched(p, l, off, 5, "long-and-small")
 
 
+def test_batched_medium_queues_in_one_list_segment():
+    # 2,400 queues: chunks of two queues on a 256-CU device, so the medium
+    # queues (every pair whose chunk index is a multiple of 8) all fall into
+    # one of the medium list's segments; the workgroups serving the other
+    # segments find theirs empty and must help drain that one. Some of those
+    # queues have keys too wide for a 32-bit element and are handed on.
+    sizes = [300 + (i % 7) * 500 if (i // 2) % 8 == 0 else 10 for i in range(2400)]
+    p, l, off = fuzz_segments(sizes, seed=29, classes=5, max_len=3000)
+    for q in range(0, 2400, 160):
+        l[off[q]:off[q + 1]] = np.random.default_rng(q).integers(0, 2**31 - 1, off[q + 1] - off[q])
+    check_batched(p, l, off, 5, "one-segment")
+
+
 def test_batched_many_long_queues():
     sizes = [16385 + 977 * k for k in range(24)] + [3, 0, 200000]
     p, l, off = fuzz_segments(sizes, seed=26, classes=8, max_len=100000)
