@@ -2876,7 +2876,10 @@ hipError_t launch_global_schedule(const GArgs& a, hipStream_t st, const StageEve
   mark(ev, 1, true, st);
   mark(ev, 6, false, st);
   if (a.split_mid) {
-    for (int s = 1; s < kMaxScatter - 1; ++s) {
+    // Ranks below 2^8 and lengths below 2^31 make the mixed-radix value
+    // below 2^(39 - d0), so at most (38 - d0) / 10 middle passes of 10 bits.
+    const int max_mids = (38 - a.d0) / 10;
+    for (int s = 1; s <= max_mids && s < kMaxScatter - 1; ++s) {
       hipLaunchKernelGGL(g_mid_count, dim3(a.mid.blocks), dim3(NT), 0, st, a, s);
       hipLaunchKernelGGL(g_mid_scan, dim3(kMaxBins / 4), dim3(NT), 0, st, a, s);
       hipLaunchKernelGGL(g_mid_scatter, dim3(a.mid.blocks), dim3(NT), 0, st, a, s);
