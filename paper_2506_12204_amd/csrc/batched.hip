@@ -127,6 +127,8 @@ __device__ __forceinline__ void hand_on(const BArgs& a, int L, int j, int64_t s)
 
 // ---- one queue in LDS ------------------------------------------------------------
 
+constexpr uint32_t kClsCopies = 8;  // copies of the class sums (a power of two)
+
 // LDS of a group of NW waves that schedules one queue of at most NW*64*R
 // requests with D-bit digits on elements of type ET.
 template <int NW, int R, int D, typename ET>
@@ -385,7 +387,11 @@ __device__ bool schedule_loaded(const BArgs& a, int64_t s, int64_t base, int m,
   const uint32_t kb = wl + bit_width32(pmax - pmin);
   if (kb + IDB > EBITS) return false;
   const uint32_t P = pmax - pmin + 1;
-  for (uint32_t c = t; c < P; c += NT) sh.cls[c] = 0;
+  // class sums in kClsCopies copies (lane % kClsCopies) when they fit, so that
+  // the lanes of a round that change class together spread over that many
+  // LDS addresses
+  const uint32_t K = P * kClsCopies <= 256 ? kClsCopies : 1u;
+  for (uint32_t c = t; c < P * K; c += NT) sh.cls[c] = 0;
 
   // ---- elements (past the end: all ones, the last digit of every pass; those
   // elements come last in the input, so they stay last) ---------------------------
@@ -501,7 +507,9 @@ __device__ bool schedule_loaded(const BArgs& a, int64_t s, int64_t base, int m,
       if (j < m) {
         const int cls = (int)(uint32_t)(e[r] >> cshift);  // class - pmin
         if (cls != cur) {  // a lane's positions increase, so its classes do not decrease
-          if (cur >= 0) atomicAdd(reinterpret_cast<unsigned long long*>(&sh.cls[cur]), acc);
+          if (cur >= 0)
+            atomicAdd(reinterpret_cast<unsigned long long*>(&sh.cls[cur * K + (lane & (K - 1))]),
+                      acc);
           cur = cls;
           acc = 0;
         }
@@ -509,21 +517,24 @@ __device__ bool schedule_loaded(const BArgs& a, int64_t s, int64_t base, int m,
       }
     }
   }
-  if (cur >= 0) atomicAdd(reinterpret_cast<unsigned long long*>(&sh.cls[cur]), acc);
+  if (cur >= 0)
+    atomicAdd(reinterpret_cast<unsigned long long*>(&sh.cls[cur * K + (lane & (K - 1))]), acc);
   group_sync<NW>();
 
   // ---- totals of the queue: exact, and below 2^59, so the high words are 0 ------
   const int64_t C1 = 1 + a.num_classes;
   uint64_t* tot = a.totals + 2 * s * C1;
   for (int c = t; c < a.num_classes; c += NT) {
-    const uint64_t v = ((uint32_t)c >= pmin && (uint32_t)c <= pmax) ? sh.cls[c - pmin] : 0ull;
+    uint64_t v = 0;
+    if ((uint32_t)c >= pmin && (uint32_t)c <= pmax)
+      for (uint32_t k = 0; k < K; ++k) v += sh.cls[(c - pmin) * K + k];
     tot[2 * (1 + c)] = v;
     tot[2 * (1 + c) + 1] = 0;
   }
   // the queue's total, the sum of its classes' sums, by the first wave alone
   if (w == 0) {
     uint64_t part = 0;
-    for (uint32_t c = lane; c < P; c += kWave) part += sh.cls[c];
+    for (uint32_t c = lane; c < P * K; c += kWave) part += sh.cls[c];
     part = wave_rsum_u64(part);
     if (lane == 0) {
       tot[0] = part;
