@@ -299,6 +299,17 @@ def test_batched_medium_queues_in_one_list_segment():
     check_batched(p, l, off, 5, "one-segment")
 
 
+def test_batched_more_queues_than_planner_chunks():
+    # 600,000 queues: more than the resident planner workgroups take in one
+    # chunk of 256 each, so every planner workgroup plans several chunks
+    rng = np.random.default_rng(30)
+    sizes = rng.integers(0, 4, 600_000)
+    sizes[::4999] = 300
+    sizes[7::99991] = 5000
+    p, l, off = fuzz_segments(sizes, seed=31, classes=3, max_len=2000)
+    check_batched(p, l, off, 3, "many-chunks", forms=("async",))
+
+
 def test_batched_many_long_queues():
     sizes = [16385 + 977 * k for k in range(24)] + [3, 0, 200000]
     p, l, off = fuzz_segments(sizes, seed=26, classes=8, max_len=100000)
