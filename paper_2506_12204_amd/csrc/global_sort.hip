@@ -802,12 +802,7 @@ __device__ void first_fast(const GArgs& a, int g, FirstFastShared<D0>& sh) {
         if (wb + r * kWave + lane >= cv) key[r] |= M0;
     }
 #pragma unroll
-    for (int r = 0; r < R1; ++r) {
-#if defined(SEMSCHED_FIRST_HYBRID)
-      if (r % SEMSCHED_FIRST_HYBRID == 0) { rk[r] = rank_round_c<D0>(key[r] & M0, mycnt); continue; }
-#endif
-      rk[r] = rank_round_mask(key[r] & M0, masks, mycnt);
-    }
+    for (int r = 0; r < R1; ++r) rk[r] = rank_round_mask(key[r] & M0, masks, mycnt);
   };
 
   load_first(a, pri, lo, tile_items(lo), pv, lv);
