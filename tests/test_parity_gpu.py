@@ -299,6 +299,18 @@ def test_batched_medium_queues_in_one_list_segment():
     check_batched(p, l, off, 5, "one-segment")
 
 
+@pytest.mark.parametrize("classes", [32, 33])
+def test_batched_class_sums_at_the_copy_limit(classes):
+    # the class sums of a queue are kept in eight copies while its classes
+    # span at most 32 ranks, in one copy beyond that
+    sizes = [5, 256, 257, 1000, 4096, 4097, 9000]
+    p, l, off = fuzz_segments(sizes, seed=32 + classes, classes=classes, max_len=700)
+    for q in range(len(sizes)):  # every queue spans the full range of ranks
+        p[off[q]] = 0
+        p[off[q + 1] - 1] = classes - 1
+    check_batched(p, l, off, classes, f"classes-{classes}")
+
+
 def test_batched_more_queues_than_planner_chunks():
     # 600,000 queues: more than the resident planner workgroups take in one
     # chunk of 256 each, so every planner workgroup plans several chunks
