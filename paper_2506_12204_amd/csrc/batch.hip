@@ -158,18 +158,25 @@ __device__ void block_sort(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t 
   block_sync();  // (the last pass's reads are done before callers write)
 }
 
-// Sorts the first n entries (n <= 8 * BT) of key / id (and pay).
+// Sorts the first n entries (n <= 8 * BT) of key / id (and pay), with E
+// entries per thread, the fewest of 1, 2, 4, 5, 6 or 8 that hold n (each
+// pass costs about E rounds per wave, padding included; the sort with a
+// payload keeps to 1, 2, 4 and 8, whose kernel the other widths made spill).
 template <bool PAYLOAD>
 __device__ void sort_pairs(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t n,
                            SortScratch& sc) {
   if (n <= (uint32_t)BT) block_sort<1, PAYLOAD>(key, id, pay, n, sc);
   else if (n <= 2u * BT) block_sort<2, PAYLOAD>(key, id, pay, n, sc);
   else if (n <= 4u * BT) block_sort<4, PAYLOAD>(key, id, pay, n, sc);
+  else if (!PAYLOAD && n <= 5u * BT) block_sort<5, PAYLOAD>(key, id, pay, n, sc);
+  else if (!PAYLOAD && n <= 6u * BT) block_sort<6, PAYLOAD>(key, id, pay, n, sc);
   else block_sort<8, PAYLOAD>(key, id, pay, n, sc);
 }
 
+template <bool PAYLOAD>
 __device__ __forceinline__ uint32_t sort_size(uint32_t n) {
-  return n <= (uint32_t)BT ? BT : n <= 2u * BT ? 2 * BT : n <= 4u * BT ? 4 * BT : 8 * BT;
+  return n <= (uint32_t)BT ? BT : n <= 2u * BT ? 2 * BT : n <= 4u * BT ? 4 * BT
+         : !PAYLOAD && n <= 5u * BT ? 5 * BT : !PAYLOAD && n <= 6u * BT ? 6 * BT : 8 * BT;
 }
 
 // Number of entries of a sorted list below (k, i).
@@ -266,7 +273,7 @@ __global__ __launch_bounds__(BT) void b_select(SelArgs a) {
   const uint32_t nh = (uint32_t)min(a.b, a.n_heap);
   const uint32_t nc_in = nh + (uint32_t)a.n_buffer;
   const uint32_t no = (uint32_t)a.n_ongoing;
-  const uint32_t NC = sort_size(nc_in), NO = sort_size(no);
+  const uint32_t NC = sort_size<false>(nc_in), NO = sort_size<false>(no);
   if (t == 0) sh.bad = 0;
   block_sync();
   // gather the keys; ids outside [0, n_ids) are reported and sort last
@@ -394,7 +401,7 @@ __global__ __launch_bounds__(BT) void b_evict(EvictArgs a) {
   __shared__ EvictShared sh;
   const uint32_t t = threadIdx.x;
   const uint32_t nr = (uint32_t)a.n_cached;
-  const uint32_t N = sort_size(nr);
+  const uint32_t N = sort_size<true>(nr);
   if (t == 0) sh.bad = 0;
   block_sync();
   for (uint32_t i = t; i < N; i += BT) {
