@@ -99,14 +99,47 @@ __device__ void block_sort(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t 
   }
   block_sync();  // (the partials' words are the scans' scratch below)
   const uint64_t kor = (uint64_t)kor_hi << 32 | kor_lo;
-  const uint64_t kvary = kor ^ ((uint64_t)kand_hi << 32 | kand_lo);
-  const uint32_t ivary = ior ^ iand;
+  uint64_t kvary = kor ^ ((uint64_t)kand_hi << 32 | kand_lo);
+  uint32_t ivary = ior ^ iand;
 #pragma unroll
   for (int r = 0; r < E; ++r) {
     if (at(r) >= n) {
       xk[r] = kor;
       xi[r] = ior;
     }
+  }
+  // Packed form: the spans of varying bits of the id, the key's low word and
+  // its high word, laid end to end in one u64 (id lowest), when they fit. Its
+  // order is the order by (key, id), and its bytes take the passes, in place
+  // of the id's and the key's varying bytes (41 bits and 6 passes against 7
+  // bytes for ids of 26 bits, lengths of 12 and ranks of 3). The key array
+  // then carries the packed value, and the keys are rebuilt from it (and the
+  // bits that do not vary) after the last pass.
+  const uint32_t v0 = ivary, v1 = (uint32_t)kvary, v2 = (uint32_t)(kvary >> 32);
+  const uint32_t l0 = v0 ? __builtin_ctz(v0) : 0, w0 = v0 ? 32 - __builtin_clz(v0) - l0 : 0;
+  const uint32_t l1 = v1 ? __builtin_ctz(v1) : 0, w1 = v1 ? 32 - __builtin_clz(v1) - l1 : 0;
+  const uint32_t l2 = v2 ? __builtin_ctz(v2) : 0, w2 = v2 ? 32 - __builtin_clz(v2) - l2 : 0;
+  const uint32_t pbits = w0 + w1 + w2;
+  auto low_mask = [](uint32_t wd) { return wd >= 32 ? ~0u : (1u << wd) - 1u; };
+  const uint32_t m0 = low_mask(w0), m1 = low_mask(w1), m2 = low_mask(w2);
+  uint32_t vbytes = 0;  // passes of the byte form
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+    vbytes += ((v0 >> (8 * b)) & 0xffu ? 1u : 0u) + ((v1 >> (8 * b)) & 0xffu ? 1u : 0u) +
+              ((v2 >> (8 * b)) & 0xffu ? 1u : 0u);
+  const bool packed = pbits <= 64 && (pbits + 7) / 8 < vbytes;
+  const uint32_t s2 = w0 + w1;  // below 64 when the high word's span is not empty
+  bool packed_moved = false;  // the key array holds packed values
+  if (packed) {
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+      const uint64_t f0 = (xi[r] >> l0) & m0;
+      const uint64_t f1 = ((uint32_t)xk[r] >> l1) & m1;
+      const uint64_t f2 = ((uint32_t)(xk[r] >> 32) >> l2) & m2;
+      xk[r] = f0 | (f1 << w0) | (w2 ? f2 << s2 : 0ull);
+    }
+    kvary = pbits >= 64 ? ~0ull : (1ull << pbits) - 1;
+    ivary = 0;
   }
   uint16_t* mycnt = sc.cnt[w];
   for (int pass = 0; pass < 12; ++pass) {
@@ -146,6 +179,7 @@ __device__ void block_sort(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t 
       id[q] = xi[r];
       if (PAYLOAD) pay[q] = xp[r];
     }
+    packed_moved = packed;
     block_sync();  // the pass is scattered
 #pragma unroll
     for (int r = 0; r < E; ++r) {
@@ -153,6 +187,15 @@ __device__ void block_sort(uint64_t* key, uint32_t* id, uint32_t* pay, uint32_t 
       xk[r] = key[i];
       xi[r] = id[i];
       if (PAYLOAD) xp[r] = pay[i];
+    }
+  }
+  if (packed_moved) {  // (uniform) the keys back from the packed values
+    const uint32_t keep_lo = kand_lo & ~(m1 << l1), keep_hi = kand_hi & ~(m2 << l2);
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+      const uint32_t f1 = (uint32_t)(xk[r] >> w0) & m1;
+      const uint32_t f2 = w2 ? (uint32_t)(xk[r] >> s2) & m2 : 0u;
+      key[at(r)] = (uint64_t)(keep_hi | (f2 << l2)) << 32 | (keep_lo | (f1 << l1));
     }
   }
   block_sync();  // (the last pass's reads are done before callers write)

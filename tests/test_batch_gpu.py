@@ -235,3 +235,37 @@ def test_full_range_keys_and_ids():
                     usage, usage // 3, dev(demands, np.int64))
     assert v.cpu().numpy().tolist() == want_v
     assert u.cpu().numpy().tolist() == want_u
+
+
+def test_packed_key_spans():
+    # keys whose varying bits fit one u64 once packed (the sorts' packed form):
+    # lengths 2^20 + [0, 5000) and ranks 64 + [0, 6) (constant bits above
+    # the spans of both words, which the keys get back after the passes), ids
+    # that are multiples of 16 (a span starting at bit 4), ties on the key
+    import paper_2506_12204_amd as ss
+    rng = np.random.default_rng(78)
+    n_ids = 1 << 22
+    p = np.full(n_ids, 64, np.uint8)
+    l = np.full(n_ids, 1 << 20, np.int32)
+    ids = (16 * rng.choice(n_ids // 16, 4096 * 3 + 8192, replace=False)).astype(np.int32)
+    p[ids] = 64 + rng.integers(0, 6, ids.size)
+    l[ids] = (1 << 20) + rng.integers(0, 5000, ids.size)
+    l[ids[:300]] = (1 << 20) + 77  # ties on (rank, length) across ids
+    p[ids[:300]] = 65
+    stage = (rng.random(n_ids) < 0.5).astype(np.uint8)
+    waiting = ids[:4096]
+    heap = waiting[np.lexsort((waiting, l[waiting], p[waiting]))]
+    buf, ong = ids[4096:8192], ids[8192:12288]
+    print("[gpu] select, packed key spans", flush=True)
+    want = select_batch(p, l, stage, heap.tolist(), buf.tolist(), ong.tolist(), 4096)
+    assert run_select(p, l, stage, heap, buf, ong, 4096) == want
+    cached = ids[-8192:]
+    kv = rng.integers(0, 1 << 20, cached.size).astype(np.int64)
+    demands = rng.integers(0, 1 << 24, 500).astype(np.int64)
+    usage = int(kv.sum())
+    print("[gpu] evict, packed key spans", flush=True)
+    want_v, want_u = evict(p, l, cached.tolist(), kv.tolist(), usage, usage // 3, demands.tolist())
+    v, u = ss.evict(dev(p, np.uint8), dev(l, np.int32), dev(cached, np.int32), dev(kv, np.int64),
+                    usage, usage // 3, dev(demands, np.int64))
+    assert v.cpu().numpy().tolist() == want_v
+    assert u.cpu().numpy().tolist() == want_u
