@@ -799,7 +799,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   // ---- phase 0: queue starts and first tiles (workgroup 0); zero the totals --------
   if (blockIdx.x == 0) {
     uint64_t carry_e = 0;
-    uint32_t carry_t = 0;
+    uint32_t carry_t = 0, carry_i = 0;
     for (uint32_t k0 = 0; k0 < K; k0 += kLT) {
       const uint32_t k = k0 + t;
       uint64_t m = 0;
@@ -808,20 +808,25 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
         m = (uint64_t)(a.offsets[s + 1] - a.offsets[s]);
       }
       const uint32_t tiles = (uint32_t)((m + kLongTile - 1) / kLongTile);
+      const uint32_t items = k < K ? (tiles <= kLongRowsFew ? 1u : 256u) : 0u;
       uint64_t tot_e;
-      uint32_t tot_t;
+      uint32_t tot_t, tot_i;
       const uint64_t ex_e = block_excl_scan_u64<kLT>(m, sh.part, tot_e);
       const uint32_t ex_t = block_excl_scan_u32<kLT>(tiles, sh.part32, tot_t);
+      const uint32_t ex_i = block_excl_scan_u32<kLT>(items, sh.part32, tot_i);
       if (k < K) {
         a.lbase[k] = carry_e + ex_e;
         a.tstart[k] = carry_t + ex_t;
+        a.istart[k] = carry_i + ex_i;
       }
       carry_e += tot_e;
       carry_t += tot_t;
+      carry_i += tot_i;
     }
     if (t == 0) {
       a.lbase[K] = carry_e;
       a.tstart[K] = carry_t;
+      a.istart[K] = carry_i;
       if (carry_t > a.max_tiles) atomicOr(a.flags, kFlagInval);  // (cannot happen)
       a.ctl->ranges[0] = 0xffu;
       a.ctl->ranges[1] = 0;
@@ -836,19 +841,25 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   }
   grid.sync();
   const uint32_t ntiles = a.tstart[K];
+  const uint32_t nitems = a.istart[K];
 
   // ---- phase R: ranges and validation of all long queues --------------------------
-  for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
-    const LongTile x = long_tile(a, tt, K);
+  // Reduced over the workgroup's tiles first, then one atomic per range word
+  // and workgroup, skipped when it would not change the word: atomics on one
+  // line serialise, and one per wave and tile queued thousands on it.
+  {
     uint32_t lmin = 0xffffffffu, lmax = 0, pmin = 0xffu, pmax = 0, bad = 0;
-    for (int i = t; i < x.cnt; i += kLT) {
-      const uint32_t p = a.priority[x.base + x.lo + i];
-      const int32_t l = a.length[x.base + x.lo + i];
-      bad |= (l < 0) | ((int)p >= a.num_classes);
-      lmin = min(lmin, (uint32_t)l);
-      lmax = max(lmax, (uint32_t)l);
-      pmin = min(pmin, p);
-      pmax = max(pmax, p);
+    for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+      const LongTile x = long_tile(a, tt, K);
+      for (int i = t; i < x.cnt; i += kLT) {
+        const uint32_t p = a.priority[x.base + x.lo + i];
+        const int32_t l = a.length[x.base + x.lo + i];
+        bad |= (l < 0) | ((int)p >= a.num_classes);
+        lmin = min(lmin, (uint32_t)l);
+        lmax = max(lmax, (uint32_t)l);
+        pmin = min(pmin, p);
+        pmax = max(pmax, p);
+      }
     }
     lmin = wave_min_u32(lmin);
     lmax = wave_max_u32(lmax);
@@ -857,10 +868,24 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     bad = wave_or_u32(bad);
     if (lane == 0) {
       if (bad) atomicOr(a.flags, kFlagRange);
-      atomicMin(&a.ctl->ranges[0], pmin);
-      atomicMax(&a.ctl->ranges[1], pmax);
-      atomicMin(&a.ctl->ranges[2], lmin);
-      atomicMax(&a.ctl->ranges[3], lmax);
+      sh.red[0][w] = pmin;
+      sh.red[1][w] = pmax;
+      sh.red[2][w] = lmin;
+      sh.red[3][w] = lmax;
+    }
+    block_sync();
+    if (t == 0) {
+      for (int v = 1; v < kLW; ++v) {
+        pmin = min(pmin, sh.red[0][v]);
+        pmax = max(pmax, sh.red[1][v]);
+        lmin = min(lmin, sh.red[2][v]);
+        lmax = max(lmax, sh.red[3][v]);
+      }
+      uint32_t* rg = a.ctl->ranges;
+      if (pmin < load_agent(rg + 0)) atomicMin(rg + 0, pmin);
+      if (pmax > load_agent(rg + 1)) atomicMax(rg + 1, pmax);
+      if (lmin < load_agent(rg + 2)) atomicMin(rg + 2, lmin);
+      if (lmax > load_agent(rg + 3)) atomicMax(rg + 3, lmax);
     }
   }
   grid.sync();
@@ -928,19 +953,44 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     }
     grid.sync();
     // ---- phase B: per queue and digit, offsets over the queue's tiles ----------------
-    for (uint32_t k = blockIdx.x; k < K; k += gridDim.x) {
+    // A queue of few tiles is one work item: thread d runs down digit d's
+    // column and the digit bases are added at once. A queue of many tiles is
+    // 256 items, one per digit, each a block scan down its column in rows of
+    // kLT tiles; its digit totals go to qtot and the digit bases are added
+    // by the scatter (phase C).
+    for (uint32_t it = blockIdx.x; it < nitems; it += gridDim.x) {
+      uint32_t k = 0, hi = K;  // istart[k] <= it < istart[k + 1]
+      while (hi - k > 1) {
+        const uint32_t mid = (k + hi) / 2;
+        if (a.istart[mid] <= it) k = mid;
+        else hi = mid;
+      }
       const uint32_t r0 = a.tstart[k], r1 = a.tstart[k + 1];
-      uint32_t tot = 0;
-      if (t < 256)
-        for (uint32_t row = r0; row < r1; ++row) tot += a.hist[(size_t)row * 256 + t];
-      uint32_t total;
-      uint32_t run = block_excl_scan_u32<kLT>(t < 256 ? tot : 0u, sh.part32, total);
-      if (t < 256)
-        for (uint32_t row = r0; row < r1; ++row) {
-          const uint32_t c = a.hist[(size_t)row * 256 + t];
-          a.hist[(size_t)row * 256 + t] = run;
-          run += c;
+      if (r1 - r0 <= kLongRowsFew) {
+        uint32_t tot = 0;
+        if (t < 256)
+          for (uint32_t row = r0; row < r1; ++row) tot += a.hist[(size_t)row * 256 + t];
+        uint32_t total;
+        uint32_t run = block_excl_scan_u32<kLT>(t < 256 ? tot : 0u, sh.part32, total);
+        if (t < 256)
+          for (uint32_t row = r0; row < r1; ++row) {
+            const uint32_t c = a.hist[(size_t)row * 256 + t];
+            a.hist[(size_t)row * 256 + t] = run;
+            run += c;
+          }
+      } else {
+        const uint32_t d = it - a.istart[k];
+        uint32_t carry = 0;
+        for (uint32_t row0 = r0; row0 < r1; row0 += kLT) {
+          const uint32_t row = row0 + t;
+          const uint32_t c = row < r1 ? a.hist[(size_t)row * 256 + d] : 0u;
+          uint32_t total;
+          const uint32_t ex = block_excl_scan_u32<kLT>(c, sh.part32, total);
+          if (row < r1) a.hist[(size_t)row * 256 + d] = carry + ex;
+          carry += total;
         }
+        if (t == 0) a.qtot[it] = carry;
+      }
     }
     grid.sync();
     // ---- phase C: stable scatter of every tile ----------------------------------------
@@ -949,7 +999,13 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       uint64_t key[kLR];
       uint32_t id[kLR], dg[kLR], rk[kLR];
       load_elems(x, q, key, id);
-      if (t < 256) sh.hrow[t] = a.hist[(size_t)tt * 256 + t];
+      uint32_t dbase = 0;  // queues of many tiles: the digit's base in the queue
+      if (a.tstart[x.k + 1] - a.tstart[x.k] > kLongRowsFew) {  // (uniform)
+        const uint32_t c = t < 256 ? a.qtot[a.istart[x.k] + t] : 0u;
+        uint32_t total;
+        dbase = block_excl_scan_u32<kLT>(c, sh.part32, total);
+      }
+      if (t < 256) sh.hrow[t] = a.hist[(size_t)tt * 256 + t] + dbase;
       clear_counters<256>(sh.cnt[w]);
 #pragma unroll
       for (int r = 0; r < kLR; ++r) {
@@ -1018,11 +1074,35 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     }
   }
   grid.sync();
-  // phase D3: order, waits and class totals of every tile
+  // phase D3: order, waits and class totals of every tile. The class sums
+  // of the workgroup's consecutive tiles of one queue add up in LDS and go
+  // to the queue's totals when the queue changes and at the end (one atomic
+  // per class and one for the total at each such flush).
   const uint32_t P = pmax - pmin + 1;
+  int64_t cur_s = -1;  // (uniform) the queue whose sums the LDS totals hold
+  auto flush = [&]() {
+    block_sync();  // every lane's sums are in
+    uint64_t* tot = a.totals + 2 * cur_s * C1;
+    for (uint32_t c = t; c < P; c += kLT) {
+      const U128 v = {sh.clo[c], sh.chi[c]};
+      if (v.lo | v.hi) atomic_add128(tot + 2 * (1 + pmin + c), tot + 2 * (1 + pmin + c) + 1, v);
+    }
+    if (t == 0) {
+      U128 g = {0, 0};
+      for (uint32_t c = 0; c < P; ++c) add128(g, U128{sh.clo[c], sh.chi[c]});
+      if (g.lo | g.hi) atomic_add128(tot, tot + 1, g);
+    }
+    block_sync();  // the sums are read
+    for (uint32_t c = t; c < P; c += kLT) sh.clo[c] = sh.chi[c] = 0;
+  };
+  for (uint32_t c = t; c < P; c += kLT) sh.clo[c] = sh.chi[c] = 0;
   for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
     const LongTile x = long_tile(a, tt, K);
-    for (uint32_t c = t; c < P; c += kLT) sh.clo[c] = sh.chi[c] = 0;
+    if (x.s != cur_s) {  // (uniform)
+      if (cur_s >= 0) flush();
+      cur_s = x.s;
+    }
+    block_sync();  // the totals are cleared
     uint32_t len[kLR];
     uint64_t key[kLR];
     uint32_t id[kLR];
@@ -1068,17 +1148,9 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       }
     }
     if (cur >= 0) atomic_add128(&sh.clo[cur], &sh.chi[cur], acc);
-    block_sync();
-    uint64_t* tot = a.totals + 2 * x.s * C1;
-    for (uint32_t c = t; c < P; c += kLT) {
-      const U128 v = {sh.clo[c], sh.chi[c]};
-      if (v.lo | v.hi) {
-        atomic_add128(tot + 2 * (1 + pmin + c), tot + 2 * (1 + pmin + c) + 1, v);
-        atomic_add128(tot, tot + 1, v);
-      }
-    }
-    block_sync();
+    block_sync();  // (sh.part is read; the next tile writes it)
   }
+  if (cur_s >= 0) flush();  // (uniform)
 }
 
 // ---- host side -------------------------------------------------------------------

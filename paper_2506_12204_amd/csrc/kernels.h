@@ -82,6 +82,8 @@ struct BArgs {
   uint64_t* tsum;           // [max_tiles] length sums, then wait bases
   uint64_t* lbase;          // [long list + 1] start of every long queue in keys/ids
   uint32_t* tstart;         // [long list + 1] first tile of every long queue
+  uint32_t* istart;         // [long list + 1] first digit-offset work item of every long queue
+  uint32_t* qtot;           // [long_items_max] digit totals of the queues of many tiles
 };
 
 // Single queue of a.n_single <= kSegLargeCap requests (a.offsets null), one
@@ -93,6 +95,13 @@ hipError_t launch_batched(const BArgs& a, hipStream_t st);
 // Workspace parts of the segmented sort for `long_cap` requests in long
 // queues out of num_segments queues.
 uint32_t long_max_tiles(uint64_t long_cap, int64_t num_segments);
+// A long queue of at most kLongRowsFew tiles takes its digit offsets in one
+// work item; a longer one in 256, one per digit (over its tiles in parallel).
+constexpr uint32_t kLongRowsFew = 32;
+// Most digit-offset work items of the long queues (and entries of qtot).
+inline uint64_t long_items_max(uint64_t long_cap, int64_t queues) {
+  return (uint64_t)queues + 256 * (long_cap / ((uint64_t)kLongRowsFew * kLongTile) + 1);
+}
 
 // ---------------------------------------------------------------------------
 // Global multi-pass path (one queue longer than kSegLargeCap).
