@@ -904,7 +904,9 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   const uint64_t lmask = wl ? ((1ull << wl) - 1) : 0;
 
   // element r of this thread in tile x: request x.lo + w*64*kLR + r*64 + lane
-  auto load_elems = [&](const LongTile& x, int q, uint64_t (&key)[kLR], uint32_t (&id)[kLR]) {
+  // (with_ids false: the ids are not read, for the counting phase)
+  auto load_elems = [&](const LongTile& x, int q, uint64_t (&key)[kLR], uint32_t (&id)[kLR],
+                        bool with_ids) {
 #pragma unroll
     for (int r = 0; r < kLR; ++r) {
       const int i = w * kWave * kLR + r * kWave + lane;
@@ -919,7 +921,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
         } else {
           const uint64_t at = a.lbase[x.k] + (uint64_t)(x.lo + i);
           key[r] = a.keys[(q - 1) & 1][at];
-          id[r] = a.ids[(q - 1) & 1][at];
+          if (with_ids) id[r] = a.ids[(q - 1) & 1][at];
         }
       }
     }
@@ -932,7 +934,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       const LongTile x = long_tile(a, tt, K);
       uint64_t key[kLR];
       uint32_t id[kLR];
-      load_elems(x, q, key, id);
+      load_elems(x, q, key, id, false);
       clear_counters<256>(sh.cnt[w]);
 #pragma unroll
       for (int r = 0; r < kLR; ++r) {
@@ -998,7 +1000,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       const LongTile x = long_tile(a, tt, K);
       uint64_t key[kLR];
       uint32_t id[kLR], dg[kLR], rk[kLR];
-      load_elems(x, q, key, id);
+      load_elems(x, q, key, id, true);
       uint32_t dbase = 0;  // queues of many tiles: the digit's base in the queue
       if (a.tstart[x.k + 1] - a.tstart[x.k] > kLongRowsFew) {  // (uniform)
         const uint32_t c = t < 256 ? a.qtot[a.istart[x.k] + t] : 0u;
