@@ -597,7 +597,7 @@ BLayout batched_layout(int64_t S, uint64_t long_cap) {
     L.keys1 = take(8 * long_cap);
     L.ids0 = take(4 * long_cap);
     L.ids1 = take(4 * long_cap);
-    L.hist = take(4 * 256 * (size_t)L.max_tiles);
+    L.hist = take(4 * ((size_t)1 << kLongDigitBits) * (size_t)L.max_tiles);
     L.tsum = take(8 * (size_t)L.max_tiles);
     L.lbase = take(8 * (size_t)(queues + 1));
     L.tstart = take(4 * (size_t)(queues + 1));

@@ -737,7 +737,7 @@ __global__ __launch_bounds__(kWideThreads) void b_wide(BArgs a) {
 // kLongTile requests (a tile never spans two queues); the key of a request is
 // (priority - pmin) << wl | (length - lmin) with the ranges of all long
 // queues together, and the queue a tile belongs to is not part of the key:
-// digit offsets are scanned per queue over its own tiles. Per 8-bit digit
+// digit offsets are scanned per queue over its own tiles. Per 10-bit digit
 // pass: count every tile's digits, scan the counts per queue and digit over
 // the queue's tiles (plus the queue's digit bases), scatter every tile
 // stably. Then the waits: every tile's length sum, the exclusive scan of
@@ -747,10 +747,20 @@ __global__ __launch_bounds__(kWideThreads) void b_wide(BArgs a) {
 constexpr int kLT = 512;
 constexpr int kLW = kLT / kWave;
 constexpr int kLR = kLongTile / kLT;  // rounds per thread
+constexpr int kLB = 1 << kLongDigitBits;  // digits of a pass
+constexpr int kLO = kLB / kLT;            // digits per thread (consecutive)
 
 struct LongLds {
-  uint16_t cnt[kLW][256];
-  uint32_t hrow[256];
+  uint16_t cnt[kLW][kLB];
+  uint32_t hrow[kLB];
+  uint32_t dstart[kLB];  // start of each digit's run in the staged tile
+  union {
+    struct {  // the scatter's tile, staged in digit order
+      uint64_t key[kLongTile];
+      uint32_t id[kLongTile];
+    } st;
+    uint32_t acnt[kLW][kLB];  // the counting phase's per-wave counts
+  } u;
   uint64_t clo[256], chi[256];
   uint64_t part[kLW + 1];
   uint32_t part32[kLW + 1];
@@ -808,7 +818,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
         m = (uint64_t)(a.offsets[s + 1] - a.offsets[s]);
       }
       const uint32_t tiles = (uint32_t)((m + kLongTile - 1) / kLongTile);
-      const uint32_t items = k < K ? (tiles <= kLongRowsFew ? 1u : 256u) : 0u;
+      const uint32_t items = k < K ? (tiles <= kLongRowsFew ? 1u : (uint32_t)kLB) : 0u;
       uint64_t tot_e;
       uint32_t tot_t, tot_i;
       const uint64_t ex_e = block_excl_scan_u64<kLT>(m, sh.part, tot_e);
@@ -900,7 +910,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   const uint32_t lmin = range(2), lmax = range(3);
   const uint32_t wl = bit_width32(lmax - lmin);
   const uint32_t kb = wl + bit_width32(pmax - pmin);
-  const int npass = kb ? (int)((kb + 7) / 8) : 1;
+  const int npass = kb ? (int)((kb + kLongDigitBits - 1) / kLongDigitBits) : 1;
   const uint64_t lmask = wl ? ((1ull << wl) - 1) : 0;
 
   // element r of this thread in tile x: request x.lo + w*64*kLR + r*64 + lane
@@ -928,38 +938,39 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   };
 
   for (int q = 0; q < npass; ++q) {
-    const uint32_t shift = 8 * q;
+    const uint32_t shift = kLongDigitBits * q;
     // ---- phase A: digit counts of every tile ----------------------------------------
     for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
       const LongTile x = long_tile(a, tt, K);
       uint64_t key[kLR];
       uint32_t id[kLR];
       load_elems(x, q, key, id, false);
-      clear_counters<256>(sh.cnt[w]);
+      // (counts only: one LDS add per request into the wave's own table)
+      uint32_t* mine = sh.u.acnt[w];
+      for (int b = lane; b < kLB; b += kWave) mine[b] = 0;
 #pragma unroll
       for (int r = 0; r < kLR; ++r) {
         const int i = w * kWave * kLR + r * kWave + lane;
-        // past the end: digit 255 counted, then taken off below
-        (void)rank_round_c<8>((uint32_t)(key[r] >> shift) & 255u, sh.cnt[w]);
-        (void)i;
+        if (i < x.cnt) atomicAdd(&mine[(uint32_t)(key[r] >> shift) & (kLB - 1)], 1u);
       }
       block_sync();
-      if (t < 256) {
+#pragma unroll
+      for (int o = 0; o < kLO; ++o) {
+        const int d = kLO * t + o;
         uint32_t c = 0;
 #pragma unroll
-        for (int v = 0; v < kLW; ++v) c += sh.cnt[v][t];
-        if (t == 255) c -= (uint32_t)(kLongTile - x.cnt);
-        a.hist[(size_t)tt * 256 + t] = c;
+        for (int v = 0; v < kLW; ++v) c += sh.u.acnt[v][d];
+        a.hist[(size_t)tt * kLB + d] = c;
       }
       block_sync();
     }
     grid.sync();
     // ---- phase B: per queue and digit, offsets over the queue's tiles ----------------
-    // A queue of few tiles is one work item: thread d runs down digit d's
-    // column and the digit bases are added at once. A queue of many tiles is
-    // 256 items, one per digit, each a block scan down its column in rows of
-    // kLT tiles; its digit totals go to qtot and the digit bases are added
-    // by the scatter (phase C).
+    // A queue of few tiles is one work item: each thread runs down the
+    // columns of its kLO digits and the digit bases are added at once. A
+    // queue of many tiles is kLB items, one per digit, each a block scan down
+    // its column in rows of kLT tiles; its digit totals go to qtot and the
+    // digit bases are added by the scatter (phase C).
     for (uint32_t it = blockIdx.x; it < nitems; it += gridDim.x) {
       uint32_t k = 0, hi = K;  // istart[k] <= it < istart[k + 1]
       while (hi - k > 1) {
@@ -969,26 +980,36 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       }
       const uint32_t r0 = a.tstart[k], r1 = a.tstart[k + 1];
       if (r1 - r0 <= kLongRowsFew) {
-        uint32_t tot = 0;
-        if (t < 256)
-          for (uint32_t row = r0; row < r1; ++row) tot += a.hist[(size_t)row * 256 + t];
+        uint32_t tot[kLO], sum = 0;
+#pragma unroll
+        for (int o = 0; o < kLO; ++o) {
+          tot[o] = 0;
+          for (uint32_t row = r0; row < r1; ++row)
+            tot[o] += a.hist[(size_t)row * kLB + kLO * t + o];
+          sum += tot[o];
+        }
         uint32_t total;
-        uint32_t run = block_excl_scan_u32<kLT>(t < 256 ? tot : 0u, sh.part32, total);
-        if (t < 256)
+        uint32_t run = block_excl_scan_u32<kLT>(sum, sh.part32, total);
+#pragma unroll
+        for (int o = 0; o < kLO; ++o) {
+          uint32_t r = run;
           for (uint32_t row = r0; row < r1; ++row) {
-            const uint32_t c = a.hist[(size_t)row * 256 + t];
-            a.hist[(size_t)row * 256 + t] = run;
-            run += c;
+            uint32_t* h = a.hist + (size_t)row * kLB + kLO * t + o;
+            const uint32_t c = *h;
+            *h = r;
+            r += c;
           }
+          run += tot[o];
+        }
       } else {
         const uint32_t d = it - a.istart[k];
         uint32_t carry = 0;
         for (uint32_t row0 = r0; row0 < r1; row0 += kLT) {
           const uint32_t row = row0 + t;
-          const uint32_t c = row < r1 ? a.hist[(size_t)row * 256 + d] : 0u;
+          const uint32_t c = row < r1 ? a.hist[(size_t)row * kLB + d] : 0u;
           uint32_t total;
           const uint32_t ex = block_excl_scan_u32<kLT>(c, sh.part32, total);
-          if (row < r1) a.hist[(size_t)row * 256 + d] = carry + ex;
+          if (row < r1) a.hist[(size_t)row * kLB + d] = carry + ex;
           carry += total;
         }
         if (t == 0) a.qtot[it] = carry;
@@ -1001,41 +1022,78 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       uint64_t key[kLR];
       uint32_t id[kLR], dg[kLR], rk[kLR];
       load_elems(x, q, key, id, true);
-      uint32_t dbase = 0;  // queues of many tiles: the digit's base in the queue
+      uint32_t dbase[kLO] = {};  // queues of many tiles: the digits' bases in the queue
       if (a.tstart[x.k + 1] - a.tstart[x.k] > kLongRowsFew) {  // (uniform)
-        const uint32_t c = t < 256 ? a.qtot[a.istart[x.k] + t] : 0u;
+        uint32_t c[kLO], sum = 0;
+#pragma unroll
+        for (int o = 0; o < kLO; ++o) {
+          c[o] = a.qtot[a.istart[x.k] + kLO * t + o];
+          sum += c[o];
+        }
         uint32_t total;
-        dbase = block_excl_scan_u32<kLT>(c, sh.part32, total);
+        uint32_t run = block_excl_scan_u32<kLT>(sum, sh.part32, total);
+#pragma unroll
+        for (int o = 0; o < kLO; ++o) {
+          dbase[o] = run;
+          run += c[o];
+        }
       }
-      if (t < 256) sh.hrow[t] = a.hist[(size_t)tt * 256 + t] + dbase;
-      clear_counters<256>(sh.cnt[w]);
+#pragma unroll
+      for (int o = 0; o < kLO; ++o)
+        sh.hrow[kLO * t + o] = a.hist[(size_t)tt * kLB + kLO * t + o] + dbase[o];
+      clear_counters<kLB>(sh.cnt[w]);
 #pragma unroll
       for (int r = 0; r < kLR; ++r) {
-        dg[r] = (uint32_t)(key[r] >> shift) & 255u;
-        rk[r] = rank_round_c<8>(dg[r], sh.cnt[w]);
+        dg[r] = (uint32_t)(key[r] >> shift) & (kLB - 1);
+        rk[r] = rank_round_c<kLongDigitBits>(dg[r], sh.cnt[w]);
       }
       block_sync();
-      if (t < 256) {
+      // owners: the waves' offsets within each digit, then the digits'
+      // starts in the tile (elements past the end count in the last digit
+      // and rank after its real ones, so they shift no real position)
+      uint32_t tot[kLO], sum = 0;
+#pragma unroll
+      for (int o = 0; o < kLO; ++o) {
+        const int d = kLO * t + o;
         uint32_t run = 0;
 #pragma unroll
         for (int v = 0; v < kLW; ++v) {
-          const uint32_t c = sh.cnt[v][t];
-          sh.cnt[v][t] = (uint16_t)run;
+          const uint32_t c = sh.cnt[v][d];
+          sh.cnt[v][d] = (uint16_t)run;
           run += c;
+        }
+        tot[o] = run;
+        sum += run;
+      }
+      {
+        uint32_t total;
+        uint32_t st = block_excl_scan_u32<kLT>(sum, sh.part32, total);  // (barriers)
+#pragma unroll
+        for (int o = 0; o < kLO; ++o) {
+          sh.dstart[kLO * t + o] = st;
+          st += tot[o];
+        }
+      }
+      block_sync();
+      // stage the tile in digit order, then write it out in runs per digit
+#pragma unroll
+      for (int r = 0; r < kLR; ++r) {
+        const int i = w * kWave * kLR + r * kWave + lane;
+        if (i < x.cnt) {
+          const uint32_t j = sh.dstart[dg[r]] + sh.cnt[w][dg[r]] + rk[r];
+          sh.u.st.key[j] = key[r];
+          sh.u.st.id[j] = id[r];
         }
       }
       block_sync();
       uint64_t* kout = a.keys[q & 1];
       uint32_t* iout = a.ids[q & 1];
-#pragma unroll
-      for (int r = 0; r < kLR; ++r) {
-        const int i = w * kWave * kLR + r * kWave + lane;
-        if (i < x.cnt) {
-          const uint64_t at =
-              a.lbase[x.k] + sh.hrow[dg[r]] + sh.cnt[w][dg[r]] + rk[r];
-          kout[at] = key[r];
-          iout[at] = id[r];
-        }
+      for (int j = t; j < x.cnt; j += kLT) {
+        const uint64_t k = sh.u.st.key[j];
+        const uint32_t d = (uint32_t)(k >> shift) & (kLB - 1);
+        const uint64_t at = a.lbase[x.k] + sh.hrow[d] + (uint32_t)(j - (int)sh.dstart[d]);
+        kout[at] = k;
+        iout[at] = sh.u.st.id[j];
       }
       block_sync();
     }

@@ -78,7 +78,7 @@ struct BArgs {
   uint32_t max_tiles;
   uint64_t* keys[2];        // [long_cap]
   uint32_t* ids[2];         // [long_cap]
-  uint32_t* hist;           // [max_tiles][256] digit counts, then offsets
+  uint32_t* hist;           // [max_tiles][2^kLongDigitBits] digit counts, then offsets
   uint64_t* tsum;           // [max_tiles] length sums, then wait bases
   uint64_t* lbase;          // [long list + 1] start of every long queue in keys/ids
   uint32_t* tstart;         // [long list + 1] first tile of every long queue
@@ -95,12 +95,15 @@ hipError_t launch_batched(const BArgs& a, hipStream_t st);
 // Workspace parts of the segmented sort for `long_cap` requests in long
 // queues out of num_segments queues.
 uint32_t long_max_tiles(uint64_t long_cap, int64_t num_segments);
+// Digits of a pass of the segmented sort of the long queues.
+constexpr int kLongDigitBits = 10;
 // A long queue of at most kLongRowsFew tiles takes its digit offsets in one
-// work item; a longer one in 256, one per digit (over its tiles in parallel).
+// work item; a longer one in one per digit (over its tiles in parallel).
 constexpr uint32_t kLongRowsFew = 32;
 // Most digit-offset work items of the long queues (and entries of qtot).
 inline uint64_t long_items_max(uint64_t long_cap, int64_t queues) {
-  return (uint64_t)queues + 256 * (long_cap / ((uint64_t)kLongRowsFew * kLongTile) + 1);
+  return (uint64_t)queues +
+         (1u << kLongDigitBits) * (long_cap / ((uint64_t)kLongRowsFew * kLongTile) + 1);
 }
 
 // ---------------------------------------------------------------------------
