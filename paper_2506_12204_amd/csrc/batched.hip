@@ -767,28 +767,35 @@ struct LongLds {
   uint32_t red[4][kLW];
 };
 
-// Tile t of the long queues: its list entry k (binary search over the first
-// tiles of the K queues), queue s, the queue's first request `base` and
-// size m, the tile's first request within the queue `lo` and its size.
-struct LongTile {
-  int64_t k, s, base, m, lo;
-  int cnt;
-};
-
-__device__ LongTile long_tile(const BArgs& a, uint32_t t, uint32_t K) {
-  uint32_t lo = 0, hi = K;  // tstart[lo] <= t < tstart[hi]
-  while (hi - lo > 1) {
-    const uint32_t mid = (lo + hi) / 2;
-    if (a.tstart[mid] <= t) lo = mid;
+// Tile t of the long queues, found by a binary search over the first tiles
+// of the K queues (in long-list order). Its chain of dependent loads is paid
+// once per call: phase R stores the result in a.tdesc for the later phases.
+__device__ LongTileDesc long_tile(const BArgs& a, uint32_t t, uint32_t K) {
+  uint32_t k = 0, hi = K;  // tstart[k] <= t < tstart[hi]
+  while (hi - k > 1) {
+    const uint32_t mid = (k + hi) / 2;
+    if (a.tstart[mid] <= t) k = mid;
     else hi = mid;
   }
-  LongTile x;
-  x.k = lo;
-  x.s = a.lists[list_base(a, kListLong, 0) + lo];
-  x.base = a.offsets[x.s];
-  x.m = a.offsets[x.s + 1] - x.base;
-  x.lo = (int64_t)(t - a.tstart[lo]) * kLongTile;
-  x.cnt = (int)min((int64_t)kLongTile, x.m - x.lo);
+  LongTileDesc x;
+  const uint32_t r0 = a.tstart[k];
+  x.s = a.lists[list_base(a, kListLong, 0) + k];
+  const int64_t base = a.offsets[x.s];
+  const int64_t m = a.offsets[x.s + 1] - base;
+  x.lo = (t - r0) * (uint32_t)kLongTile;  // (below m < 2^31)
+  x.cnt = (int32_t)min((int64_t)kLongTile, m - (int64_t)x.lo);
+  x.first = base + x.lo;
+  x.at = a.lbase[k] + x.lo;
+  x.item0 = a.istart[k];
+  x.rows = a.tstart[k + 1] - r0;
+  return x;
+}
+
+// Tile tt's descriptor, or an empty tile past the last one.
+__device__ __forceinline__ LongTileDesc tile_or_empty(const BArgs& a, uint32_t tt,
+                                                      uint32_t ntiles) {
+  LongTileDesc x = {};
+  if (tt < ntiles) x = a.tdesc[tt];
   return x;
 }
 
@@ -860,15 +867,29 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   {
     uint32_t lmin = 0xffffffffu, lmax = 0, pmin = 0xffu, pmax = 0, bad = 0;
     for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
-      const LongTile x = long_tile(a, tt, K);
-      for (int i = t; i < x.cnt; i += kLT) {
-        const uint32_t p = a.priority[x.base + x.lo + i];
-        const int32_t l = a.length[x.base + x.lo + i];
-        bad |= (l < 0) | ((int)p >= a.num_classes);
-        lmin = min(lmin, (uint32_t)l);
-        lmax = max(lmax, (uint32_t)l);
-        pmin = min(pmin, p);
-        pmax = max(pmax, p);
+      const LongTileDesc x = long_tile(a, tt, K);
+      if (t == 0) a.tdesc[tt] = x;
+      uint32_t p[kLR];
+      int32_t l[kLR];
+#pragma unroll
+      for (int r = 0; r < kLR; ++r) {  // (every load issued before the first use)
+        const int i = r * kLT + t;
+        p[r] = 0;
+        l[r] = 0;
+        if (i < x.cnt) {
+          p[r] = a.priority[x.first + i];
+          l[r] = a.length[x.first + i];
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < kLR; ++r) {
+        if (r * kLT + t < x.cnt) {
+          bad |= (l[r] < 0) | ((int)p[r] >= a.num_classes);
+          lmin = min(lmin, (uint32_t)l[r]);
+          lmax = max(lmax, (uint32_t)l[r]);
+          pmin = min(pmin, p[r]);
+          pmax = max(pmax, p[r]);
+        }
       }
     }
     lmin = wave_min_u32(lmin);
@@ -915,8 +936,8 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
 
   // element r of this thread in tile x: request x.lo + w*64*kLR + r*64 + lane
   // (with_ids false: the ids are not read, for the counting phase)
-  auto load_elems = [&](const LongTile& x, int q, uint64_t (&key)[kLR], uint32_t (&id)[kLR],
-                        bool with_ids) {
+  auto load_elems = [&](const LongTileDesc& x, int q, uint64_t (&key)[kLR],
+                        uint32_t (&id)[kLR], bool with_ids) {
 #pragma unroll
     for (int r = 0; r < kLR; ++r) {
       const int i = w * kWave * kLR + r * kWave + lane;
@@ -924,14 +945,13 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       id[r] = 0;
       if (i < x.cnt) {
         if (q == 0) {
-          const uint32_t p = a.priority[x.base + x.lo + i];
-          const uint32_t l = (uint32_t)a.length[x.base + x.lo + i];
+          const uint32_t p = a.priority[x.first + i];
+          const uint32_t l = (uint32_t)a.length[x.first + i];
           key[r] = ((uint64_t)(p - pmin) << wl) | (uint64_t)(l - lmin);
-          id[r] = (uint32_t)(x.lo + i);
+          id[r] = x.lo + (uint32_t)i;
         } else {
-          const uint64_t at = a.lbase[x.k] + (uint64_t)(x.lo + i);
-          key[r] = a.keys[(q - 1) & 1][at];
-          if (with_ids) id[r] = a.ids[(q - 1) & 1][at];
+          key[r] = a.keys[(q - 1) & 1][x.at + i];
+          if (with_ids) id[r] = a.ids[(q - 1) & 1][x.at + i];
         }
       }
     }
@@ -940,11 +960,17 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   for (int q = 0; q < npass; ++q) {
     const uint32_t shift = kLongDigitBits * q;
     // ---- phase A: digit counts of every tile ----------------------------------------
+    // (the workgroup's next tile is loaded while this one is counted)
+    {
+    LongTileDesc x = tile_or_empty(a, blockIdx.x, ntiles);
+    uint64_t key[kLR];
+    uint32_t id[kLR];
+    load_elems(x, q, key, id, false);
     for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
-      const LongTile x = long_tile(a, tt, K);
-      uint64_t key[kLR];
-      uint32_t id[kLR];
-      load_elems(x, q, key, id, false);
+      const LongTileDesc xn = tile_or_empty(a, tt + gridDim.x, ntiles);
+      uint64_t nkey[kLR];
+      uint32_t nid[kLR];
+      load_elems(xn, q, nkey, nid, false);
       // (counts only: one LDS add per request into the wave's own table)
       uint32_t* mine = sh.u.acnt[w];
       for (int b = lane; b < kLB; b += kWave) mine[b] = 0;
@@ -963,6 +989,10 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
         a.hist[(size_t)tt * kLB + d] = c;
       }
       block_sync();
+      x = xn;
+#pragma unroll
+      for (int r = 0; r < kLR; ++r) key[r] = nkey[r];
+    }
     }
     grid.sync();
     // ---- phase B: per queue and digit, offsets over the queue's tiles ----------------
@@ -1017,36 +1047,51 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     }
     grid.sync();
     // ---- phase C: stable scatter of every tile ----------------------------------------
-    for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
-      const LongTile x = long_tile(a, tt, K);
-      uint64_t key[kLR];
-      uint32_t id[kLR], dg[kLR], rk[kLR];
-      load_elems(x, q, key, id, true);
-      uint32_t dbase[kLO] = {};  // queues of many tiles: the digits' bases in the queue
-      if (a.tstart[x.k + 1] - a.tstart[x.k] > kLongRowsFew) {  // (uniform)
-        uint32_t c[kLO], sum = 0;
+    // (the workgroup's next tile, its digit offsets and its queue's digit
+    // totals are loaded while this one is placed and written)
+    {
+    LongTileDesc x = tile_or_empty(a, blockIdx.x, ntiles);
+    uint64_t key[kLR];
+    uint32_t id[kLR], hv[kLO], qv[kLO];
+    auto load_offsets = [&](const LongTileDesc& y, uint32_t ty, uint32_t (&h)[kLO],
+                            uint32_t (&c)[kLO]) {
 #pragma unroll
-        for (int o = 0; o < kLO; ++o) {
-          c[o] = a.qtot[a.istart[x.k] + kLO * t + o];
-          sum += c[o];
-        }
+      for (int o = 0; o < kLO; ++o) {
+        h[o] = y.cnt > 0 ? a.hist[(size_t)ty * kLB + kLO * t + o] : 0u;
+        c[o] = y.rows > kLongRowsFew ? a.qtot[y.item0 + kLO * t + o] : 0u;
+      }
+    };
+    load_elems(x, q, key, id, true);
+    load_offsets(x, blockIdx.x, hv, qv);
+    for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+      uint32_t dg[kLR], rk[kLR];
+      uint32_t dbase[kLO] = {};  // queues of many tiles: the digits' bases in the queue
+      if (x.rows > kLongRowsFew) {  // (uniform)
+        uint32_t sum = 0;
+#pragma unroll
+        for (int o = 0; o < kLO; ++o) sum += qv[o];
         uint32_t total;
         uint32_t run = block_excl_scan_u32<kLT>(sum, sh.part32, total);
 #pragma unroll
         for (int o = 0; o < kLO; ++o) {
           dbase[o] = run;
-          run += c[o];
+          run += qv[o];
         }
       }
 #pragma unroll
-      for (int o = 0; o < kLO; ++o)
-        sh.hrow[kLO * t + o] = a.hist[(size_t)tt * kLB + kLO * t + o] + dbase[o];
+      for (int o = 0; o < kLO; ++o) sh.hrow[kLO * t + o] = hv[o] + dbase[o];
       clear_counters<kLB>(sh.cnt[w]);
 #pragma unroll
       for (int r = 0; r < kLR; ++r) {
         dg[r] = (uint32_t)(key[r] >> shift) & (kLB - 1);
         rk[r] = rank_round_c<kLongDigitBits>(dg[r], sh.cnt[w]);
       }
+      const uint32_t tn = tt + gridDim.x;
+      const LongTileDesc xn = tile_or_empty(a, tn, ntiles);
+      uint64_t nkey[kLR];
+      uint32_t nid[kLR];
+      load_elems(xn, q, nkey, nid, true);
+      load_offsets(xn, tn, hv, qv);
       block_sync();
       // owners: the waves' offsets within each digit, then the digits'
       // starts in the tile (elements past the end count in the last digit
@@ -1086,16 +1131,23 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
         }
       }
       block_sync();
-      uint64_t* kout = a.keys[q & 1];
-      uint32_t* iout = a.ids[q & 1];
+      uint64_t* kout = a.keys[q & 1] + (x.at - x.lo);  // the queue's first element
+      uint32_t* iout = a.ids[q & 1] + (x.at - x.lo);
       for (int j = t; j < x.cnt; j += kLT) {
         const uint64_t k = sh.u.st.key[j];
         const uint32_t d = (uint32_t)(k >> shift) & (kLB - 1);
-        const uint64_t at = a.lbase[x.k] + sh.hrow[d] + (uint32_t)(j - (int)sh.dstart[d]);
+        const uint32_t at = sh.hrow[d] + (uint32_t)(j - (int)sh.dstart[d]);
         kout[at] = k;
         iout[at] = sh.u.st.id[j];
       }
       block_sync();
+      x = xn;
+#pragma unroll
+      for (int r = 0; r < kLR; ++r) {
+        key[r] = nkey[r];
+        id[r] = nid[r];
+      }
+    }
     }
     grid.sync();
   }
@@ -1105,10 +1157,16 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   const uint32_t* sid = a.ids[(npass - 1) & 1];
   // phase D1: length sum of every tile
   for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
-    const LongTile x = long_tile(a, tt, K);
+    const LongTileDesc x = a.tdesc[tt];
+    uint64_t v[kLR];
+#pragma unroll
+    for (int r = 0; r < kLR; ++r) {  // (every load issued before the first use)
+      const int i = r * kLT + t;
+      v[r] = i < x.cnt ? (skey[x.at + i] & lmask) + lmin : 0;
+    }
     uint64_t s = 0;
-    for (int i = t; i < x.cnt; i += kLT)
-      s += (skey[a.lbase[x.k] + x.lo + i] & lmask) + lmin;
+#pragma unroll
+    for (int r = 0; r < kLR; ++r) s += v[r];
     s = wave_sum_u64(s);
     if (lane == 0) sh.part[w] = s;
     block_sync();
@@ -1156,39 +1214,53 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     for (uint32_t c = t; c < P; c += kLT) sh.clo[c] = sh.chi[c] = 0;
   };
   for (uint32_t c = t; c < P; c += kLT) sh.clo[c] = sh.chi[c] = 0;
-  for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
-    const LongTile x = long_tile(a, tt, K);
-    if (x.s != cur_s) {  // (uniform)
-      if (cur_s >= 0) flush();
-      cur_s = x.s;
-    }
-    block_sync();  // the totals are cleared
-    uint32_t len[kLR];
-    uint64_t key[kLR];
-    uint32_t id[kLR];
-    uint64_t mine = 0;
+  // (the workgroup's next tile and its wait base are loaded while this one
+  // is written)
+  auto load_sorted = [&](const LongTileDesc& y, uint32_t ty, uint64_t (&key)[kLR],
+                         uint32_t (&id)[kLR], uint64_t& wbase) {
 #pragma unroll
     for (int r = 0; r < kLR; ++r) {
       const int i = w * kWave * kLR + r * kWave + lane;
       key[r] = 0;
       id[r] = 0;
-      len[r] = 0;
-      if (i < x.cnt) {
-        const uint64_t at = a.lbase[x.k] + (uint64_t)(x.lo + i);
-        key[r] = skey[at];
-        id[r] = sid[at];
-        len[r] = (uint32_t)((key[r] & lmask) + lmin);
+      if (i < y.cnt) {
+        key[r] = skey[y.at + i];
+        id[r] = sid[y.at + i];
       }
+    }
+    wbase = y.cnt > 0 ? a.tsum[ty] : 0;
+  };
+  LongTileDesc x = tile_or_empty(a, blockIdx.x, ntiles);
+  uint64_t key[kLR], wbase;
+  uint32_t id[kLR];
+  load_sorted(x, blockIdx.x, key, id, wbase);
+  for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+    if (x.s != cur_s) {  // (uniform)
+      if (cur_s >= 0) flush();
+      cur_s = x.s;
+    }
+    block_sync();  // the totals are cleared
+    const uint32_t tn = tt + gridDim.x;
+    const LongTileDesc xn = tile_or_empty(a, tn, ntiles);
+    uint64_t nkey[kLR], nwbase;
+    uint32_t nid[kLR];
+    load_sorted(xn, tn, nkey, nid, nwbase);
+    uint32_t len[kLR];
+    uint64_t mine = 0;
+#pragma unroll
+    for (int r = 0; r < kLR; ++r) {
+      const int i = w * kWave * kLR + r * kWave + lane;
+      len[r] = i < x.cnt ? (uint32_t)((key[r] & lmask) + lmin) : 0u;
       mine += len[r];
     }
     const uint64_t wsum = wave_sum_u64(mine);
     if (lane == 0) sh.part[w] = wsum;
     block_sync();
-    uint64_t run = a.tsum[tt];
+    uint64_t run = wbase;
     for (int v = 0; v < w; ++v) run += sh.part[v];  // (w is uniform)
     int cur = -1;
     U128 acc = {0, 0};
-    const int64_t out0 = x.base + x.lo;
+    const int64_t out0 = x.first;
 #pragma unroll
     for (int r = 0; r < kLR; ++r) {
       const int i = w * kWave * kLR + r * kWave + lane;
@@ -1209,6 +1281,13 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     }
     if (cur >= 0) atomic_add128(&sh.clo[cur], &sh.chi[cur], acc);
     block_sync();  // (sh.part is read; the next tile writes it)
+    x = xn;
+    wbase = nwbase;
+#pragma unroll
+    for (int r = 0; r < kLR; ++r) {
+      key[r] = nkey[r];
+      id[r] = nid[r];
+    }
   }
   if (cur_s >= 0) flush();  // (uniform)
 }

@@ -56,6 +56,19 @@ struct alignas(128) GrabLine {
   uint32_t pad[30];
 };
 
+// One tile of the segmented sort of the long queues: found once per call by a
+// search over the queues' first tiles, then read by every later phase with
+// one load.
+struct LongTileDesc {
+  int64_t first;   // global index of the tile's first request
+  uint64_t at;     // position of that request in the keys/ids arrays
+  int64_t s;       // the queue
+  uint32_t lo;     // the tile's first request within the queue
+  int32_t cnt;     // requests in the tile
+  uint32_t item0;  // the queue's first digit-offset work item
+  uint32_t rows;   // tiles of the queue
+};
+
 struct BArgs {
   const uint8_t* priority;
   const int32_t* length;
@@ -84,6 +97,7 @@ struct BArgs {
   uint32_t* tstart;         // [long list + 1] first tile of every long queue
   uint32_t* istart;         // [long list + 1] first digit-offset work item of every long queue
   uint32_t* qtot;           // [long_items_max] digit totals of the queues of many tiles
+  LongTileDesc* tdesc;      // [max_tiles] every tile's place, written once per call
 };
 
 // Single queue of a.n_single <= kSegLargeCap requests (a.offsets null), one
