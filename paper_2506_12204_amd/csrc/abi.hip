@@ -573,7 +573,7 @@ int check_batched_args(const uint8_t* p, const int32_t* l, const int64_t* offset
 // queues longer than kSegLargeCap.
 struct BLayout {
   size_t ctl = 64, grab = 0, lists = 0, keys0 = 0, keys1 = 0, ids0 = 0, ids1 = 0, hist = 0, tsum = 0,
-         lbase = 0, tstart = 0, istart = 0, qtot = 0, tdesc = 0, total = 0;
+         lbase = 0, tstart = 0, istart = 0, qtot = 0, tdesc = 0, imap = 0, total = 0;
   uint32_t max_tiles = 0;
 };
 
@@ -602,8 +602,9 @@ BLayout batched_layout(int64_t S, uint64_t long_cap) {
     L.lbase = take(8 * (size_t)(queues + 1));
     L.tstart = take(4 * (size_t)(queues + 1));
     L.istart = take(4 * (size_t)(queues + 1));
-    L.qtot = take(4 * (size_t)long_items_max(long_cap, (int64_t)queues));
+    L.qtot = take(4 * (size_t)kLongColDigits * (size_t)long_items_max(long_cap, (int64_t)queues));
     L.tdesc = take(sizeof(LongTileDesc) * (size_t)L.max_tiles);
+    L.imap = take(4 * (size_t)long_items_max(long_cap, (int64_t)queues));
   }
   L.total = off;
   return L;
@@ -662,6 +663,7 @@ int enqueue_batched(const uint8_t* p, const int32_t* l, const int64_t* offsets,
     a.istart = reinterpret_cast<uint32_t*>(base + L.istart);
     a.qtot = reinterpret_cast<uint32_t*>(base + L.qtot);
     a.tdesc = reinterpret_cast<LongTileDesc*>(base + L.tdesc);
+    a.imap = reinterpret_cast<uint32_t*>(base + L.imap);
   }
   return launch_batched(a, st) == hipSuccess ? SEM_OK : SEM_EDEVICE;
 }

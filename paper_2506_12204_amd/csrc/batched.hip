@@ -749,6 +749,10 @@ constexpr int kLW = kLT / kWave;
 constexpr int kLR = kLongTile / kLT;  // rounds per thread
 constexpr int kLB = 1 << kLongDigitBits;  // digits of a pass
 constexpr int kLO = kLB / kLT;            // digits per thread (consecutive)
+constexpr int kCD = kLongColDigits;       // digits of a column item
+constexpr int kCR = 512;                  // rows of a column item's block
+constexpr int kCS = kLT / kCD;            // row segments of a block (a thread each per digit)
+constexpr int kCSR = kCR / kCS;           // rows of a segment
 
 struct LongLds {
   uint16_t cnt[kLW][kLB];
@@ -760,6 +764,10 @@ struct LongLds {
       uint32_t id[kLongTile];
     } st;
     uint32_t acnt[kLW][kLB];  // the counting phase's per-wave counts
+    struct {  // a column item's block of rows (padded rows), its segments' sums
+      uint32_t v[kCR][kCD + 1];
+      uint32_t seg[kCS][kCD];
+    } col;
   } u;
   uint64_t clo[256], chi[256];
   uint64_t part[kLW + 1];
@@ -825,7 +833,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
         m = (uint64_t)(a.offsets[s + 1] - a.offsets[s]);
       }
       const uint32_t tiles = (uint32_t)((m + kLongTile - 1) / kLongTile);
-      const uint32_t items = k < K ? (tiles <= kLongRowsFew ? 1u : (uint32_t)kLB) : 0u;
+      const uint32_t items = k < K ? (tiles <= kLongRowsFew ? 1u : (uint32_t)(kLB / kCD)) : 0u;
       uint64_t tot_e;
       uint32_t tot_t, tot_i;
       const uint64_t ex_e = block_excl_scan_u64<kLT>(m, sh.part, tot_e);
@@ -869,6 +877,10 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
       const LongTileDesc x = long_tile(a, tt, K);
       if (t == 0) a.tdesc[tt] = x;
+      if (x.lo == 0) {  // (uniform) the queue's first tile: map its digit-offset items
+        const uint32_t nit = x.rows <= kLongRowsFew ? 1u : (uint32_t)(kLB / kCD);
+        for (uint32_t j = t; j < nit; j += kLT) a.imap[x.item0 + j] = tt;
+      }
       uint32_t p[kLR];
       int32_t l[kLR];
 #pragma unroll
@@ -998,18 +1010,14 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     // ---- phase B: per queue and digit, offsets over the queue's tiles ----------------
     // A queue of few tiles is one work item: each thread runs down the
     // columns of its kLO digits and the digit bases are added at once. A
-    // queue of many tiles is kLB items, one per digit, each a block scan down
-    // its column in rows of kLT tiles; its digit totals go to qtot and the
-    // digit bases are added by the scatter (phase C).
+    // queue of many tiles is kLB / kCD items of kCD digits each, whose
+    // columns are scanned together down the queue's tiles; its digit totals
+    // go to qtot and the digit bases are added by the scatter (phase C).
     for (uint32_t it = blockIdx.x; it < nitems; it += gridDim.x) {
-      uint32_t k = 0, hi = K;  // istart[k] <= it < istart[k + 1]
-      while (hi - k > 1) {
-        const uint32_t mid = (k + hi) / 2;
-        if (a.istart[mid] <= it) k = mid;
-        else hi = mid;
-      }
-      const uint32_t r0 = a.tstart[k], r1 = a.tstart[k + 1];
-      if (r1 - r0 <= kLongRowsFew) {
+      const uint32_t r0 = a.imap[it];  // the queue's first tile
+      const LongTileDesc y = a.tdesc[r0];
+      const uint32_t r1 = r0 + y.rows;
+      if (y.rows <= kLongRowsFew) {
         uint32_t tot[kLO], sum = 0;
 #pragma unroll
         for (int o = 0; o < kLO; ++o) {
@@ -1032,17 +1040,58 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
           run += tot[o];
         }
       } else {
-        const uint32_t d = it - a.istart[k];
-        uint32_t carry = 0;
-        for (uint32_t row0 = r0; row0 < r1; row0 += kLT) {
-          const uint32_t row = row0 + t;
-          const uint32_t c = row < r1 ? a.hist[(size_t)row * kLB + d] : 0u;
-          uint32_t total;
-          const uint32_t ex = block_excl_scan_u32<kLT>(c, sh.part32, total);
-          if (row < r1) a.hist[(size_t)row * kLB + d] = carry + ex;
-          carry += total;
+        // kCD digits from d0: blocks of kCR rows are loaded coalesced into
+        // LDS, each thread scans kCSR rows of one digit, a thread per digit
+        // scans the segments' sums (carrying the earlier blocks' totals), and
+        // the offsets go back coalesced
+        const uint32_t d0 = (it - y.item0) * kCD;
+        uint32_t carry = 0;  // (threads t < kCD: digit d0 + t)
+        for (uint32_t row0 = r0; row0 < r1; row0 += kCR) {
+          uint32_t* hb = a.hist + (size_t)row0 * kLB + d0;  // (uniform)
+          const uint32_t nr = min(r1 - row0, (uint32_t)kCR);
+          // the thread index through an empty asm: the offsets below are
+          // formed here, not hoisted out of every loop around this one (they
+          // would hold registers through the other phases)
+          int tv = t;
+          asm volatile("" : "+v"(tv));
+#pragma unroll
+          for (int j = 0; j < kCR * kCD / kLT; ++j) {
+            const int v = j * kLT + tv;
+            sh.u.col.v[v / kCD][v % kCD] =
+                (uint32_t)(v / kCD) < nr ? hb[(v / kCD) * kLB + v % kCD] : 0u;
+          }
+          block_sync();
+          {
+            const int dd = tv % kCD, sg = tv / kCD;
+            uint32_t run = 0;
+#pragma unroll
+            for (int k = 0; k < kCSR; ++k) {
+              const uint32_t c = sh.u.col.v[sg * kCSR + k][dd];
+              sh.u.col.v[sg * kCSR + k][dd] = run;
+              run += c;
+            }
+            sh.u.col.seg[sg][dd] = run;
+          }
+          block_sync();
+          if (t < kCD) {
+#pragma unroll 8
+            for (int g = 0; g < kCS; ++g) {
+              const uint32_t c = sh.u.col.seg[g][t];
+              sh.u.col.seg[g][t] = carry;
+              carry += c;
+            }
+          }
+          block_sync();
+#pragma unroll
+          for (int j = 0; j < kCR * kCD / kLT; ++j) {
+            const int v = j * kLT + tv;
+            if ((uint32_t)(v / kCD) < nr)
+              hb[(v / kCD) * kLB + v % kCD] =
+                  sh.u.col.v[v / kCD][v % kCD] + sh.u.col.seg[(v / kCD) / kCSR][v % kCD];
+          }
+          block_sync();
         }
-        if (t == 0) a.qtot[it] = carry;
+        if (t < kCD) a.qtot[(size_t)it * kCD + t] = carry;
       }
     }
     grid.sync();
@@ -1058,7 +1107,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
 #pragma unroll
       for (int o = 0; o < kLO; ++o) {
         h[o] = y.cnt > 0 ? a.hist[(size_t)ty * kLB + kLO * t + o] : 0u;
-        c[o] = y.rows > kLongRowsFew ? a.qtot[y.item0 + kLO * t + o] : 0u;
+        c[o] = y.rows > kLongRowsFew ? a.qtot[(size_t)y.item0 * kCD + kLO * t + o] : 0u;
       }
     };
     load_elems(x, q, key, id, true);
@@ -1156,26 +1205,38 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   const uint64_t* skey = a.keys[(npass - 1) & 1];
   const uint32_t* sid = a.ids[(npass - 1) & 1];
   // phase D1: length sum of every tile
-  for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
-    const LongTileDesc x = a.tdesc[tt];
-    uint64_t v[kLR];
+  // (the workgroup's next tile is loaded while this one is summed)
+  {
+  auto load_keys = [&](const LongTileDesc& y, uint64_t (&v)[kLR]) {
 #pragma unroll
-    for (int r = 0; r < kLR; ++r) {  // (every load issued before the first use)
+    for (int r = 0; r < kLR; ++r) {
       const int i = r * kLT + t;
-      v[r] = i < x.cnt ? (skey[x.at + i] & lmask) + lmin : 0;
+      v[r] = i < y.cnt ? skey[y.at + i] : 0;
     }
+  };
+  LongTileDesc x = tile_or_empty(a, blockIdx.x, ntiles);
+  uint64_t v[kLR];
+  load_keys(x, v);
+  for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+    const LongTileDesc xn = tile_or_empty(a, tt + gridDim.x, ntiles);
+    uint64_t nv[kLR];
+    load_keys(xn, nv);
     uint64_t s = 0;
 #pragma unroll
-    for (int r = 0; r < kLR; ++r) s += v[r];
+    for (int r = 0; r < kLR; ++r) s += r * kLT + t < x.cnt ? (v[r] & lmask) + lmin : 0;
     s = wave_sum_u64(s);
     if (lane == 0) sh.part[w] = s;
     block_sync();
     if (t == 0) {
-      uint64_t v = 0;
-      for (int u = 0; u < kLW; ++u) v += sh.part[u];
-      a.tsum[tt] = v;
+      uint64_t sum = 0;
+      for (int u = 0; u < kLW; ++u) sum += sh.part[u];
+      a.tsum[tt] = sum;
     }
     block_sync();
+    x = xn;
+#pragma unroll
+    for (int r = 0; r < kLR; ++r) v[r] = nv[r];
+  }
   }
   grid.sync();
   // phase D2: per queue, exclusive scan of its tiles' sums

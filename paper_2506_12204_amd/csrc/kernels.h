@@ -96,8 +96,9 @@ struct BArgs {
   uint64_t* lbase;          // [long list + 1] start of every long queue in keys/ids
   uint32_t* tstart;         // [long list + 1] first tile of every long queue
   uint32_t* istart;         // [long list + 1] first digit-offset work item of every long queue
-  uint32_t* qtot;           // [long_items_max] digit totals of the queues of many tiles
+  uint32_t* qtot;           // [kLongColDigits * long_items_max] digit totals of the queues of many tiles
   LongTileDesc* tdesc;      // [max_tiles] every tile's place, written once per call
+  uint32_t* imap;           // [long_items_max] first tile of each digit-offset item's queue
 };
 
 // Single queue of a.n_single <= kSegLargeCap requests (a.offsets null), one
@@ -112,12 +113,14 @@ uint32_t long_max_tiles(uint64_t long_cap, int64_t num_segments);
 // Digits of a pass of the segmented sort of the long queues.
 constexpr int kLongDigitBits = 10;
 // A long queue of at most kLongRowsFew tiles takes its digit offsets in one
-// work item; a longer one in one per digit (over its tiles in parallel).
+// work item; a longer one in one per kLongColDigits digits.
 constexpr uint32_t kLongRowsFew = 32;
-// Most digit-offset work items of the long queues (and entries of qtot).
+// Digits of one work item of a longer queue (its columns are scanned together).
+constexpr int kLongColDigits = 16;
+// Most digit-offset work items of the long queues.
 inline uint64_t long_items_max(uint64_t long_cap, int64_t queues) {
-  return (uint64_t)queues +
-         (1u << kLongDigitBits) * (long_cap / ((uint64_t)kLongRowsFew * kLongTile) + 1);
+  return (uint64_t)queues + ((1u << kLongDigitBits) / kLongColDigits) *
+                                (long_cap / ((uint64_t)kLongRowsFew * kLongTile) + 1);
 }
 
 // ---------------------------------------------------------------------------
