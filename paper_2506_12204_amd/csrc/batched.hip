@@ -944,6 +944,10 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   const uint32_t wl = bit_width32(lmax - lmin);
   const uint32_t kb = wl + bit_width32(pmax - pmin);
   const int npass = kb ? (int)((kb + kLongDigitBits - 1) / kLongDigitBits) : 1;
+  // the key's bits split evenly over the passes: longer runs per digit in
+  // the scatter than a full first digit and a short last one
+  const uint32_t dbits = (kb + npass - 1) / npass;
+  const uint32_t dmask = (1u << dbits) - 1;
   const uint64_t lmask = wl ? ((1ull << wl) - 1) : 0;
 
   // element r of this thread in tile x: request x.lo + w*64*kLR + r*64 + lane
@@ -970,7 +974,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   };
 
   for (int q = 0; q < npass; ++q) {
-    const uint32_t shift = kLongDigitBits * q;
+    const uint32_t shift = dbits * q;
     // ---- phase A: digit counts of every tile ----------------------------------------
     // (the workgroup's next tile is loaded while this one is counted)
     {
@@ -989,7 +993,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
 #pragma unroll
       for (int r = 0; r < kLR; ++r) {
         const int i = w * kWave * kLR + r * kWave + lane;
-        if (i < x.cnt) atomicAdd(&mine[(uint32_t)(key[r] >> shift) & (kLB - 1)], 1u);
+        if (i < x.cnt) atomicAdd(&mine[(uint32_t)(key[r] >> shift) & dmask], 1u);
       }
       block_sync();
 #pragma unroll
@@ -1132,7 +1136,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       clear_counters<kLB>(sh.cnt[w]);
 #pragma unroll
       for (int r = 0; r < kLR; ++r) {
-        dg[r] = (uint32_t)(key[r] >> shift) & (kLB - 1);
+        dg[r] = (uint32_t)(key[r] >> shift) & dmask;
         rk[r] = rank_round_c<kLongDigitBits>(dg[r], sh.cnt[w]);
       }
       const uint32_t tn = tt + gridDim.x;
@@ -1184,7 +1188,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       uint32_t* iout = a.ids[q & 1] + (x.at - x.lo);
       for (int j = t; j < x.cnt; j += kLT) {
         const uint64_t k = sh.u.st.key[j];
-        const uint32_t d = (uint32_t)(k >> shift) & (kLB - 1);
+        const uint32_t d = (uint32_t)(k >> shift) & dmask;
         const uint32_t at = sh.hrow[d] + (uint32_t)(j - (int)sh.dstart[d]);
         kout[at] = k;
         iout[at] = sh.u.st.id[j];

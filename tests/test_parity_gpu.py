@@ -333,6 +333,16 @@ def test_batched_one_long_queue():
     check_batched(p, l, off, 5, "one-long")
 
 
+@pytest.mark.parametrize("classes,max_len", [(2, 256), (4, 512), (3, 2**19), (5, 2**27),
+                                             (200, 2**24)])
+def test_batched_long_queue_key_widths(classes, max_len):
+    # 9, 11, 21, 30 and 32 key bits: one pass, and splits of the key over two
+    # to four passes that are not all of the widest digit
+    sizes = [20000, 70000, 5, 300000]
+    p, l, off = fuzz_segments(sizes, seed=40 + classes, classes=classes, max_len=max_len)
+    check_batched(p, l, off, classes, f"long-keys-{classes}-{max_len}")
+
+
 def test_batched_wide_keys_in_short_queues():
     # lengths over the whole int32 range: short queues whose key does not fit
     # a 32-bit element go to the 64-bit kernel, long ones to the segmented sort
