@@ -857,6 +857,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       a.ctl->ranges[1] = 0;
       a.ctl->ranges[2] = 0xffffffffu;
       a.ctl->ranges[3] = 0;
+      a.ctl->ranges[4] = 0;
     }
   }
   for (int64_t i = (int64_t)blockIdx.x * kLT + t; i < (int64_t)K * 2 * C1;
@@ -873,10 +874,11 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   // and workgroup, skipped when it would not change the word: atomics on one
   // line serialise, and one per wave and tile queued thousands on it.
   {
-    uint32_t lmin = 0xffffffffu, lmax = 0, pmin = 0xffu, pmax = 0, bad = 0;
+    uint32_t lmin = 0xffffffffu, lmax = 0, pmin = 0xffu, pmax = 0, bad = 0, mmax = 0;
     for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
       const LongTileDesc x = long_tile(a, tt, K);
       if (t == 0) a.tdesc[tt] = x;
+      mmax = max(mmax, x.lo + (uint32_t)x.cnt);  // (uniform) the queue's size at its last tile
       if (x.lo == 0) {  // (uniform) the queue's first tile: map its digit-offset items
         const uint32_t nit = x.rows <= kLongRowsFew ? 1u : (uint32_t)(kLB / kCD);
         for (uint32_t j = t; j < nit; j += kLT) a.imap[x.item0 + j] = tt;
@@ -929,6 +931,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       if (pmax > load_agent(rg + 1)) atomicMax(rg + 1, pmax);
       if (lmin < load_agent(rg + 2)) atomicMin(rg + 2, lmin);
       if (lmax > load_agent(rg + 3)) atomicMax(rg + 3, lmax);
+      if (mmax > load_agent(rg + 4)) atomicMax(rg + 4, mmax);  // (mmax: the same in every thread)
     }
   }
   grid.sync();
@@ -949,6 +952,13 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   const uint32_t dbits = (kb + npass - 1) / npass;
   const uint32_t dmask = (1u << dbits) - 1;
   const uint64_t lmask = wl ? ((1ull << wl) - 1) : 0;
+  // When the key and the request's index in its queue fit 64 bits together,
+  // the index rides in the element's low ib bits (8 bytes per element
+  // between the passes instead of a key and a separate id); else ib = 0.
+  const uint32_t idb = bit_width32(range(4) - 1);
+  const bool packed = kb + idb <= 64;
+  const uint32_t ib = packed ? idb : 0u;
+  const uint64_t idmask = (1ull << ib) - 1;
 
   // element r of this thread in tile x: request x.lo + w*64*kLR + r*64 + lane
   // (with_ids false: the ids are not read, for the counting phase)
@@ -963,18 +973,19 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
         if (q == 0) {
           const uint32_t p = a.priority[x.first + i];
           const uint32_t l = (uint32_t)a.length[x.first + i];
-          key[r] = ((uint64_t)(p - pmin) << wl) | (uint64_t)(l - lmin);
           id[r] = x.lo + (uint32_t)i;
+          key[r] = ((((uint64_t)(p - pmin) << wl) | (uint64_t)(l - lmin)) << ib) |
+                   (packed ? id[r] : 0u);
         } else {
           key[r] = a.keys[(q - 1) & 1][x.at + i];
-          if (with_ids) id[r] = a.ids[(q - 1) & 1][x.at + i];
+          if (with_ids && !packed) id[r] = a.ids[(q - 1) & 1][x.at + i];
         }
       }
     }
   };
 
   for (int q = 0; q < npass; ++q) {
-    const uint32_t shift = dbits * q;
+    const uint32_t shift = ib + dbits * q;
     // ---- phase A: digit counts of every tile ----------------------------------------
     // (the workgroup's next tile is loaded while this one is counted)
     {
@@ -1180,7 +1191,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
         if (i < x.cnt) {
           const uint32_t j = sh.dstart[dg[r]] + sh.cnt[w][dg[r]] + rk[r];
           sh.u.st.key[j] = key[r];
-          sh.u.st.id[j] = id[r];
+          if (!packed) sh.u.st.id[j] = id[r];
         }
       }
       block_sync();
@@ -1191,7 +1202,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
         const uint32_t d = (uint32_t)(k >> shift) & dmask;
         const uint32_t at = sh.hrow[d] + (uint32_t)(j - (int)sh.dstart[d]);
         kout[at] = k;
-        iout[at] = sh.u.st.id[j];
+        if (!packed) iout[at] = sh.u.st.id[j];
       }
       block_sync();
       x = xn;
@@ -1227,7 +1238,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     load_keys(xn, nv);
     uint64_t s = 0;
 #pragma unroll
-    for (int r = 0; r < kLR; ++r) s += r * kLT + t < x.cnt ? (v[r] & lmask) + lmin : 0;
+    for (int r = 0; r < kLR; ++r) s += r * kLT + t < x.cnt ? ((v[r] >> ib) & lmask) + lmin : 0;
     s = wave_sum_u64(s);
     if (lane == 0) sh.part[w] = s;
     block_sync();
@@ -1290,7 +1301,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       id[r] = 0;
       if (i < y.cnt) {
         key[r] = skey[y.at + i];
-        id[r] = sid[y.at + i];
+        id[r] = packed ? (uint32_t)(key[r] & idmask) : sid[y.at + i];
       }
     }
     wbase = y.cnt > 0 ? a.tsum[ty] : 0;
@@ -1315,7 +1326,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
 #pragma unroll
     for (int r = 0; r < kLR; ++r) {
       const int i = w * kWave * kLR + r * kWave + lane;
-      len[r] = i < x.cnt ? (uint32_t)((key[r] & lmask) + lmin) : 0u;
+      len[r] = i < x.cnt ? (uint32_t)(((key[r] >> ib) & lmask) + lmin) : 0u;
       mine += len[r];
     }
     const uint64_t wsum = wave_sum_u64(mine);
@@ -1335,7 +1346,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       if (i < x.cnt) {
         a.order[out0 + i] = (int32_t)id[r];
         a.wait[out0 + i] = (int64_t)wt;
-        const int cls = (int)(key[r] >> wl);
+        const int cls = (int)(key[r] >> (ib + wl));
         if (cls != cur) {
           if (cur >= 0) atomic_add128(&sh.clo[cur], &sh.chi[cur], acc);
           cur = cls;

@@ -44,7 +44,7 @@ struct BCtl {
   uint32_t count[kLists];             // entries of the long list (count[kListLong])
   uint32_t empty[kLists][kSubLists];  // 1 once a segment was found exhausted (a hint)
   uint64_t long_elems;                // requests in the long list's queues
-  uint32_t ranges[4];                 // long queues: pmin, pmax, lmin, lmax
+  uint32_t ranges[5];                 // long queues: pmin, pmax, lmin, lmax, longest
 };
 // One segment of a list, alone in its 128-byte line: its entry count (the
 // planner's filing atomics) and the next batch to grab (the kernels'

@@ -343,6 +343,14 @@ def test_batched_long_queue_key_widths(classes, max_len):
     check_batched(p, l, off, classes, f"long-keys-{classes}-{max_len}")
 
 
+def test_batched_long_queue_key_and_index_beyond_64_bits():
+    # 39 key bits (256 classes, lengths over the whole int32 range) and a
+    # queue of more than 2^25 requests (26 index bits): the elements between
+    # the passes keep the index apart from the key
+    p, l, off = fuzz_segments([5, 2**25 + 3, 7], seed=61, classes=256, max_len=2**31 - 1)
+    check_batched(p, l, off, 256, "long-keys-65-bits")
+
+
 def test_batched_wide_keys_in_short_queues():
     # lengths over the whole int32 range: short queues whose key does not fit
     # a 32-bit element go to the 64-bit kernel, long ones to the segmented sort
