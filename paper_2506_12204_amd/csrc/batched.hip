@@ -775,6 +775,14 @@ struct LongLds {
   uint32_t red[4][kLW];
 };
 
+// Waits for every outstanding global load and store of the wave (s_waitcnt
+// with vmcnt 0; expcnt and lgkmcnt at their maxima, so not waited for). At
+// the top of a tile loop whose next tile is loaded ahead: loads and stores
+// share that counter, and with the previous tile's stores still pending the
+// compiler's own wait at the first use of a loaded value waits for all of
+// them, the next tile's loads too; after this wait it places none.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Tile t of the long queues, found by a binary search over the first tiles
 // of the K queues (in long-list order). Its chain of dependent loads is paid
 // once per call: phase R stores the result in a.tdesc for the later phases.
@@ -994,6 +1002,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     uint32_t id[kLR];
     load_elems(x, q, key, id, false);
     for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+      wait_vmem();
       const LongTileDesc xn = tile_or_empty(a, tt + gridDim.x, ntiles);
       uint64_t nkey[kLR];
       uint32_t nid[kLR];
@@ -1128,6 +1137,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
     load_elems(x, q, key, id, true);
     load_offsets(x, blockIdx.x, hv, qv);
     for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+      wait_vmem();
       uint32_t dg[kLR], rk[kLR];
       uint32_t dbase[kLO] = {};  // queues of many tiles: the digits' bases in the queue
       if (x.rows > kLongRowsFew) {  // (uniform)
@@ -1233,6 +1243,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   uint64_t v[kLR];
   load_keys(x, v);
   for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+    wait_vmem();
     const LongTileDesc xn = tile_or_empty(a, tt + gridDim.x, ntiles);
     uint64_t nv[kLR];
     load_keys(xn, nv);
@@ -1294,15 +1305,17 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   // is written)
   auto load_sorted = [&](const LongTileDesc& y, uint32_t ty, uint64_t (&key)[kLR],
                          uint32_t (&id)[kLR], uint64_t& wbase) {
+    // (packed: the ids are taken from the keys where they are stored, so
+    // that no load waits for the one before it)
 #pragma unroll
     for (int r = 0; r < kLR; ++r) {
       const int i = w * kWave * kLR + r * kWave + lane;
-      key[r] = 0;
-      id[r] = 0;
-      if (i < y.cnt) {
-        key[r] = skey[y.at + i];
-        id[r] = packed ? (uint32_t)(key[r] & idmask) : sid[y.at + i];
-      }
+      key[r] = i < y.cnt ? skey[y.at + i] : 0ull;
+    }
+#pragma unroll
+    for (int r = 0; r < kLR; ++r) {
+      const int i = w * kWave * kLR + r * kWave + lane;
+      id[r] = !packed && i < y.cnt ? sid[y.at + i] : 0u;
     }
     wbase = y.cnt > 0 ? a.tsum[ty] : 0;
   };
@@ -1311,16 +1324,12 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
   uint32_t id[kLR];
   load_sorted(x, blockIdx.x, key, id, wbase);
   for (uint32_t tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+    wait_vmem();
     if (x.s != cur_s) {  // (uniform)
       if (cur_s >= 0) flush();
       cur_s = x.s;
     }
     block_sync();  // the totals are cleared
-    const uint32_t tn = tt + gridDim.x;
-    const LongTileDesc xn = tile_or_empty(a, tn, ntiles);
-    uint64_t nkey[kLR], nwbase;
-    uint32_t nid[kLR];
-    load_sorted(xn, tn, nkey, nid, nwbase);
     uint32_t len[kLR];
     uint64_t mine = 0;
 #pragma unroll
@@ -1329,6 +1338,11 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       len[r] = i < x.cnt ? (uint32_t)(((key[r] >> ib) & lmask) + lmin) : 0u;
       mine += len[r];
     }
+    const uint32_t tn = tt + gridDim.x;
+    const LongTileDesc xn = tile_or_empty(a, tn, ntiles);
+    uint64_t nkey[kLR], nwbase;
+    uint32_t nid[kLR];
+    load_sorted(xn, tn, nkey, nid, nwbase);
     const uint64_t wsum = wave_sum_u64(mine);
     if (lane == 0) sh.part[w] = wsum;
     block_sync();
@@ -1344,7 +1358,7 @@ __global__ __launch_bounds__(kLT) void b_long(BArgs a) {
       const uint64_t wt = run + incl - len[r];
       run += last_lane_u64(incl);
       if (i < x.cnt) {
-        a.order[out0 + i] = (int32_t)id[r];
+        a.order[out0 + i] = (int32_t)(packed ? (uint32_t)(key[r] & idmask) : id[r]);
         a.wait[out0 + i] = (int64_t)wt;
         const int cls = (int)(key[r] >> (ib + wl));
         if (cls != cur) {
