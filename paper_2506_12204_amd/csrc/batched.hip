@@ -737,10 +737,12 @@ __global__ __launch_bounds__(kWideThreads) void b_wide(BArgs a) {
 // kLongTile requests (a tile never spans two queues); the key of a request is
 // (priority - pmin) << wl | (length - lmin) with the ranges of all long
 // queues together, and the queue a tile belongs to is not part of the key:
-// digit offsets are scanned per queue over its own tiles. Per 10-bit digit
-// pass: count every tile's digits, scan the counts per queue and digit over
-// the queue's tiles (plus the queue's digit bases), scatter every tile
-// stably. Then the waits: every tile's length sum, the exclusive scan of
+// digit offsets are scanned per queue over its own tiles. The key's live
+// bits are split evenly over passes of at most 10 bits; when the key and the
+// request's index in its queue fit 64 bits, the index rides below the key in
+// one element. Per pass: count every tile's digits, scan the counts per
+// queue and digit over the queue's tiles (plus the queue's digit bases),
+// scatter every tile stably. Then the waits: every tile's length sum, the exclusive scan of
 // those per queue, and every tile's own scan, with exact 128-bit class
 // totals. Grid-wide phases are separated by grid syncs; the launch is
 // cooperative, so every workgroup is resident.
