@@ -64,7 +64,19 @@ WORKLOAD_TEXT = {
     "c4": "65,536 queues x 256 requests, 4 urgency classes uniform, lognormal lengths, seed 3",
     "c5": "16,384 queues of sizes U[1,4096], 8 classes (70 % in class 7), Pareto lengths "
           "with 30 % copied from the left neighbour, seed 4",
+    "long": "16 queues x 2^20 requests, 5 urgency classes uniform, lengths uniform in "
+            "[1,32768], 20 % copying an earlier request's class and length, seed 3",
 }
+
+
+def long_queue_workload():
+    """16 queues of 2^20 requests: every queue is longer than one workgroup's
+    LDS holds, so the whole batch goes through the segmented sort of long
+    queues (the queues are cut into tiles of the batch, ranked per queue)."""
+    from workloads import Workload, fuzz_segments
+    p, l, off = fuzz_segments([1 << 20] * 16, seed=3, classes=5, max_len=32768)
+    return Workload(name="long", priority=p, length=l, offsets=off, num_classes=5,
+                    meta={"queues": 16, "queue_size": 1 << 20, "seed": 3})
 POLICY_COUNTERS = os.path.join(ROOT, "profiles", "policy_c3_counters.md")
 POLICY_SOURCE = (os.path.join(CSRC, "policy.hip"),) + COMMON
 # The pass each policy's roofline is taken on: its name, the algorithmic
@@ -561,7 +573,7 @@ def bench_batched(args) -> int:
     import paper_2506_12204_amd as ss
     from workloads import generate, workload_sha256
 
-    w = generate(args.workload)
+    w = long_queue_workload() if args.workload == "long" else generate(args.workload)
     n = w.n
     s = len(w.offsets) - 1
     c = int(w.num_classes)
@@ -798,8 +810,8 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c3", choices=["c3", "c2", "c4", "c5"],
-                    help="c4 and c5 are batched queues (the schedule op only)")
+    ap.add_argument("--workload", default="c3", choices=["c3", "c2", "c4", "c5", "long"],
+                    help="c4, c5 and long are batched queues (the schedule op only)")
     ap.add_argument("--op", default="schedule", choices=["schedule", "insert", "policy", "cost", "iteration"],
                     help="schedule (default): the whole queue; insert: 2^16 arrivals "
                          "merged into the schedule of the rest; policy: the queue under "
@@ -826,7 +838,7 @@ def main() -> int:
         return bench_cost(args)
     if args.op == "iteration":
         return bench_iteration(args)
-    if args.workload in ("c4", "c5"):
+    if args.workload in ("c4", "c5", "long"):
         return bench_batched(args)
 
     return bench_queue(args)

@@ -186,6 +186,10 @@ int oracle_schedule_batched_parallel(const uint8_t *pri, const int32_t *len,
   const int64_t stride = 1 + num_classes;
   int rc = ORACLE_OK;
   int used = 1;
+  /* queues handed out in chunks of up to 16, fewer when there are too few
+     queues to give every thread several chunks (16 long queues: one each) */
+  const int64_t per = num_segments / (8 * (int64_t)omp_get_max_threads());
+  const int chunk = (int)(per < 1 ? 1 : (per > 16 ? 16 : per));
 #pragma omp parallel
   {
     rec_t *recs = (rec_t *)malloc((size_t)(biggest ? biggest : 1) * sizeof(rec_t));
@@ -193,7 +197,7 @@ int oracle_schedule_batched_parallel(const uint8_t *pri, const int32_t *len,
     int mine = (recs && tmp) ? ORACLE_OK : ORACLE_ENOMEM;
 #pragma omp single
     used = omp_get_num_threads();
-#pragma omp for schedule(dynamic, 16)
+#pragma omp for schedule(dynamic, chunk)
     for (int64_t s = 0; s < num_segments; ++s) {
       if (mine != ORACLE_OK) continue;
       int64_t a = offsets[s], m = offsets[s + 1] - offsets[s];
