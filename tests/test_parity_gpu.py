@@ -343,6 +343,16 @@ def test_batched_long_queue_key_widths(classes, max_len):
     check_batched(p, l, off, classes, f"long-keys-{classes}-{max_len}")
 
 
+def test_batched_long_queue_tile_boundaries():
+    # queues ending on and just past 8,192-request tile edges; 32 tiles (the
+    # most whose digit offsets are one work item) and 33 (scanned in column
+    # items of 16 digits); 600 tiles, past one 512-tile block of a column item
+    t = 8192
+    sizes = [2 * t, 2 * t + 1, 3 * t, 3 * t + 1, 32 * t, 32 * t + 1, 5, 600 * t - 3]
+    p, l, off = fuzz_segments(sizes, seed=71, classes=6, max_len=50000)
+    check_batched(p, l, off, 6, "long-tile-edges")
+
+
 def test_batched_long_queue_key_and_index_beyond_64_bits():
     # 39 key bits (256 classes, lengths over the whole int32 range) and a
     # queue of more than 2^25 requests (26 index bits): the elements between
